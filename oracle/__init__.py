@@ -1,0 +1,269 @@
+"""CPU oracle for the MoE layer over a GPU expert cache.  TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg use this module; the
+product library never imports or calls it.  It shares no code with the HIP path.
+
+It is a plain, slow, obviously correct restatement of what one MoE layer computes when only
+the experts resident in the GPU expert cache are evaluated (Section 3.2 and Section 4.1 of the
+paper: the router and the cache lookup run on the GPU, resident experts execute there, the
+misses go elsewhere, and the partial sums from both sides add up to the exact layer output).
+Every floating-point step runs in float64 on exactly decoded weights; results are cast to
+float32 at the end.
+
+The paper does not print the layer's formulas (Section 2 only says a layer holds E experts and
+routes each token to k of them).  The readings taken here:
+
+* top-k: the k largest raw float32 logits of the token, ordered by (logit descending, expert id
+  ascending); -0.0 counts as +0.0.  Both gating functions are strictly increasing, so selecting
+  on logits equals selecting on scores.
+* gates: softmax mode, g_j = exp(l_j - l_max) / sum_i exp(l_i - l_max) over the k selected
+  (a softmax over all E renormalised over the k); sigmoid mode, g_j = s_j / sum_i s_i with
+  s = 1/(1+exp(-l)).  No routed scaling factor, no group-limited routing, no bias correction.
+* hit/miss: pair (t, j) is a hit iff its expert maps to a valid slot: 0 <= slot < n_slots, the
+  slot is not the shared expert's slot, and no other expert maps to the same slot.  Anything
+  else is a miss (Section 4.1 rewrites routed ids into slot ids or a CPU flag).
+* permutation: hit pairs p = t*k + j sorted stably by expert id (so, within one expert, by
+  ascending p); misses likewise.  Offsets are exclusive prefix sums of per-expert counts.
+* expert FFN (SwiGLU): FFN(x) = W2 (silu(W1 x) * (W3 x)), silu(z) = z / (1 + exp(-z)).
+* output: out[t] = sum over hit pairs of g_tj FFN_e(x_t) (+ FFN_shared(x_t), weight 1, when a
+  shared expert is configured); a token without hits and without shared expert gets 0.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+GATE_SOFTMAX = 0
+GATE_SIGMOID = 1
+DT_F32 = 0
+DT_BF16 = 1
+DT_FP8 = 2
+
+STATUS_SLOT_RANGE = 1     # a slot outside [-1, n_slots)
+STATUS_SLOT_DUP = 2       # two experts share one slot
+STATUS_SLOT_SHARED = 4    # a routed expert points at the shared expert's slot
+
+
+# ----------------------------------------------------------------------------------------
+# Weight codecs (exact decodes to float64)
+# ----------------------------------------------------------------------------------------
+
+def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
+    """bfloat16 is the top half of an IEEE float32: widen the bit pattern, then reinterpret."""
+    b = np.ascontiguousarray(bits).view(np.uint16).astype(np.uint32) << np.uint32(16)
+    return b.view(np.float32).astype(np.float64)
+
+
+def e4m3fn_value(code: int) -> float:
+    """OCP FP8 E4M3 ("fn" variant): 1 sign, 4 exponent (bias 7), 3 mantissa bits.
+
+    exponent 0 is subnormal (m/8 * 2^-6); S.1111.111 is NaN; there are no infinities.
+    """
+    s = -1.0 if code & 0x80 else 1.0
+    e = (code >> 3) & 0xF
+    m = code & 0x7
+    if e == 0xF and m == 0x7:
+        return float("nan")
+    if e == 0:
+        return s * (m / 8.0) * 2.0 ** (-6)
+    return s * (1.0 + m / 8.0) * 2.0 ** (e - 7)
+
+
+E4M3FN_TABLE = np.array([e4m3fn_value(c) for c in range(256)], dtype=np.float64)
+
+
+def fp8_blocks_to_f64(codes: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """Dequantise [R][C] e4m3fn codes with one float32 scale per 128x128 block."""
+    r, c = codes.shape
+    v = E4M3FN_TABLE[np.ascontiguousarray(codes).view(np.uint8)]
+    s = np.repeat(np.repeat(scales.astype(np.float64), 128, axis=0), 128, axis=1)
+    assert s.shape == (r, c)
+    return v * s
+
+
+def decode_weight(bank: np.ndarray, w_dtype: int, scales=None) -> np.ndarray:
+    if w_dtype == DT_F32:
+        return bank.astype(np.float64)
+    if w_dtype == DT_BF16:
+        return bf16_bits_to_f64(bank)
+    return fp8_blocks_to_f64(bank, scales)
+
+
+# ----------------------------------------------------------------------------------------
+# Routing: top-k selection and gates
+# ----------------------------------------------------------------------------------------
+
+def route_topk(logits: np.ndarray, k: int) -> np.ndarray:
+    """[T][E] float32 -> [T][k] int32 expert ids, ordered by (logit desc, id asc)."""
+    logits = np.asarray(logits, dtype=np.float32)
+    T, E = logits.shape
+    ids = np.zeros((T, k), dtype=np.int32)
+    for t in range(T):
+        row = logits[t].copy()
+        row[row == 0] = 0.0                       # -0.0 -> +0.0
+        order = np.argsort(-row, kind="stable")   # stable: equal logits keep ascending id
+        ids[t] = order[:k]
+    return ids
+
+
+def gate_weights(logits: np.ndarray, ids: np.ndarray, gating: int) -> np.ndarray:
+    """Renormalised gates of the selected experts, float64 [T][k]."""
+    T, k = ids.shape
+    g = np.zeros((T, k), dtype=np.float64)
+    for t in range(T):
+        l = logits[t, ids[t]].astype(np.float64)
+        if gating == GATE_SOFTMAX:
+            z = np.exp(l - l[0])                  # l[0] is the largest selected logit
+        elif gating == GATE_SIGMOID:
+            z = 1.0 / (1.0 + np.exp(-l))
+        else:
+            raise ValueError("unknown gating")
+        g[t] = z / z.sum()
+    return g
+
+
+# ----------------------------------------------------------------------------------------
+# Classification against the slot table and the expert-sorted permutation
+# ----------------------------------------------------------------------------------------
+
+def effective_slots(slot_table: np.ndarray, n_slots: int, shared_slot: int):
+    """Valid slot per expert (-1 if the expert is not usable from the cache) and a status word."""
+    st = np.asarray(slot_table, dtype=np.int64)
+    E = st.shape[0]
+    eff = np.full(E, -1, dtype=np.int32)
+    status = 0
+    for e in range(E):
+        s = int(st[e])
+        if s == -1:
+            continue
+        if s < -1 or s >= n_slots:
+            status |= STATUS_SLOT_RANGE
+            continue
+        if shared_slot >= 0 and s == shared_slot:
+            status |= STATUS_SLOT_SHARED
+            continue
+        if any(int(st[o]) == s for o in range(E) if o != e):
+            status |= STATUS_SLOT_DUP
+            continue
+        eff[e] = s
+    return eff, status
+
+
+def partition(ids: np.ndarray, eff_slot: np.ndarray, n_experts: int):
+    """Hit/miss lists of pair indices p = t*k + j, each stably sorted by expert id."""
+    T, k = ids.shape
+    pairs = [(int(ids[t, j]), t * k + j) for t in range(T) for j in range(k)]
+    hits = [(e, p) for (e, p) in pairs if eff_slot[e] >= 0]
+    misses = [(e, p) for (e, p) in pairs if eff_slot[e] < 0]
+    hits.sort(key=lambda ep: ep[0])      # Python's sort is stable
+    misses.sort(key=lambda ep: ep[0])
+    hit_off = np.zeros(n_experts + 1, dtype=np.int32)
+    miss_off = np.zeros(n_experts + 1, dtype=np.int32)
+    for e, _ in hits:
+        hit_off[e + 1] += 1
+    for e, _ in misses:
+        miss_off[e + 1] += 1
+    hit_off = np.cumsum(hit_off).astype(np.int32)
+    miss_off = np.cumsum(miss_off).astype(np.int32)
+    hit_pairs = np.array([p for _, p in hits], dtype=np.int32)
+    miss_pairs = np.array([p for _, p in misses], dtype=np.int32)
+    return hit_pairs, hit_off, miss_pairs, miss_off
+
+
+def route(desc: dict, logits, slot_table) -> dict:
+    """Everything the routing side of the layer produces, as numpy arrays."""
+    logits = np.asarray(logits, dtype=np.float32)
+    k, E = desc["top_k"], desc["n_experts"]
+    ids = route_topk(logits, k)
+    gates = gate_weights(logits, ids, desc["gating"])
+    eff, status = effective_slots(np.asarray(slot_table), desc["n_slots"], desc["shared_slot"])
+    slots = eff[ids] if ids.size else np.zeros(ids.shape, np.int32)
+    hit_pairs, hit_off, miss_pairs, miss_off = partition(ids, eff, E)
+    m_unique = int(np.count_nonzero(miss_off[1:] > miss_off[:-1]))
+    return dict(topk_ids=ids, topk_w=gates, topk_slot=slots.astype(np.int32), eff_slot=eff,
+                hit_pairs=hit_pairs, hit_off=hit_off, miss_pairs=miss_pairs, miss_off=miss_off,
+                n_hit=len(hit_pairs), n_miss=len(miss_pairs), m_unique_miss=m_unique,
+                status=status)
+
+
+# ----------------------------------------------------------------------------------------
+# Expert evaluation and the partial layer output
+# ----------------------------------------------------------------------------------------
+
+def silu(z: np.ndarray) -> np.ndarray:
+    return z / (1.0 + np.exp(-z))
+
+
+def expert_ffn(x: np.ndarray, w1: np.ndarray, w3: np.ndarray, w2: np.ndarray) -> np.ndarray:
+    """SwiGLU expert on rows of x: [n][H] -> [n][H], all float64."""
+    return (silu(x @ w1.T) * (x @ w3.T)) @ w2.T
+
+
+def expert_weights(banks: dict, desc: dict, slot: int):
+    """Decoded (W1, W3, W2) of the expert stored in bank row ``slot``."""
+    I = desc["inter"]
+    wd = desc["w_dtype"]
+    s13 = banks.get("s13")
+    s2 = banks.get("s2")
+    w13 = decode_weight(banks["w13"][slot], wd, None if s13 is None else s13[slot])
+    w2 = decode_weight(banks["w2"][slot], wd, None if s2 is None else s2[slot])
+    return w13[:I], w13[I:], w2
+
+
+def decode_x(x: np.ndarray, x_dtype: int) -> np.ndarray:
+    if x_dtype == DT_F32:
+        return np.asarray(x, dtype=np.float64)
+    return bf16_bits_to_f64(x)
+
+
+def moe_partial(desc: dict, banks: dict, logits, slot_table, x, tokens=None):
+    """Partial MoE output over cache-resident experts.
+
+    desc   : hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot
+    banks  : w13 [n_slots][2I][H], w2 [n_slots][H][I] (float32 arrays, bf16 bit patterns as
+             uint16, or fp8 codes as uint8) and for fp8 s13, s2 block scales
+    logits : [T][E] float32; slot_table : [E] int32; x : [T][H] (float32 or bf16 bits as uint16)
+    tokens : optional list of token indices; only those rows are evaluated (others stay 0)
+
+    Returns (out [T][H] float32, routing dict from ``route``).
+    """
+    r = route(desc, logits, slot_table)
+    T = np.asarray(logits).shape[0]
+    H, k = desc["hidden"], desc["top_k"]
+    want = np.ones(T, dtype=bool) if tokens is None else np.isin(np.arange(T), tokens)
+    acc = np.zeros((T, H), dtype=np.float64)
+    # group the wanted hit pairs by expert and run each expert once over its tokens
+    for e in range(desc["n_experts"]):
+        lo, hi = r["hit_off"][e], r["hit_off"][e + 1]
+        if hi == lo:
+            continue
+        ps = [int(p) for p in r["hit_pairs"][lo:hi] if want[int(p) // k]]
+        if not ps:
+            continue
+        ts = [p // k for p in ps]
+        w1, w3, w2 = expert_weights(banks, desc, int(r["eff_slot"][e]))
+        y = expert_ffn(decode_x(x[ts], desc["x_dtype"]), w1, w3, w2)
+        for i, p in enumerate(ps):
+            acc[p // k] += r["topk_w"][p // k, p % k] * y[i]
+    if desc["shared_slot"] >= 0:
+        ts = [t for t in range(T) if want[t]]
+        if ts:
+            w1, w3, w2 = expert_weights(banks, desc, desc["shared_slot"])
+            acc[ts] += expert_ffn(decode_x(x[ts], desc["x_dtype"]), w1, w3, w2)
+    return acc.astype(np.float32), r
+
+
+# ----------------------------------------------------------------------------------------
+# Error metric used by the parity tests
+# ----------------------------------------------------------------------------------------
+
+def max_rel_err(got: np.ndarray, ref: np.ndarray) -> float:
+    """max |got - ref| / max(|ref|, rms of ref's row), over all elements."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    if ref.size == 0:
+        return 0.0
+    rms = np.sqrt(np.mean(ref * ref, axis=-1, keepdims=True))
+    den = np.maximum(np.abs(ref), rms)
+    num = np.abs(got - ref)
+    rel = np.where(den > 0, num / np.where(den > 0, den, 1.0), np.where(num > 0, np.inf, 0.0))
+    return float(rel.max())

@@ -1,0 +1,330 @@
+"""Pins for the CPU oracle: checks against hand-worked values, closed forms, library routines,
+brute force and the invariants the paper's exact-merge claim implies.  CPU only."""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+
+import oracle
+import workloads
+from tests._util import decode_bank_torch, oracle_inputs
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+# ---------------------------------------------------------------- weight codecs
+
+def test_e4m3fn_table_matches_torch_for_all_256_codes():
+    codes = torch.arange(256, dtype=torch.int32).to(torch.uint8)
+    ref = codes.view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    ours = oracle.E4M3FN_TABLE
+    nan = np.isnan(ref)
+    assert nan.sum() == 2 and np.array_equal(nan, np.isnan(ours))
+    assert np.array_equal(ref[~nan], ours[~nan])
+    assert ours[0x7E] == 448.0 and ours[0x01] == 2.0 ** -9 and ours[0x80] == 0.0
+
+
+def test_bf16_decode_matches_torch():
+    g = torch.Generator().manual_seed(5)
+    x = torch.randn(4096, generator=g) * torch.exp(torch.randn(4096, generator=g) * 20)
+    x = torch.cat([x, torch.tensor([0.0, -0.0, 1e-40, -3.0e38, 1.0])]).to(torch.bfloat16)
+    bits = x.view(torch.int16).numpy().view(np.uint16)
+    ref = x.to(torch.float64).numpy()
+    assert np.array_equal(oracle.bf16_bits_to_f64(bits), ref)
+
+
+def test_fp8_block_scales_index_by_row_and_column_block():
+    g = torch.Generator().manual_seed(1)
+    codes = torch.randint(0, 0x7E, (256, 384), generator=g, dtype=torch.int32).to(torch.uint8)
+    scales = torch.tensor([[1.0, 2.0, 4.0], [8.0, 16.0, 32.0]])
+    dec = oracle.fp8_blocks_to_f64(codes.numpy(), scales.numpy())
+    for r, c in [(0, 0), (127, 127), (128, 0), (0, 128), (255, 383), (130, 260), (5, 300)]:
+        want = oracle.e4m3fn_value(int(codes[r, c])) * float(scales[r // 128, c // 128])
+        assert dec[r, c] == want
+    assert np.array_equal(dec, decode_bank_torch(codes, 2, scales).numpy())
+
+
+# ---------------------------------------------------------------- top-k routing
+
+def _brute_topk(row, k):
+    """Expert e is at position beats(e) if beats(e) < k, where beats counts the experts that
+    outrank it: a strictly larger logit, or an equal one (with -0 == +0) and a lower id."""
+    E = len(row)
+    out = [None] * k
+    for e in range(E):
+        beats = sum(1 for o in range(E) if row[o] > row[e] or (row[o] == row[e] and o < e))
+        if beats < k:
+            out[beats] = e
+    return out
+
+
+@pytest.mark.parametrize("seed,E,k,ties", [(0, 8, 2, False), (1, 16, 1, False), (2, 16, 16, True),
+                                           (3, 33, 7, True), (4, 256, 8, True), (5, 128, 8, False)])
+def test_topk_matches_brute_force(seed, E, k, ties):
+    lay = workloads.random_layer(seed, hidden=128, inter=128, n_experts=E, top_k=k, tokens=9,
+                                 tie_logits=ties)
+    logits = lay.logits.numpy()
+    ids = oracle.route_topk(logits, k)
+    for t in range(logits.shape[0]):
+        assert ids[t].tolist() == _brute_topk([float(v) for v in logits[t]], k)
+
+
+def test_topk_ties_and_signed_zero():
+    row = np.array([[0.0, -0.0, 1.0, 1.0, -0.0, 0.0, -1.0, 1.0]], dtype=np.float32)
+    assert oracle.route_topk(row, 8)[0].tolist() == [2, 3, 7, 0, 1, 4, 5, 6]
+    assert oracle.route_topk(row, 4)[0].tolist() == [2, 3, 7, 0]
+    row = np.array([[-0.0, 0.0]], dtype=np.float32)
+    assert oracle.route_topk(row, 1)[0].tolist() == [0]
+
+
+# ---------------------------------------------------------------- gates
+
+@pytest.mark.parametrize("gating", [oracle.GATE_SOFTMAX, oracle.GATE_SIGMOID])
+def test_gates_against_library_closed_forms(gating):
+    g = torch.Generator().manual_seed(11)
+    logits = (torch.randn(20, 64, generator=g) * 3).numpy()
+    ids = oracle.route_topk(logits, 6)
+    w = oracle.gate_weights(logits, ids, gating)
+    assert np.all(np.abs(w.sum(axis=1) - 1.0) <= 1e-12)
+    l64 = logits.astype(np.float64)
+    if gating == oracle.GATE_SOFTMAX:
+        full = scipy.special.softmax(l64, axis=1)      # softmax over all E experts
+    else:
+        full = scipy.special.expit(l64)
+    sel = np.take_along_axis(full, ids.astype(np.int64), axis=1)
+    np.testing.assert_allclose(w, sel / sel.sum(axis=1, keepdims=True), rtol=1e-12, atol=0)
+    assert np.all(np.diff(w, axis=1) <= 0)             # ordered by logit
+
+
+def test_gates_special_cases():
+    logits = np.array([[0.3, -2.0, 5.0, 0.3]], dtype=np.float32)
+    for gating in (0, 1):
+        assert oracle.gate_weights(logits, oracle.route_topk(logits, 1), gating)[0, 0] == 1.0
+    eq = np.full((1, 6), 0.25, dtype=np.float32)
+    for gating in (0, 1):
+        w = oracle.gate_weights(eq, oracle.route_topk(eq, 4), gating)
+        np.testing.assert_allclose(w, 0.25, rtol=1e-15)
+
+
+# ---------------------------------------------------------------- slot validation and partition
+
+def test_effective_slots_errors():
+    st = np.array([0, 1, 1, 7, -1, -5, 3, 2], dtype=np.int32)
+    eff, status = oracle.effective_slots(st, n_slots=4, shared_slot=3)
+    assert eff.tolist() == [0, -1, -1, -1, -1, -1, -1, 2]
+    assert status == oracle.STATUS_SLOT_DUP | oracle.STATUS_SLOT_RANGE | oracle.STATUS_SLOT_SHARED
+    eff, status = oracle.effective_slots(np.array([2, -1, 0], np.int32), 3, -1)
+    assert eff.tolist() == [2, -1, 0] and status == 0
+
+
+@pytest.mark.parametrize("seed,E,k,T,n_res", [(0, 8, 2, 16, 4), (1, 16, 4, 9, 0), (2, 16, 4, 9, 16),
+                                              (3, 64, 8, 33, 20), (4, 16, 16, 5, 7), (5, 8, 1, 1, 3)])
+def test_partition_brute_force(seed, E, k, T, n_res):
+    lay = workloads.random_layer(seed, hidden=128, inter=128, n_experts=E, top_k=k, tokens=T,
+                                 n_resident=n_res, tie_logits=seed % 2 == 1)
+    desc, banks, logits, st, x = oracle_inputs(lay)
+    r = oracle.route(desc, logits, st)
+    ids = r["topk_ids"]
+    resident = {e for e in range(E) if st[e] >= 0}
+    all_pairs = set(range(T * k))
+    hit, miss = set(r["hit_pairs"].tolist()), set(r["miss_pairs"].tolist())
+    assert hit | miss == all_pairs and not (hit & miss)
+    assert len(hit) == len(r["hit_pairs"]) and len(miss) == len(r["miss_pairs"])
+    assert hit == {p for p in all_pairs if ids[p // k, p % k] in resident}
+    # canonical order: expert id ascending, then pair index ascending
+    for lst in (r["hit_pairs"], r["miss_pairs"]):
+        keys = [(int(ids[p // k, p % k]), int(p)) for p in lst]
+        assert keys == sorted(keys)
+    for lst, off in ((r["hit_pairs"], r["hit_off"]), (r["miss_pairs"], r["miss_off"])):
+        for e in range(E):
+            seg = lst[off[e]:off[e + 1]]
+            assert all(ids[p // k, p % k] == e for p in seg)
+        assert off[0] == 0 and off[E] == len(lst)
+    assert r["m_unique_miss"] == len({int(ids[p // k, p % k]) for p in miss})
+    slots = r["topk_slot"]
+    for p in all_pairs:
+        e = int(ids[p // k, p % k])
+        assert slots[p // k, p % k] == (st[e] if e in resident else -1)
+    if n_res == 0:
+        assert len(hit) == 0
+    if n_res == E:
+        assert len(miss) == 0
+
+
+def test_fig2_partition_counts():
+    """Fig. 2 decode example: 12 routed pairs, 8 hits, m = 4 unique misses."""
+    with open(os.path.join(GOLDEN, "fig2_partition.json")) as f:
+        g = json.load(f)
+    E, k = g["n_experts"], g["top_k"]
+    logits = np.full((3, E), -10.0, dtype=np.float32)
+    for t, order in enumerate(g["logits_rank_order"]):
+        for j, e in enumerate(order):
+            logits[t, e] = 5.0 - j
+    desc = dict(n_experts=E, top_k=k, gating=0, n_slots=g["n_slots"], shared_slot=-1)
+    r = oracle.route(desc, logits, np.array(g["slot_table"], np.int32))
+    ex = g["expect"]
+    assert r["n_hit"] == ex["n_hit"] and r["n_miss"] == ex["n_miss"]
+    assert r["m_unique_miss"] == ex["m_unique_miss"]
+    assert r["hit_pairs"].tolist() == ex["hit_pairs"]
+    assert r["miss_pairs"].tolist() == ex["miss_pairs"]
+
+
+# ---------------------------------------------------------------- expert FFN and layer output
+
+def test_worked_example_golden():
+    with open(os.path.join(GOLDEN, "worked_example.json")) as f:
+        g = json.load(f)
+    H, I, E = g["hidden"], g["inter"], g["n_experts"]
+    w13 = np.concatenate([np.array(g["w1"]), np.array(g["w3"])], axis=1)   # [E][2I][H]
+    banks = {"w13": w13, "w2": np.array(g["w2"])}
+    for case in g["cases"]:
+        desc = dict(hidden=H, inter=I, n_experts=E, top_k=g["top_k"], gating=case["gating"],
+                    w_dtype=oracle.DT_F32, x_dtype=oracle.DT_F32, n_slots=3, shared_slot=-1)
+        out, r = oracle.moe_partial(desc, banks, np.array(g["logits"], np.float32),
+                                    np.array(case["slot_table"], np.int32),
+                                    np.array(g["x"], np.float32))
+        assert r["topk_ids"].tolist() == case["topk_ids"]
+        np.testing.assert_allclose(r["topk_w"], case["topk_w"], rtol=1e-7)
+        np.testing.assert_allclose(out, np.array(case["out"], np.float32), rtol=1e-6, atol=0)
+
+
+def test_swiglu_identity_weights():
+    """W1 = W3 = W2 = identity, one expert, k = 1: the layer returns silu(x) * x."""
+    H = 8
+    eye = np.eye(H, dtype=np.float32)
+    banks = {"w13": np.concatenate([eye, eye])[None], "w2": eye[None]}
+    desc = dict(hidden=H, inter=H, n_experts=1, top_k=1, gating=0, w_dtype=0, x_dtype=0,
+                n_slots=1, shared_slot=-1)
+    x = np.linspace(-6, 6, 5 * H, dtype=np.float32).reshape(5, H)
+    out, _ = oracle.moe_partial(desc, banks, np.zeros((5, 1), np.float32), np.array([0], np.int32), x)
+    x64 = x.astype(np.float64)
+    np.testing.assert_allclose(out, x64 * x64 * scipy.special.expit(x64), rtol=1e-6, atol=1e-30)
+
+
+def _dense_reference(lay, resident_mask):
+    """Dense masked MoE in torch float64: every expert on every token, gate zero unless the
+    expert is among the token's top-k AND resident.  Independent of the oracle's grouping."""
+    T, E, H, I, k = lay.tokens, lay.n_experts, lay.hidden, lay.inter, lay.top_k
+    l = lay.logits.double()
+    score = torch.softmax(l, dim=1) if lay.gating == 0 else torch.sigmoid(l)
+    sel = torch.zeros(T, E, dtype=torch.bool)
+    for t in range(T):                          # inputs are tie-free, so torch.topk is exact
+        sel[t, torch.topk(l[t], k).indices] = True
+    gate = torch.where(sel, score, torch.zeros_like(score))
+    gate = gate / gate.sum(dim=1, keepdim=True)
+    gate = gate * torch.as_tensor(resident_mask, dtype=torch.float64)[None, :]
+    xd = lay.x.double()
+    out = torch.zeros(T, H, dtype=torch.float64)
+    for e in range(E):
+        slot = int(lay.slot_table_full[e])
+        w13 = decode_bank_torch(lay.w13[slot], lay.w_dtype, None if lay.s13 is None else lay.s13[slot])
+        w2 = decode_bank_torch(lay.w2[slot], lay.w_dtype, None if lay.s2 is None else lay.s2[slot])
+        a = torch.einsum("th,ih->ti", xd, w13[:I])
+        b = torch.einsum("th,ih->ti", xd, w13[I:])
+        y = torch.einsum("ti,hi->th", torch.nn.functional.silu(a) * b, w2)
+        out += gate[:, e:e + 1] * y
+    if lay.shared_slot >= 0:
+        s = lay.shared_slot
+        w13 = decode_bank_torch(lay.w13[s], lay.w_dtype, None if lay.s13 is None else lay.s13[s])
+        w2 = decode_bank_torch(lay.w2[s], lay.w_dtype, None if lay.s2 is None else lay.s2[s])
+        h = torch.nn.functional.silu(xd @ w13[:I].T) * (xd @ w13[I:].T)
+        out += h @ w2.T
+    return out.numpy()
+
+
+def _full_pool_layer(seed, w_dtype, gating, shared=False, E=8, k=3, T=12):
+    lay = workloads.random_layer(seed, hidden=128, inter=256, n_experts=E, top_k=k, tokens=T,
+                                 gating=gating, w_dtype=w_dtype, n_resident=E, shared=shared)
+    lay.slot_table_full = lay.slot_table.clone()
+    return lay
+
+
+def _with_residency(lay, mask):
+    st = lay.slot_table_full.clone()
+    st[~torch.as_tensor(mask, dtype=torch.bool)] = -1
+    lay.slot_table = st
+    return lay
+
+
+@pytest.mark.parametrize("w_dtype,gating,shared", [(0, 0, False), (1, 0, False), (1, 1, False),
+                                                   (2, 1, True), (2, 0, False)])
+def test_partial_output_matches_dense_masked_evaluation(w_dtype, gating, shared):
+    lay = _full_pool_layer(3 + w_dtype, w_dtype, gating, shared)
+    g = torch.Generator().manual_seed(9)
+    for trial in range(3):
+        mask = (torch.rand(lay.n_experts, generator=g) < 0.5).numpy()
+        if trial == 1:
+            mask[:] = True                        # full residency: the plain dense MoE output
+        _with_residency(lay, mask)
+        out, _ = oracle.moe_partial(*oracle_inputs(lay))
+        ref = _dense_reference(lay, mask)
+        np.testing.assert_allclose(out, ref.astype(np.float32), rtol=2e-6, atol=1e-7)
+
+
+@pytest.mark.parametrize("w_dtype,shared", [(1, False), (2, True)])
+def test_zero_residency_and_additivity(w_dtype, shared):
+    lay = _full_pool_layer(21, w_dtype, 1, shared, E=8, k=4, T=10)
+    E = lay.n_experts
+    _with_residency(lay, np.zeros(E, bool))
+    out0, r0 = oracle.moe_partial(*oracle_inputs(lay))
+    assert r0["n_hit"] == 0 and r0["n_miss"] == lay.tokens * lay.top_k
+    if not shared:
+        assert np.array_equal(out0, np.zeros_like(out0)) and not np.signbit(out0).any()
+    else:
+        np.testing.assert_allclose(out0, _dense_reference(lay, np.zeros(E)).astype(np.float32),
+                                   rtol=2e-6, atol=1e-7)
+    # exact merge: resident part + non-resident part = whole layer (one shared term only)
+    R = np.array([1, 0, 1, 1, 0, 0, 1, 0], bool)
+    _with_residency(lay, R)
+    a, _ = oracle.moe_partial(*oracle_inputs(lay))
+    _with_residency(lay, ~R)
+    b, _ = oracle.moe_partial(*oracle_inputs(lay))
+    _with_residency(lay, np.ones(E, bool))
+    full, _ = oracle.moe_partial(*oracle_inputs(lay))
+    merged = a.astype(np.float64) + b.astype(np.float64) - (out0.astype(np.float64) if shared else 0)
+    np.testing.assert_allclose(merged, full, rtol=1e-5, atol=1e-6)
+
+
+def test_token_subset_matches_full_rows():
+    lay = workloads.random_layer(31, hidden=128, inter=128, n_experts=16, top_k=4, tokens=20,
+                                 w_dtype=1, n_resident=9, shared=True)
+    full, _ = oracle.moe_partial(*oracle_inputs(lay))
+    sub, _ = oracle.moe_partial(*oracle_inputs(lay), tokens=[0, 7, 19])
+    assert np.array_equal(sub[[0, 7, 19]], full[[0, 7, 19]])
+    assert not sub[[1, 2, 18]].any()
+
+
+def test_max_rel_err_metric():
+    ref = np.array([[1.0, -2.0, 0.0, 4.0], [0.0, 0.0, 0.0, 0.0]])
+    assert oracle.max_rel_err(ref, ref) == 0.0
+    got = ref.copy()
+    got[0, 2] = 0.025                     # row rms = sqrt(21/4) ~ 2.29 is the floor for 0.0
+    assert abs(oracle.max_rel_err(got, ref) - 0.025 / np.sqrt(21 / 4)) < 1e-12
+    got = ref.copy()
+    got[1, 0] = 1e-30                      # an exact-zero row must stay exactly zero
+    assert oracle.max_rel_err(got, ref) == np.inf
+
+
+# ---------------------------------------------------------------- the synthetic configurations
+
+def test_tiny_config_routing_shape():
+    lay = workloads.make_layer("tiny", 16)
+    desc, banks, logits, st, x = oracle_inputs(lay)
+    assert st.tolist() == [0, -1, 1, -1, -1, 2, -1, 3]
+    out, r = oracle.moe_partial(desc, banks, logits, st, x)
+    assert out.shape == (16, 256) and r["n_hit"] + r["n_miss"] == 32
+    rows_without_hits = [t for t in range(16) if all(r["topk_slot"][t] < 0)]
+    assert all(not out[t].any() for t in rows_without_hits)
+
+
+def test_config_residency_counts():
+    from workloads import CONFIGS
+    import math
+    want = {"qwen3_decode": 64, "qwen3_prefill": 96, "dsv3_decode": 64, "dsv3_prefill": 102}
+    for name, n in want.items():
+        cfg = CONFIGS[name]
+        assert int(math.floor(cfg.resident_frac * cfg.n_experts + 1e-9)) == n
