@@ -1,0 +1,182 @@
+/*
+ * ftmoe.h -- C ABI of the MoE layer executed against a GPU expert cache (gfx950 / MI355X).
+ *
+ * What the library computes (FreeToken, Section 3.2 "Decode codesign" and Section 4.1
+ * "CUDA-Graph-compatible LRU cache"): at one MoE layer the router and the cache lookup run on
+ * the GPU; the routed (token, expert) pairs whose expert is resident in a cache slot form the
+ * hit set H and are evaluated on the GPU; the remaining pairs form the miss set M, whose m
+ * distinct experts are served elsewhere (CPU execution or a cache fill).  The GPU's partial
+ * output and the partial output of the misses add up to the exact layer output.
+ *
+ * Layer definition used throughout (the paper states it only in words, Section 2):
+ *   top-k      S_t = the k experts with the largest float32 logit, ordered by (logit desc,
+ *              expert id asc); -0.0 compares equal to +0.0.  Inputs must be finite.
+ *   gates      softmax mode: g_j = exp(l_j - l_max) / sum_{i in S_t} exp(l_i - l_max)
+ *              sigmoid mode: g_j = s_j / sum_{i in S_t} s_i,  s = 1/(1+exp(-l))
+ *   expert     FFN_e(x) = W2_e (silu(W1_e x) * (W3_e x)),  silu(z) = z / (1+exp(-z))
+ *   output     out[t] = sum_{(t,j) in H} g_tj FFN_{e_tj}(x_t)  (+ FFN_shared(x_t) if configured)
+ *
+ * Conventions for every entry point:
+ *   - All array arguments are DEVICE pointers owned by the caller, except where a field says
+ *     host.  The library never allocates, frees or synchronises inside a call; it validates
+ *     the arguments on the host, then enqueues kernels on `stream` (a hipStream_t; NULL means
+ *     the null stream) and returns.
+ *   - Host-checkable errors return a status before anything is enqueued.
+ *   - The library keeps no state between calls and is reentrant; calls that share a
+ *     workspace or output buffers must be ordered by the caller (same stream).
+ *   - Device-detected problems with the slot table (see ft_route_t.counts[3]) cannot be
+ *     returned synchronously; the offending experts are treated as misses instead.
+ */
+#ifndef FTMOE_H
+#define FTMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    FT_OK = 0,
+    FT_ERR_NULL = 1,       /* a required pointer is NULL */
+    FT_ERR_SHAPE = 2,      /* sizes out of the supported range (see ft_moe_desc_t) */
+    FT_ERR_DTYPE = 3,      /* unsupported dtype / gating / mode combination */
+    FT_ERR_CAPACITY = 4,   /* workspace smaller than ft_moe_workspace_bytes(desc, T) */
+    FT_ERR_HIP = 5         /* a HIP runtime call failed while enqueuing */
+} ft_status_t;
+
+enum { FT_GATE_SOFTMAX_TOPK_RENORM = 0, FT_GATE_SIGMOID_TOPK_RENORM = 1 };
+
+enum {
+    FT_DT_F32 = 0,              /* IEEE float32 */
+    FT_DT_BF16 = 1,             /* bfloat16 */
+    FT_DT_FP8E4M3FN_B128 = 2    /* OCP fp8 e4m3fn codes, one float32 scale per 128x128 block */
+};
+
+#define FT_SLOT_MISS (-1)
+
+/* Device status bits reported in ft_route_t.counts[3] (0 = slot table valid). */
+#define FT_DEV_SLOT_RANGE  1    /* slot_table[e] < -1 or >= n_slots: expert treated as miss */
+#define FT_DEV_SLOT_DUP    2    /* two experts share one slot: both treated as misses */
+#define FT_DEV_SLOT_SHARED 4    /* a routed expert points at shared_slot: treated as miss */
+
+/*
+ * Layer description (host struct, read during the call only).
+ *   hidden (H), inter (I): multiples of 128, 128 <= H, I <= 65536.
+ *   n_experts (E): 1..1024 routed experts.   top_k (k): 1..min(E, 64).
+ *   gating: FT_GATE_*.
+ *   w_dtype: FT_DT_F32 with x_dtype FT_DT_F32, or FT_DT_BF16 / FT_DT_FP8E4M3FN_B128 with
+ *            x_dtype FT_DT_BF16 (fp8 weights are dequantised exactly; activations stay bf16).
+ *   n_slots: number of bank rows (cache slots) in the banks, >= 0.
+ *   shared_slot: bank row of an always-resident shared expert with gate 1 for every token,
+ *                or -1 for none.
+ */
+typedef struct {
+    int32_t hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot;
+} ft_moe_desc_t;
+
+/*
+ * Expert banks: one row per cache slot, so bank row s holds the complete expert stored in
+ * slot s (Section 3 "single elastic GPU expert cache", Section 4.2 "expert banks": all banks
+ * share one expert-to-slot mapping, so one slot index addresses every tensor of an expert and
+ * a cache fill is a plain row copy, never a relayout).  Device pointers, caller-owned,
+ * row-major:
+ *   w13 [n_slots][2I][H]  rows 0..I-1 = gate projection W1, rows I..2I-1 = up projection W3
+ *   w2  [n_slots][H][I]   down projection
+ *   s13 [n_slots][2I/128][H/128], s2 [n_slots][H/128][I/128]  float32 block scales (fp8 only,
+ *       NULL otherwise): weight (r, c) = code(r, c) * scale(r/128, c/128).
+ */
+typedef struct {
+    const void *w13;
+    const void *w2;
+    const float *s13;
+    const float *s2;
+} ft_banks_t;
+
+/*
+ * Routing outputs (device pointers, caller-owned; T tokens, k = top_k, E = n_experts).
+ * Section 4.1 keeps all routing-dependent control on the GPU as fixed-shape buffers with
+ * device-resident valid counts; these are those buffers.
+ *   topk_ids  [T][k] int32   selected experts, in top-k order
+ *   topk_w    [T][k] float   renormalised gates
+ *   topk_slot [T][k] int32   slot of the expert, or FT_SLOT_MISS
+ *   hit_pairs [T*k]  int32   pair indices p = t*k + j of hits, sorted by (expert id, p);
+ *                            entries past the hit count are -1
+ *   miss_pairs[T*k]  int32   same for misses
+ *   hit_off   [E+1]  int32   hit_pairs[hit_off[e] .. hit_off[e+1]) are expert e's hits
+ *   miss_off  [E+1]  int32   same for misses
+ *   counts    [4]    int32   n_hit, n_miss, m (distinct missing experts), device status bits
+ */
+typedef struct {
+    int32_t *topk_ids;
+    float *topk_w;
+    int32_t *topk_slot;
+    int32_t *hit_pairs;
+    int32_t *miss_pairs;
+    int32_t *hit_off;
+    int32_t *miss_off;
+    int32_t *counts;
+} ft_route_t;
+
+/*
+ * Host-side destination of the miss list (pinned host memory, caller-owned, capacity for T
+ * tokens): counts[4], miss_pairs[T*k], miss_off[E+1], topk_ids[T*k], topk_w[T*k].
+ */
+typedef struct {
+    int32_t *counts;
+    int32_t *miss_pairs;
+    int32_t *miss_off;
+    int32_t *topk_ids;
+    float *topk_w;
+} ft_host_miss_t;
+
+/* Bytes of device workspace the calls need for up to max_tokens tokens; 0 if desc is invalid. */
+size_t ft_moe_workspace_bytes(const ft_moe_desc_t *desc, int32_t max_tokens);
+
+/*
+ * Router, hit/miss classification and the expert-sorted permutation only (Section 3.2: the
+ * router and cache lookup run on the GPU and identify the hits; Section 4.1: routed logical ids
+ * are rewritten into slot ids or a CPU-assignment flag).
+ *   logits     [T][E] float32 device
+ *   slot_table [E] int32 device: slot of expert e, or -1 if not resident
+ *   T >= 0 (T == 0 enqueues nothing and returns FT_OK)
+ *   route      outputs as documented in ft_route_t
+ *   ws, ws_bytes  device workspace of at least ft_moe_workspace_bytes(desc, T) bytes
+ */
+ft_status_t ft_route_only(const ft_moe_desc_t *desc, const float *logits, const int32_t *slot_table,
+                          int32_t T, const ft_route_t *route, void *ws, size_t ws_bytes,
+                          void *stream);
+
+/*
+ * The whole GPU side of one MoE layer: routing as in ft_route_only, then the grouped SwiGLU
+ * expert FFN over the hit experts' slot-resident weights (plus the shared expert), then the
+ * gate-weighted combine (Section 3.2: grouped evaluation of the GPU execution set; the GPU and
+ * CPU partial sums merge exactly).
+ *   x           [T][H] device, x_dtype
+ *   out_partial [T][H] float32 device, fully overwritten; a token with no hit (and no shared
+ *               expert) gets exact zeros.
+ */
+ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
+                           const int32_t *slot_table, const void *x, int32_t T,
+                           float *out_partial, const ft_route_t *route, void *ws,
+                           size_t ws_bytes, void *stream);
+
+/*
+ * Enqueue asynchronous device-to-host copies of the miss list (counts, miss_pairs, miss_off,
+ * topk_ids, topk_w) into pinned host buffers, full fixed capacity, so no host synchronisation
+ * is needed to size them (Section 3.2: the misses are executed on the CPU or filled into the
+ * cache; Section 4.1: fixed-shape buffers with device-resident counts).  The host may read
+ * them after synchronising with `stream`.
+ */
+ft_status_t ft_miss_list_to_host(const ft_moe_desc_t *desc, const ft_route_t *route, int32_t T,
+                                 const ft_host_miss_t *host, void *stream);
+
+/* Static string for a status code. */
+const char *ft_status_string(ft_status_t status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FTMOE_H */

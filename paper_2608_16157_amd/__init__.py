@@ -1,0 +1,207 @@
+"""Python binding of libftmoe: the MoE layer executed against a GPU expert cache on gfx950.
+
+Argument marshalling only.  Every step of the layer runs in the HIP kernels of
+``libftmoe.so``; torch provides device memory and streams.  The entry points keep the names
+of the C ABI declared in ``include/ftmoe.h``:
+
+    ft_moe_workspace_bytes(desc, max_tokens) -> int
+    ft_route_only(desc, logits, slot_table, T, route, ws, stream=None)
+    ft_moe_forward(desc, banks, logits, slot_table, x, T, out_partial, route, ws, stream=None)
+    ft_miss_list_to_host(desc, route, T, host, stream=None)
+    ft_status_string(status) -> str
+
+``desc`` is a dict with the ft_moe_desc_t fields; ``route`` a RouteBuffers; ``banks`` a dict
+with w13, w2 (and s13, s2 for fp8) device tensors; everything else device tensors.  A non-OK
+status raises FtError.  If the library is not built, importing works but every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libftmoe.so")
+
+FT_OK, FT_ERR_NULL, FT_ERR_SHAPE, FT_ERR_DTYPE, FT_ERR_CAPACITY, FT_ERR_HIP = range(6)
+FT_GATE_SOFTMAX_TOPK_RENORM, FT_GATE_SIGMOID_TOPK_RENORM = 0, 1
+FT_DT_F32, FT_DT_BF16, FT_DT_FP8E4M3FN_B128 = 0, 1, 2
+FT_SLOT_MISS = -1
+FT_DEV_SLOT_RANGE, FT_DEV_SLOT_DUP, FT_DEV_SLOT_SHARED = 1, 2, 4
+
+EXPORTED = ("ft_moe_workspace_bytes", "ft_route_only", "ft_moe_forward",
+            "ft_miss_list_to_host", "ft_status_string")
+
+
+class FtError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {_status_text(status)}")
+
+
+class ft_moe_desc_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("hidden", "inter", "n_experts", "top_k", "gating",
+                                              "w_dtype", "x_dtype", "n_slots", "shared_slot")]
+
+
+class ft_banks_t(ctypes.Structure):
+    _fields_ = [("w13", ctypes.c_void_p), ("w2", ctypes.c_void_p), ("s13", ctypes.c_void_p),
+                ("s2", ctypes.c_void_p)]
+
+
+class ft_route_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("topk_ids", "topk_w", "topk_slot", "hit_pairs",
+                                               "miss_pairs", "hit_off", "miss_off", "counts")]
+
+
+class ft_host_miss_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("counts", "miss_pairs", "miss_off", "topk_ids",
+                                               "topk_w")]
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libftmoe.so once; raise if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libftmoe.so not built ({path}); run __graft_entry__.build() or "
+                           "python paper_2608_16157_amd/build.py")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    lib.ft_moe_workspace_bytes.restype = ctypes.c_size_t
+    lib.ft_moe_workspace_bytes.argtypes = [P(ft_moe_desc_t), ctypes.c_int32]
+    lib.ft_route_only.restype = ctypes.c_int
+    lib.ft_route_only.argtypes = [P(ft_moe_desc_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                  P(ft_route_t), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.ft_moe_forward.restype = ctypes.c_int
+    lib.ft_moe_forward.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), ctypes.c_void_p, ctypes.c_void_p,
+                                   ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, P(ft_route_t),
+                                   ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.ft_miss_list_to_host.restype = ctypes.c_int
+    lib.ft_miss_list_to_host.argtypes = [P(ft_moe_desc_t), P(ft_route_t), ctypes.c_int32,
+                                         P(ft_host_miss_t), ctypes.c_void_p]
+    lib.ft_status_string.restype = ctypes.c_char_p
+    lib.ft_status_string.argtypes = [ctypes.c_int]
+    _lib = lib
+    return lib
+
+
+def _status_text(status: int) -> str:
+    try:
+        return load().ft_status_string(status).decode()
+    except RuntimeError:
+        return f"status {status}"
+
+
+def ft_status_string(status: int) -> str:
+    return load().ft_status_string(status).decode()
+
+
+# ------------------------------------------------------------------------------ marshalling
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libftmoe must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def make_desc(d: dict) -> ft_moe_desc_t:
+    return ft_moe_desc_t(**{f: int(d[f]) for f, _ in ft_moe_desc_t._fields_})
+
+
+class RouteBuffers:
+    """Device tensors behind one ft_route_t, sized for T tokens."""
+
+    def __init__(self, T: int, top_k: int, n_experts: int, device="cuda"):
+        pk = max(T * top_k, 1)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.T, self.k, self.E = T, top_k, n_experts
+        self.topk_ids = torch.empty(pk, **i32)
+        self.topk_w = torch.empty(pk, dtype=torch.float32, device=device)
+        self.topk_slot = torch.empty(pk, **i32)
+        self.hit_pairs = torch.empty(pk, **i32)
+        self.miss_pairs = torch.empty(pk, **i32)
+        self.hit_off = torch.empty(n_experts + 1, **i32)
+        self.miss_off = torch.empty(n_experts + 1, **i32)
+        self.counts = torch.empty(4, **i32)
+
+    def c(self) -> ft_route_t:
+        return ft_route_t(*[_ptr(getattr(self, n)) for n, _ in ft_route_t._fields_])
+
+
+class HostMissBuffers:
+    """Pinned host buffers behind one ft_host_miss_t."""
+
+    def __init__(self, T: int, top_k: int, n_experts: int):
+        pk = max(T * top_k, 1)
+        kw = dict(pin_memory=True)
+        self.counts = torch.empty(4, dtype=torch.int32, **kw)
+        self.miss_pairs = torch.empty(pk, dtype=torch.int32, **kw)
+        self.miss_off = torch.empty(n_experts + 1, dtype=torch.int32, **kw)
+        self.topk_ids = torch.empty(pk, dtype=torch.int32, **kw)
+        self.topk_w = torch.empty(pk, dtype=torch.float32, **kw)
+
+    def c(self) -> ft_host_miss_t:
+        return ft_host_miss_t(*[_ptr(getattr(self, n)) for n, _ in ft_host_miss_t._fields_])
+
+
+def _check(status: int, where: str):
+    if status != FT_OK:
+        raise FtError(status, where)
+
+
+def ft_moe_workspace_bytes(desc: dict, max_tokens: int) -> int:
+    return int(load().ft_moe_workspace_bytes(ctypes.byref(make_desc(desc)), int(max_tokens)))
+
+
+def alloc_workspace(desc: dict, max_tokens: int, device="cuda") -> torch.Tensor:
+    n = ft_moe_workspace_bytes(desc, max_tokens)
+    if n == 0:
+        raise FtError(FT_ERR_SHAPE, "ft_moe_workspace_bytes")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def ft_route_only(desc: dict, logits: torch.Tensor, slot_table: torch.Tensor, T: int,
+                  route: RouteBuffers, ws: torch.Tensor, stream=None) -> None:
+    st = load().ft_route_only(ctypes.byref(make_desc(desc)), _ptr(logits), _ptr(slot_table), int(T),
+                              ctypes.byref(route.c()), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "ft_route_only")
+
+
+def ft_moe_forward(desc: dict, banks: dict, logits: torch.Tensor, slot_table: torch.Tensor,
+                   x: torch.Tensor, T: int, out_partial: torch.Tensor, route: RouteBuffers,
+                   ws: torch.Tensor, stream=None) -> None:
+    b = ft_banks_t(_ptr(banks.get("w13")), _ptr(banks.get("w2")), _ptr(banks.get("s13")),
+                   _ptr(banks.get("s2")))
+    st = load().ft_moe_forward(ctypes.byref(make_desc(desc)), ctypes.byref(b), _ptr(logits),
+                               _ptr(slot_table), _ptr(x), int(T), _ptr(out_partial),
+                               ctypes.byref(route.c()), _ptr(ws), ws.numel(), _stream(stream))
+    _check(st, "ft_moe_forward")
+
+
+def ft_miss_list_to_host(desc: dict, route: RouteBuffers, T: int, host: HostMissBuffers,
+                         stream=None) -> None:
+    st = load().ft_miss_list_to_host(ctypes.byref(make_desc(desc)), ctypes.byref(route.c()), int(T),
+                                     ctypes.byref(host.c()), _stream(stream))
+    _check(st, "ft_miss_list_to_host")
+
+
+def banks_of(layer) -> dict:
+    """The bank tensors of a synthetic layer object (w13, w2, s13, s2 attributes)."""
+    return {"w13": layer.w13, "w2": layer.w2, "s13": layer.s13, "s2": layer.s2}

@@ -1,0 +1,192 @@
+// C ABI entry points of libftmoe: host-side validation, workspace carving, kernel enqueue.
+#include <hip/hip_runtime.h>
+
+#include "ftmoe_internal.h"
+
+using namespace ftmoe;
+
+namespace {
+
+bool desc_ok(const ft_moe_desc_t *d) {
+    if (!d) return false;
+    if (d->hidden < 128 || d->hidden > 65536 || d->hidden % 128) return false;
+    if (d->inter < 128 || d->inter > 65536 || d->inter % 128) return false;
+    if (d->n_experts < 1 || d->n_experts > kMaxExperts) return false;
+    if (d->top_k < 1 || d->top_k > d->n_experts || d->top_k > kMaxTopK) return false;
+    if (d->n_slots < 0) return false;
+    if (d->shared_slot < -1 || d->shared_slot >= d->n_slots) return false;
+    return true;
+}
+
+ft_status_t dtype_status(const ft_moe_desc_t *d) {
+    if (d->gating != FT_GATE_SOFTMAX_TOPK_RENORM && d->gating != FT_GATE_SIGMOID_TOPK_RENORM)
+        return FT_ERR_DTYPE;
+    if (d->w_dtype == FT_DT_F32 && d->x_dtype == FT_DT_F32) return FT_OK;
+    if ((d->w_dtype == FT_DT_BF16 || d->w_dtype == FT_DT_FP8E4M3FN_B128) && d->x_dtype == FT_DT_BF16)
+        return FT_OK;
+    return FT_ERR_DTYPE;
+}
+
+ft_status_t check_common(const ft_moe_desc_t *desc, const float *logits, const int32_t *slot_table,
+                         int32_t T, const ft_route_t *route, void *ws, size_t ws_bytes) {
+    if (!desc || !route) return FT_ERR_NULL;
+    if (!desc_ok(desc)) return FT_ERR_SHAPE;
+    if (ft_status_t s = dtype_status(desc); s != FT_OK) return s;
+    if (T < 0 || T > 1048576) return FT_ERR_SHAPE;
+    if (T == 0) return FT_OK;
+    if (!logits || !slot_table || !ws) return FT_ERR_NULL;
+    if (!route->topk_ids || !route->topk_w || !route->topk_slot || !route->hit_pairs ||
+        !route->miss_pairs || !route->hit_off || !route->miss_off || !route->counts)
+        return FT_ERR_NULL;
+    if (ws_bytes < ft_moe_workspace_bytes(desc, T)) return FT_ERR_CAPACITY;
+    return FT_OK;
+}
+
+WsView carve(const ft_moe_desc_t *d, int T, void *ws) {
+    const WsLayout L = ws_layout(d->n_experts, d->hidden, d->inter, d->top_k, d->w_dtype, T);
+    uint8_t *b = static_cast<uint8_t *>(ws);
+    WsView v;
+    v.eff_slot = reinterpret_cast<int32_t *>(b + L.eff_slot);
+    v.blk_hist = reinterpret_cast<int32_t *>(b + L.blk_hist);
+    v.grp_meta = reinterpret_cast<int32_t *>(b + L.grp_meta);
+    v.grp_slot = reinterpret_cast<int32_t *>(b + L.grp_slot);
+    v.grp_beg = reinterpret_cast<int32_t *>(b + L.grp_beg);
+    v.grp_len = reinterpret_cast<int32_t *>(b + L.grp_len);
+    v.row_tok = reinterpret_cast<int32_t *>(b + L.row_tok);
+    v.row_gate = reinterpret_cast<float *>(b + L.row_gate);
+    v.pair_row = reinterpret_cast<int32_t *>(b + L.pair_row);
+    v.h = b + L.h;
+    v.y = reinterpret_cast<float *>(b + L.y);
+    return v;
+}
+
+RouteOut route_out(const ft_route_t *r) {
+    return RouteOut{r->topk_ids, r->topk_w, r->topk_slot, r->hit_pairs, r->miss_pairs,
+                    r->hit_off, r->miss_off, r->counts};
+}
+
+RouteArgs route_args(const ft_moe_desc_t *d, const float *logits, const int32_t *slot_table, int T,
+                     const ft_route_t *route, const WsView &wv) {
+    RouteArgs a{};
+    a.logits = logits;
+    a.slot_table = slot_table;
+    a.T = T;
+    a.E = d->n_experts;
+    a.k = d->top_k;
+    a.gating = d->gating;
+    a.n_slots = d->n_slots;
+    a.shared_slot = d->shared_slot;
+    int nbits = 1;
+    while ((1 << nbits) < d->n_experts) ++nbits;
+    a.nbits = nbits;
+    a.scan_parts = 1;
+    a.ro = route_out(route);
+    a.wv = wv;
+    return a;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ft_moe_workspace_bytes(const ft_moe_desc_t *desc, int32_t max_tokens) {
+    if (!desc_ok(desc) || max_tokens < 0) return 0;
+    const int T = max_tokens > 0 ? max_tokens : 1;
+    return ws_layout(desc->n_experts, desc->hidden, desc->inter, desc->top_k, desc->w_dtype, T).total;
+}
+
+ft_status_t ft_route_only(const ft_moe_desc_t *desc, const float *logits, const int32_t *slot_table,
+                          int32_t T, const ft_route_t *route, void *ws, size_t ws_bytes,
+                          void *stream) {
+    if (ft_status_t s = check_common(desc, logits, slot_table, T, route, ws, ws_bytes); s != FT_OK)
+        return s;
+    if (T == 0) return FT_OK;
+    const WsView wv = carve(desc, T, ws);
+    const RouteArgs ra = route_args(desc, logits, slot_table, T, route, wv);
+    if (launch_route(ra, static_cast<hipStream_t>(stream)) != hipSuccess) return FT_ERR_HIP;
+    return FT_OK;
+}
+
+ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
+                           const int32_t *slot_table, const void *x, int32_t T,
+                           float *out_partial, const ft_route_t *route, void *ws,
+                           size_t ws_bytes, void *stream) {
+    if (ft_status_t s = check_common(desc, logits, slot_table, T, route, ws, ws_bytes); s != FT_OK)
+        return s;
+    if (!banks) return FT_ERR_NULL;
+    if (T == 0) return FT_OK;
+    if (!x || !out_partial) return FT_ERR_NULL;
+    if (desc->n_slots > 0 && (!banks->w13 || !banks->w2)) return FT_ERR_NULL;
+    if (desc->w_dtype == FT_DT_FP8E4M3FN_B128 && desc->n_slots > 0 && (!banks->s13 || !banks->s2))
+        return FT_ERR_NULL;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const WsView wv = carve(desc, T, ws);
+    const RouteArgs ra = route_args(desc, logits, slot_table, T, route, wv);
+    if (launch_route(ra, s) != hipSuccess) return FT_ERR_HIP;
+
+    ExpertArgs ea{};
+    ea.w13 = banks->w13;
+    ea.w2 = banks->w2;
+    ea.s13 = banks->s13;
+    ea.s2 = banks->s2;
+    ea.x = x;
+    ea.out = out_partial;
+    ea.T = T;
+    ea.H = desc->hidden;
+    ea.I = desc->inter;
+    ea.k = desc->top_k;
+    ea.w_dtype = desc->w_dtype;
+    ea.n_slots = desc->n_slots;
+    ea.shared = desc->shared_slot >= 0 ? 1 : 0;
+    const long routed_slots = desc->n_slots - ea.shared;
+    long mg = desc->n_experts;
+    if (routed_slots < mg) mg = routed_slots;
+    if (static_cast<long>(T) * desc->top_k < mg) mg = static_cast<long>(T) * desc->top_k;
+    ea.max_groups = static_cast<int>(mg) + ea.shared;
+    ea.pair_row = wv.pair_row;
+    ea.ro = ra.ro;
+    ea.wv = wv;
+    if (launch_experts(ea, s) != hipSuccess) return FT_ERR_HIP;
+    return FT_OK;
+}
+
+ft_status_t ft_miss_list_to_host(const ft_moe_desc_t *desc, const ft_route_t *route, int32_t T,
+                                 const ft_host_miss_t *host, void *stream) {
+    if (!desc || !route || !host) return FT_ERR_NULL;
+    if (!desc_ok(desc)) return FT_ERR_SHAPE;
+    if (T < 0) return FT_ERR_SHAPE;
+    if (!host->counts || !host->miss_pairs || !host->miss_off || !host->topk_ids || !host->topk_w)
+        return FT_ERR_NULL;
+    if (!route->counts || !route->miss_pairs || !route->miss_off || !route->topk_ids ||
+        !route->topk_w)
+        return FT_ERR_NULL;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    const size_t pk = static_cast<size_t>(T) * desc->top_k;
+    const hipMemcpyKind d2h = hipMemcpyDeviceToHost;
+    if (hipMemcpyAsync(host->counts, route->counts, 4 * sizeof(int32_t), d2h, s) != hipSuccess)
+        return FT_ERR_HIP;
+    if (hipMemcpyAsync(host->miss_off, route->miss_off, (desc->n_experts + 1) * sizeof(int32_t), d2h,
+                       s) != hipSuccess)
+        return FT_ERR_HIP;
+    if (pk) {
+        if (hipMemcpyAsync(host->miss_pairs, route->miss_pairs, pk * sizeof(int32_t), d2h, s) != hipSuccess ||
+            hipMemcpyAsync(host->topk_ids, route->topk_ids, pk * sizeof(int32_t), d2h, s) != hipSuccess ||
+            hipMemcpyAsync(host->topk_w, route->topk_w, pk * sizeof(float), d2h, s) != hipSuccess)
+            return FT_ERR_HIP;
+    }
+    return FT_OK;
+}
+
+const char *ft_status_string(ft_status_t status) {
+    switch (status) {
+        case FT_OK: return "FT_OK";
+        case FT_ERR_NULL: return "FT_ERR_NULL: a required pointer is NULL";
+        case FT_ERR_SHAPE: return "FT_ERR_SHAPE: sizes out of the supported range";
+        case FT_ERR_DTYPE: return "FT_ERR_DTYPE: unsupported dtype or gating";
+        case FT_ERR_CAPACITY: return "FT_ERR_CAPACITY: workspace too small";
+        case FT_ERR_HIP: return "FT_ERR_HIP: a HIP runtime call failed";
+    }
+    return "unknown status";
+}
+
+}  // extern "C"

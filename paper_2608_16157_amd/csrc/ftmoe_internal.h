@@ -1,0 +1,111 @@
+// Internal host/device interface of libftmoe: argument bundles, workspace layout, launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/ftmoe.h"
+
+namespace ftmoe {
+
+constexpr int kMaxExperts = 1024;
+constexpr int kMaxTopK = 64;
+constexpr int kTokPerBlk = 16;          // tokens per workgroup in the multi-block router
+constexpr int kFusedMaxPairs = 2048;    // T*k handled by the single-workgroup router
+constexpr int kFusedMaxLds = 64 * 1024;
+
+// Routing outputs (the caller's ft_route_t, flattened).
+struct RouteOut {
+    int32_t *topk_ids;
+    float *topk_w;
+    int32_t *topk_slot;
+    int32_t *hit_pairs;
+    int32_t *miss_pairs;
+    int32_t *hit_off;
+    int32_t *miss_off;
+    int32_t *counts;
+};
+
+// Views into the caller's workspace.
+//  rows: the hit list positions 0..n_hit-1 followed by T rows of the shared expert; row r
+//  evaluates token row_tok[r] with gate row_gate[r].  Groups: one per hit expert (ascending
+//  expert id) and then the shared expert; group g covers rows [grp_beg[g], +grp_len[g]) and
+//  reads the weights of bank row grp_slot[g].
+struct WsView {
+    int32_t *eff_slot;   // [E]
+    int32_t *blk_hist;   // [nblk][E]
+    int32_t *grp_meta;   // [4]: G (groups incl. shared), U (hit groups), n_hit, T
+    int32_t *grp_slot;   // [E+1]
+    int32_t *grp_beg;    // [E+1]
+    int32_t *grp_len;    // [E+1]
+    int32_t *row_tok;    // [T*k + T]
+    float *row_gate;     // [T*k + T]
+    int32_t *pair_row;   // [T*k] row of a hit pair, -1 for a miss
+    void *h;             // [T*k + T][I] SwiGLU activations (bf16, or f32 for f32 weights)
+    float *y;            // [T*k + T][H] gate-scaled expert outputs
+};
+
+struct RouteArgs {
+    const float *logits;
+    const int32_t *slot_table;
+    int T, E, k, gating, n_slots, shared_slot, nbits, scan_parts;
+    RouteOut ro;
+    WsView wv;
+};
+
+struct ExpertArgs {
+    const void *w13;
+    const void *w2;
+    const float *s13;
+    const float *s2;
+    const void *x;
+    float *out;
+    int T, H, I, k, w_dtype, n_slots, shared;
+    int max_groups;   // upper bound on groups, known on the host
+    int32_t *pair_row;
+    RouteOut ro;
+    WsView wv;
+};
+
+struct WsLayout {
+    size_t eff_slot, blk_hist, grp_meta, grp_slot, grp_beg, grp_len, row_tok, row_gate, pair_row,
+        h, y, total;
+};
+
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int T) {
+    WsLayout L{};
+    size_t o = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = o;
+        o = align_up(o + bytes, 256);
+        return at;
+    };
+    const size_t nblk = (static_cast<size_t>(T) + kTokPerBlk - 1) / kTokPerBlk;
+    const size_t rows = static_cast<size_t>(T) * k + T;
+    L.eff_slot = take(4u * E);
+    L.blk_hist = take(4u * nblk * E);
+    L.grp_meta = take(16);
+    L.grp_slot = take(4u * (E + 1));
+    L.grp_beg = take(4u * (E + 1));
+    L.grp_len = take(4u * (E + 1));
+    L.row_tok = take(4u * rows);
+    L.row_gate = take(4u * rows);
+    L.pair_row = take(4u * static_cast<size_t>(T) * k);
+    L.h = take(rows * I * (w_dtype == FT_DT_F32 ? 4u : 2u));
+    L.y = take(rows * H * 4u);
+    L.total = o;
+    return L;
+}
+
+inline int fused_route_lds_bytes(int E, int P) {
+    return 4 * (6 * E + 2 + 2 * P + 16 * E + 1);
+}
+inline int scan_route_lds_bytes(int E, int parts) { return 4 * (6 * E + 3 + parts * E); }
+
+hipError_t launch_route(const RouteArgs &a, hipStream_t s);
+hipError_t launch_experts(const ExpertArgs &a, hipStream_t s);
+
+}  // namespace ftmoe

@@ -1,0 +1,105 @@
+"""Host-side checks of the C ABI: the library loads, exports what include/ftmoe.h declares,
+and rejects bad arguments before touching the GPU.  CPU only."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_16157_amd as ftm
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    src = open(os.path.join(ROOT, "include", "ftmoe.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ft_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ftm.load()
+    names = _declared_functions()
+    assert set(names) == set(ftm.EXPORTED)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings():
+    for s in range(6):
+        assert ftm.ft_status_string(s).startswith("FT_")
+    assert ftm.ft_status_string(99) == "unknown status"
+
+
+def _desc(**kw):
+    d = workloads.make_layer("tiny", 4).desc()
+    d.update(kw)
+    return d
+
+
+def test_workspace_bytes():
+    for name, cfg in workloads.CONFIGS.items():
+        d = dict(hidden=cfg.hidden, inter=cfg.inter, n_experts=cfg.n_experts, top_k=cfg.top_k,
+                 gating=cfg.gating, w_dtype=cfg.w_dtype, x_dtype=cfg.x_dtype, n_slots=200,
+                 shared_slot=-1)
+        for T in cfg.tokens:
+            assert ftm.ft_moe_workspace_bytes(d, T) > 0
+        assert ftm.ft_moe_workspace_bytes(d, 64) >= ftm.ft_moe_workspace_bytes(d, 8)
+    assert ftm.ft_moe_workspace_bytes(_desc(hidden=100), 4) == 0
+    assert ftm.ft_moe_workspace_bytes(_desc(top_k=9), 4) == 0       # k > E
+    assert ftm.ft_moe_workspace_bytes(_desc(n_experts=2000, top_k=2), 4) == 0
+    assert ftm.ft_moe_workspace_bytes(_desc(shared_slot=4), 4) == 0  # shared slot outside pool
+    assert ftm.ft_moe_workspace_bytes(_desc(), -1) == 0
+
+
+FAKE = 0x10000  # never dereferenced: every case below fails host validation first
+
+
+def _route_call(desc, T, ws_bytes=1 << 40, logits=FAKE, null_route=False):
+    lib = ftm.load()
+    r = ftm.ft_route_t(*([None] * 8 if null_route else [FAKE] * 8))
+    return lib.ft_route_only(ctypes.byref(ftm.make_desc(desc)), logits, FAKE, T, ctypes.byref(r),
+                             FAKE, ws_bytes, None)
+
+
+
+@pytest.mark.parametrize("desc_kw,T,kw,want", [
+    ({}, 0, {}, ftm.FT_OK),                                    # T == 0 is a no-op
+    ({}, 4, {"logits": None}, ftm.FT_ERR_NULL),
+    ({}, 4, {"null_route": True}, ftm.FT_ERR_NULL),
+    ({"hidden": 200}, 4, {}, ftm.FT_ERR_SHAPE),
+    ({}, -1, {}, ftm.FT_ERR_SHAPE),
+    ({"gating": 7}, 4, {}, ftm.FT_ERR_DTYPE),
+    ({"w_dtype": 1, "x_dtype": 0}, 4, {}, ftm.FT_ERR_DTYPE),   # bf16 weights need bf16 x
+    ({"w_dtype": 0, "x_dtype": 1}, 4, {}, ftm.FT_ERR_DTYPE),
+    ({}, 4, {"ws_bytes": 64}, ftm.FT_ERR_CAPACITY),
+])
+def test_route_only_rejects_before_enqueue(desc_kw, T, kw, want):
+    assert _route_call(_desc(**desc_kw), T, **kw) == want
+
+
+def test_forward_rejects_null_banks():
+    lib = ftm.load()
+    d = ftm.make_desc(_desc())
+    r = ftm.ft_route_t(*[FAKE] * 8)
+    b = ftm.ft_banks_t(None, None, None, None)
+    st = lib.ft_moe_forward(ctypes.byref(d), ctypes.byref(b), FAKE, FAKE, FAKE, 4, FAKE,
+                            ctypes.byref(r), FAKE, 1 << 40, None)
+    assert st == ftm.FT_ERR_NULL
+    st = lib.ft_moe_forward(ctypes.byref(d), None, FAKE, FAKE, FAKE, 4, FAKE,
+                            ctypes.byref(r), FAKE, 1 << 40, None)
+    assert st == ftm.FT_ERR_NULL
+    fp8 = ftm.make_desc(_desc(w_dtype=2, x_dtype=1))
+    b = ftm.ft_banks_t(FAKE, FAKE, None, None)                  # fp8 without scales
+    st = lib.ft_moe_forward(ctypes.byref(fp8), ctypes.byref(b), FAKE, FAKE, FAKE, 4, FAKE,
+                            ctypes.byref(r), FAKE, 1 << 40, None)
+    assert st == ftm.FT_ERR_NULL
+
+
+def test_miss_list_to_host_rejects_nulls():
+    lib = ftm.load()
+    d = ftm.make_desc(_desc())
+    r = ftm.ft_route_t(*[FAKE] * 8)
+    h = ftm.ft_host_miss_t(None, FAKE, FAKE, FAKE, FAKE)
+    assert lib.ft_miss_list_to_host(ctypes.byref(d), ctypes.byref(r), 4, ctypes.byref(h), None) == ftm.FT_ERR_NULL

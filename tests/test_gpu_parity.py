@@ -1,0 +1,229 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle, on the same seeded inputs.
+
+Lists, ids, slots, offsets and counts must be bit-exact; gates within 2e-6; layer outputs
+within the max-relative-error bound (row-RMS floor) of 1e-3 for fp32 weights, 1e-2 for bf16
+and 3e-2 for fp8 weights, and rows the oracle makes exactly zero must be exactly zero.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_16157_amd as ftm
+import workloads
+from tests._util import oracle_inputs
+
+pytestmark = pytest.mark.gpu
+
+TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2}
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def run_route(lay):
+    T, desc = lay.tokens, lay.desc()
+    ws = ftm.alloc_workspace(desc, T)
+    route = ftm.RouteBuffers(T, lay.top_k, lay.n_experts)
+    ftm.ft_route_only(desc, lay.logits, lay.slot_table, T, route, ws)
+    torch.cuda.synchronize()
+    return route
+
+
+def run_forward(lay, T=None):
+    T = lay.tokens if T is None else T
+    desc = lay.desc()
+    ws = ftm.alloc_workspace(desc, T)
+    route = ftm.RouteBuffers(T, lay.top_k, lay.n_experts)
+    out = torch.full((T, lay.hidden), float("nan"), dtype=torch.float32, device="cuda")
+    ftm.ft_moe_forward(desc, ftm.banks_of(lay), lay.logits, lay.slot_table, lay.x, T, out, route, ws)
+    torch.cuda.synchronize()
+    return out, route
+
+
+def check_route(route, r, T, k):
+    pk = T * k
+    g = lambda t: t.cpu().numpy()
+    assert np.array_equal(g(route.topk_ids)[:pk].reshape(T, k), r["topk_ids"])
+    assert np.array_equal(g(route.topk_slot)[:pk].reshape(T, k), r["topk_slot"])
+    np.testing.assert_allclose(g(route.topk_w)[:pk].reshape(T, k), r["topk_w"], rtol=0, atol=2e-6)
+    hp, mp = g(route.hit_pairs)[:pk], g(route.miss_pairs)[:pk]
+    assert np.array_equal(hp[: r["n_hit"]], r["hit_pairs"])
+    assert np.array_equal(mp[: r["n_miss"]], r["miss_pairs"])
+    assert np.all(hp[r["n_hit"]:] == -1) and np.all(mp[r["n_miss"]:] == -1)
+    assert np.array_equal(g(route.hit_off), r["hit_off"])
+    assert np.array_equal(g(route.miss_off), r["miss_off"])
+    assert g(route.counts).tolist() == [r["n_hit"], r["n_miss"], r["m_unique_miss"], r["status"]]
+
+
+def check_output(out, ref, w_dtype, rows=None):
+    got = out.cpu().numpy()
+    if rows is not None:
+        got, ref = got[rows], ref[rows]
+    assert np.isfinite(got).all()
+    zero = ~ref.any(axis=1)
+    assert not got[zero].any(), "rows without hits must be exactly zero"
+    err = oracle.max_rel_err(got, ref)
+    _say(f"   max_rel_err={err:.3e} (tol {TOL[w_dtype]:.0e})")
+    assert err <= TOL[w_dtype]
+
+
+# ------------------------------------------------------------------ routing, bit-exact
+
+ROUTE_CASES = [("tiny", 16), ("qwen3_decode", 1), ("qwen3_decode", 8), ("qwen3_decode", 32),
+               ("dsv3_decode", 1), ("dsv3_decode", 16), ("dsv3_decode", 64),
+               ("qwen3_prefill", 4096), ("dsv3_prefill", 8192), ("qwen3_decode", 300)]
+
+
+def _route_only_layer(name, T):
+    """Logits and slot table of a config; weights are not needed for routing."""
+    cfg = workloads.CONFIGS[name]
+    small = workloads.LayerConfig(**{**cfg.__dict__, "hidden": 128, "inter": 128})
+    return workloads.make_layer_from(small, T, device="cuda")
+
+
+@pytest.mark.parametrize("name,T", ROUTE_CASES)
+def test_route_bit_exact_configs(name, T):
+    _say(f"route {name} T={T}")
+    lay = _route_only_layer(name, T)
+    route = run_route(lay)
+    desc, banks, logits, st, x = oracle_inputs(lay)
+    check_route(route, oracle.route(desc, logits, st), T, lay.top_k)
+
+
+@pytest.mark.parametrize("seed,E,k,T,ties", [(0, 8, 8, 5, True), (1, 1024, 64, 3, False),
+                                             (2, 1000, 7, 33, True), (3, 64, 1, 2500, False),
+                                             (4, 256, 8, 257, True), (5, 130, 13, 4099, True),
+                                             (6, 1024, 8, 600, False), (7, 2, 2, 1, True)])
+def test_route_bit_exact_random(seed, E, k, T, ties):
+    _say(f"route random seed={seed} E={E} k={k} T={T}")
+    lay = workloads.random_layer(seed, hidden=128, inter=128, n_experts=E, top_k=k, tokens=T,
+                                 tie_logits=ties, zipf_s=1.0 if seed % 2 else 0.0, device="cuda")
+    route = run_route(lay)
+    desc, banks, logits, st, x = oracle_inputs(lay)
+    check_route(route, oracle.route(desc, logits, st), T, k)
+
+
+def test_route_deterministic():
+    lay = _route_only_layer("dsv3_prefill", 8192)
+    a, b = run_route(lay), run_route(lay)
+    for n in ("topk_ids", "topk_w", "topk_slot", "hit_pairs", "miss_pairs", "hit_off", "miss_off",
+              "counts"):
+        assert torch.equal(getattr(a, n), getattr(b, n)), n
+
+
+@pytest.mark.parametrize("T", [5, 700])
+def test_invalid_slot_tables_flagged_and_treated_as_misses(T):
+    lay = workloads.random_layer(11, hidden=128, inter=128, n_experts=16, top_k=4, tokens=T,
+                                 n_resident=10, shared=True, device="cuda")
+    st = lay.slot_table.clone()
+    res = (st >= 0).nonzero().flatten().tolist()
+    st[res[0]] = st[res[1]]                  # duplicate
+    st[res[2]] = lay.n_slots + 5             # out of range
+    st[res[3]] = lay.shared_slot             # points at the shared expert
+    lay.slot_table = st
+    _say(f"invalid slot table T={T}: {st.tolist()}")
+    route = run_route(lay)
+    desc, banks, logits, stn, x = oracle_inputs(lay)
+    r = oracle.route(desc, logits, stn)
+    assert r["status"] == 7
+    check_route(route, r, T, lay.top_k)
+
+
+# ------------------------------------------------------------------ whole layer
+
+@pytest.mark.parametrize("name,T", [("tiny", 16), ("qwen3_decode", 1), ("qwen3_decode", 8),
+                                    ("qwen3_decode", 32), ("dsv3_decode", 1), ("dsv3_decode", 16)])
+def test_forward_configs_full(name, T):
+    _say(f"forward {name} T={T}")
+    lay = workloads.make_layer(name, T, device="cuda")
+    out, route = run_forward(lay)
+    ref, r = oracle.moe_partial(*oracle_inputs(lay))
+    check_route(route, r, T, lay.top_k)
+    check_output(out, ref, lay.w_dtype)
+
+
+@pytest.mark.parametrize("name,T,rows", [("dsv3_decode", 64, [0, 13, 63]),
+                                         ("qwen3_prefill", 4096, list(range(0, 4096, 97)) + [4095]),
+                                         ("dsv3_prefill", 8192, [0, 1023, 1024, 3000, 8191])])
+def test_forward_configs_sampled(name, T, rows):
+    _say(f"forward {name} T={T} sampled rows {rows}")
+    lay = workloads.make_layer(name, T, device="cuda")
+    out, route = run_forward(lay)
+    ref, r = oracle.moe_partial(*oracle_inputs(lay), tokens=rows)
+    check_route(route, r, T, lay.top_k)
+    check_output(out, ref, lay.w_dtype, rows=rows)
+
+
+RANDOM_FWD = [
+    # seed, w_dtype, gating, E, k, T, n_res, shared, H, I
+    (0, workloads.DT_BF16, 0, 8, 2, 1, 4, False, 128, 256),
+    (1, workloads.DT_BF16, 1, 16, 4, 37, 16, False, 256, 128),
+    (2, workloads.DT_BF16, 0, 16, 4, 70, 0, False, 128, 128),
+    (3, workloads.DT_BF16, 0, 16, 4, 70, 0, True, 128, 128),
+    (4, workloads.DT_FP8, 1, 32, 8, 19, 9, True, 384, 256),
+    (5, workloads.DT_FP8, 0, 12, 3, 130, 12, False, 256, 384),
+    (6, workloads.DT_F32, 0, 8, 3, 45, 5, True, 128, 384),
+    (7, workloads.DT_F32, 1, 4, 4, 3, 2, False, 640, 128),
+    (8, workloads.DT_BF16, 0, 64, 6, 700, 40, True, 256, 256),
+]
+
+
+@pytest.mark.parametrize("case", RANDOM_FWD, ids=[str(c[0]) for c in RANDOM_FWD])
+def test_forward_random_shapes(case):
+    seed, wdt, gating, E, k, T, n_res, shared, H, I = case
+    _say(f"forward random {case}")
+    lay = workloads.random_layer(seed, hidden=H, inter=I, n_experts=E, top_k=k, tokens=T,
+                                 gating=gating, w_dtype=wdt, n_resident=n_res, shared=shared,
+                                 device="cuda")
+    out, route = run_forward(lay)
+    ref, r = oracle.moe_partial(*oracle_inputs(lay))
+    check_route(route, r, T, k)
+    check_output(out, ref, wdt)
+    if n_res == 0 and not shared:
+        assert not out.any()
+
+
+def test_forward_T0_is_noop():
+    lay = workloads.make_layer("tiny", 16, device="cuda")
+    desc = lay.desc()
+    ws = ftm.alloc_workspace(desc, 16)
+    route = ftm.RouteBuffers(16, lay.top_k, lay.n_experts)
+    out = torch.full((16, lay.hidden), 7.0, device="cuda")
+    ftm.ft_moe_forward(desc, ftm.banks_of(lay), lay.logits, lay.slot_table, lay.x, 0, out, route, ws)
+    torch.cuda.synchronize()
+    assert bool((out == 7.0).all())
+
+
+def test_miss_list_to_host():
+    lay = workloads.make_layer("tiny", 16, device="cuda")
+    out, route = run_forward(lay)
+    host = ftm.HostMissBuffers(16, lay.top_k, lay.n_experts)
+    ftm.ft_miss_list_to_host(lay.desc(), route, 16, host)
+    torch.cuda.synchronize()
+    assert torch.equal(host.counts, route.counts.cpu())
+    assert torch.equal(host.miss_pairs, route.miss_pairs.cpu())
+    assert torch.equal(host.miss_off, route.miss_off.cpu())
+    assert torch.equal(host.topk_ids, route.topk_ids.cpu())
+    assert torch.equal(host.topk_w, route.topk_w.cpu())
+
+
+def test_forward_deterministic_and_slot_table_change():
+    """Same inputs twice give identical bits; a new slot table between calls (the runtime cache
+    rebuild of Section 3.3) is honoured, down to zero residency."""
+    lay = workloads.random_layer(12, hidden=256, inter=256, n_experts=32, top_k=4, tokens=40,
+                                 w_dtype=workloads.DT_BF16, n_resident=20, device="cuda")
+    a, _ = run_forward(lay)
+    b, _ = run_forward(lay)
+    assert torch.equal(a, b)
+    st = lay.slot_table.clone()
+    st[: 16] = -1
+    lay.slot_table = st
+    out, route = run_forward(lay)
+    ref, r = oracle.moe_partial(*oracle_inputs(lay))
+    check_route(route, r, 40, 4)
+    check_output(out, ref, workloads.DT_BF16)
+    lay.slot_table = torch.full_like(st, -1)
+    out, route = run_forward(lay)
+    assert not out.any() and int(route.counts[0]) == 0
