@@ -155,12 +155,35 @@ ft_status_t ft_route_only(const ft_moe_desc_t *desc, const float *logits, const 
  * CPU partial sums merge exactly).
  *   x           [T][H] device, x_dtype
  *   out_partial [T][H] float32 device, fully overwritten; a token with no hit (and no shared
- *               expert) gets exact zeros.
+ *               expert) gets exact zeros.  The gate-weighted expert outputs are summed with
+ *               float32 atomic adds, so the order of that sum (and the last bits) may differ
+ *               between calls; the routing outputs are bit-reproducible.
+ *   x, out_partial, banks->w13 and banks->w2 must be 16-byte aligned (FT_ERR_SHAPE otherwise).
  */
 ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
                            const int32_t *slot_table, const void *x, int32_t T,
                            float *out_partial, const ft_route_t *route, void *ws,
                            size_t ws_bytes, void *stream);
+
+/*
+ * Stage boundaries of one ft_moe_forward call, for attributing device time per stage without
+ * a profiler.  ev[i] is recorded on the call's stream when stage i starts and ev[FT_PROF_STAGES]
+ * when the last stage ends: stage 0 routing (top-k, classification, permutation), stage 1 the
+ * grouped gate/up projection with SiLU-mul, stage 2 the grouped down projection, stage 3 the
+ * combine (a stage that a fused kernel absorbs records two adjacent events).  Entries are
+ * hipEvent_t handles created by the caller; NULL entries are skipped.
+ */
+#define FT_PROF_STAGES 4
+typedef struct {
+    void *ev[FT_PROF_STAGES + 1];
+} ft_prof_events_t;
+
+/* ft_moe_forward, plus hipEventRecord of the caller's stage events (may be NULL). */
+ft_status_t ft_moe_forward_profiled(const ft_moe_desc_t *desc, const ft_banks_t *banks,
+                                    const float *logits, const int32_t *slot_table, const void *x,
+                                    int32_t T, float *out_partial, const ft_route_t *route,
+                                    void *ws, size_t ws_bytes, void *stream,
+                                    const ft_prof_events_t *events);
 
 /*
  * Enqueue asynchronous device-to-host copies of the miss list (counts, miss_pairs, miss_off,

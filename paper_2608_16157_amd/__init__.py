@@ -7,6 +7,8 @@ of the C ABI declared in ``include/ftmoe.h``:
     ft_moe_workspace_bytes(desc, max_tokens) -> int
     ft_route_only(desc, logits, slot_table, T, route, ws, stream=None)
     ft_moe_forward(desc, banks, logits, slot_table, x, T, out_partial, route, ws, stream=None)
+    ft_moe_forward_profiled(desc, banks, logits, slot_table, x, T, out_partial, route, ws,
+                            events, stream=None)
     ft_miss_list_to_host(desc, route, T, host, stream=None)
     ft_status_string(status) -> str
 
@@ -32,7 +34,8 @@ FT_SLOT_MISS = -1
 FT_DEV_SLOT_RANGE, FT_DEV_SLOT_DUP, FT_DEV_SLOT_SHARED = 1, 2, 4
 
 EXPORTED = ("ft_moe_workspace_bytes", "ft_route_only", "ft_moe_forward",
-            "ft_miss_list_to_host", "ft_status_string")
+            "ft_moe_forward_profiled", "ft_miss_list_to_host", "ft_status_string")
+FT_PROF_STAGES = 4
 
 
 class FtError(RuntimeError):
@@ -54,6 +57,10 @@ class ft_banks_t(ctypes.Structure):
 class ft_route_t(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("topk_ids", "topk_w", "topk_slot", "hit_pairs",
                                                "miss_pairs", "hit_off", "miss_off", "counts")]
+
+
+class ft_prof_events_t(ctypes.Structure):
+    _fields_ = [("ev", ctypes.c_void_p * 5)]
 
 
 class ft_host_miss_t(ctypes.Structure):
@@ -83,6 +90,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.ft_moe_forward.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), ctypes.c_void_p, ctypes.c_void_p,
                                    ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, P(ft_route_t),
                                    ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.ft_moe_forward_profiled.restype = ctypes.c_int
+    lib.ft_moe_forward_profiled.argtypes = lib.ft_moe_forward.argtypes + [P(ft_prof_events_t)]
     lib.ft_miss_list_to_host.restype = ctypes.c_int
     lib.ft_miss_list_to_host.argtypes = [P(ft_moe_desc_t), P(ft_route_t), ctypes.c_int32,
                                          P(ft_host_miss_t), ctypes.c_void_p]
@@ -193,6 +202,22 @@ def ft_moe_forward(desc: dict, banks: dict, logits: torch.Tensor, slot_table: to
                                _ptr(slot_table), _ptr(x), int(T), _ptr(out_partial),
                                ctypes.byref(route.c()), _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "ft_moe_forward")
+
+
+def ft_moe_forward_profiled(desc: dict, banks: dict, logits: torch.Tensor, slot_table: torch.Tensor,
+                            x: torch.Tensor, T: int, out_partial: torch.Tensor, route: RouteBuffers,
+                            ws: torch.Tensor, events, stream=None) -> None:
+    """``events``: FT_PROF_STAGES + 1 hipEvent_t handles (ints) or None entries."""
+    b = ft_banks_t(_ptr(banks.get("w13")), _ptr(banks.get("w2")), _ptr(banks.get("s13")),
+                   _ptr(banks.get("s2")))
+    ev = ft_prof_events_t()
+    for i, e in enumerate(events):
+        ev.ev[i] = e
+    st = load().ft_moe_forward_profiled(ctypes.byref(make_desc(desc)), ctypes.byref(b), _ptr(logits),
+                                        _ptr(slot_table), _ptr(x), int(T), _ptr(out_partial),
+                                        ctypes.byref(route.c()), _ptr(ws), ws.numel(),
+                                        _stream(stream), ctypes.byref(ev))
+    _check(st, "ft_moe_forward_profiled")
 
 
 def ft_miss_list_to_host(desc: dict, route: RouteBuffers, T: int, host: HostMissBuffers,

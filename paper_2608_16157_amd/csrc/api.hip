@@ -54,9 +54,7 @@ WsView carve(const ft_moe_desc_t *d, int T, void *ws) {
     v.grp_len = reinterpret_cast<int32_t *>(b + L.grp_len);
     v.row_tok = reinterpret_cast<int32_t *>(b + L.row_tok);
     v.row_gate = reinterpret_cast<float *>(b + L.row_gate);
-    v.pair_row = reinterpret_cast<int32_t *>(b + L.pair_row);
     v.h = b + L.h;
-    v.y = reinterpret_cast<float *>(b + L.y);
     return v;
 }
 
@@ -107,10 +105,14 @@ ft_status_t ft_route_only(const ft_moe_desc_t *desc, const float *logits, const 
     return FT_OK;
 }
 
-ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
-                           const int32_t *slot_table, const void *x, int32_t T,
-                           float *out_partial, const ft_route_t *route, void *ws,
-                           size_t ws_bytes, void *stream) {
+}  // extern "C"
+
+namespace {
+
+ft_status_t forward_impl(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
+                         const int32_t *slot_table, const void *x, int32_t T, float *out_partial,
+                         const ft_route_t *route, void *ws, size_t ws_bytes, void *stream,
+                         const ft_prof_events_t *events) {
     if (ft_status_t s = check_common(desc, logits, slot_table, T, route, ws, ws_bytes); s != FT_OK)
         return s;
     if (!banks) return FT_ERR_NULL;
@@ -119,9 +121,14 @@ ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, c
     if (desc->n_slots > 0 && (!banks->w13 || !banks->w2)) return FT_ERR_NULL;
     if (desc->w_dtype == FT_DT_FP8E4M3FN_B128 && desc->n_slots > 0 && (!banks->s13 || !banks->s2))
         return FT_ERR_NULL;
+    const uintptr_t al = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(out_partial) |
+                         reinterpret_cast<uintptr_t>(banks->w13) | reinterpret_cast<uintptr_t>(banks->w2);
+    if (al % 16) return FT_ERR_SHAPE;
     const hipStream_t s = static_cast<hipStream_t>(stream);
+    Prof prof(events, s);
     const WsView wv = carve(desc, T, ws);
     const RouteArgs ra = route_args(desc, logits, slot_table, T, route, wv);
+    if (!prof.mark(0)) return FT_ERR_HIP;
     if (launch_route(ra, s) != hipSuccess) return FT_ERR_HIP;
 
     ExpertArgs ea{};
@@ -143,11 +150,32 @@ ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, c
     if (routed_slots < mg) mg = routed_slots;
     if (static_cast<long>(T) * desc->top_k < mg) mg = static_cast<long>(T) * desc->top_k;
     ea.max_groups = static_cast<int>(mg) + ea.shared;
-    ea.pair_row = wv.pair_row;
     ea.ro = ra.ro;
     ea.wv = wv;
-    if (launch_experts(ea, s) != hipSuccess) return FT_ERR_HIP;
+    if (launch_experts(ea, s, prof) != hipSuccess) return FT_ERR_HIP;
+    if (!prof.mark(FT_PROF_STAGES)) return FT_ERR_HIP;
     return FT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
+                           const int32_t *slot_table, const void *x, int32_t T,
+                           float *out_partial, const ft_route_t *route, void *ws,
+                           size_t ws_bytes, void *stream) {
+    return forward_impl(desc, banks, logits, slot_table, x, T, out_partial, route, ws, ws_bytes,
+                        stream, nullptr);
+}
+
+ft_status_t ft_moe_forward_profiled(const ft_moe_desc_t *desc, const ft_banks_t *banks,
+                                    const float *logits, const int32_t *slot_table, const void *x,
+                                    int32_t T, float *out_partial, const ft_route_t *route,
+                                    void *ws, size_t ws_bytes, void *stream,
+                                    const ft_prof_events_t *events) {
+    return forward_impl(desc, banks, logits, slot_table, x, T, out_partial, route, ws, ws_bytes,
+                        stream, events);
 }
 
 ft_status_t ft_miss_list_to_host(const ft_moe_desc_t *desc, const ft_route_t *route, int32_t T,

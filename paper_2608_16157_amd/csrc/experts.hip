@@ -1,34 +1,61 @@
 // Grouped SwiGLU expert evaluation over slot-resident weights (Section 3.2: grouped evaluation
 // of the GPU execution set; Section 4.2: every bank row is one slot, so a group's weights are
-// addressed as bank + slot * expert_stride with no relayout), then the gate-weighted combine.
+// addressed as bank + slot * expert_stride with no relayout), with the gate-weighted combine
+// fused into the down projection.
 //
-// General path, any token count and any weight dtype:
-//   grouped_gemv<GATEUP>: h[r] = silu(W1 x_tok(r)) * (W3 x_tok(r))        per group, 8 h-columns/WG
-//   grouped_gemv<DOWN>  : y[r] = gate(r) * W2 h[r]                         per group, 16 y-columns/WG
-//   combine             : out[t] = sum_j y[row(t,j)] (+ y[shared row of t]) in fixed j order
-// The weights stream from HBM once per (group, column tile); tokens of a group are the MFMA M
-// dimension (16-row tiles), weight rows the N dimension, and the hidden/intermediate dimension
-// is the contraction, split over the 4 waves of a workgroup in 128-wide blocks (the fp8 scale
-// block size) and reduced through LDS.
+// Streaming (GEMV-like) path, any token count and any weight dtype:
+//   grouped_gemv<GATEUP>: h[r] = silu(W1 x_tok(r)) * (W3 x_tok(r))       per group, 8 h-columns/WG
+//                         (also zeroes out_partial)
+//   grouped_gemv<DOWN>  : out[tok(r)] += gate(r) * W2 h[r]               per group, 16 columns/WG
+// The weights stream from HBM once per (group, column tile).  Tokens of a group are the MFMA M
+// dimension (16-row tiles), weight rows the N dimension; the contraction (hidden or intermediate
+// dimension) is split over the 4 waves of a workgroup in contiguous runs of 128-wide blocks (the
+// fp8 scale block), whose weight loads a wave issues in batches before any MFMA consumes them;
+// the waves' partial sums are reduced through LDS.
 #include "ftmoe_device.h"
 #include "ftmoe_internal.h"
 
+#include <algorithm>
+#include <type_traits>
+
 namespace ftmoe {
+
+// Tuning constants (measured on MI355X; see the design notes for the sweep).
+#ifndef FT_GEMV_NB
+#define FT_GEMV_NB 2
+#endif
+#ifndef FT_GEMV_MT_MAX
+#define FT_GEMV_MT_MAX 2
+#endif
+#ifndef FT_GEMV_D_F32
+#define FT_GEMV_D_F32 1
+#endif
+#ifndef FT_GEMV_D_BF16
+#define FT_GEMV_D_BF16 1
+#endif
+#ifndef FT_GEMV_D_FP8
+#define FT_GEMV_D_FP8 1
+#endif
+#ifndef FT_GEMV_NT_LOADS
+#define FT_GEMV_NT_LOADS 0
+#endif
 
 constexpr int kGemvThreads = 256;
 constexpr int kGemvWaves = kGemvThreads / kWave;
-constexpr int kMTiles = 4;                 // 16-row M tiles per pass (64 rows)
-constexpr int kPassRows = 16 * kMTiles;
 
 enum { EPI_GATEUP = 0, EPI_DOWN = 1 };
 
 template <int WT> struct WTr;
-template <> struct WTr<FT_DT_F32> { static constexpr int kLoads = 8, kElem = 4; };
-template <> struct WTr<FT_DT_BF16> { static constexpr int kLoads = 4, kElem = 2; };
-template <> struct WTr<FT_DT_FP8E4M3FN_B128> { static constexpr int kLoads = 2, kElem = 1; };
+// kLoads: 16-byte weight loads per lane per 128-wide K block; kBatch: K blocks in flight ahead
+template <> struct WTr<FT_DT_F32> { static constexpr int kLoads = 8, kElem = 4, kBatch = FT_GEMV_D_F32; };
+template <> struct WTr<FT_DT_BF16> { static constexpr int kLoads = 4, kElem = 2, kBatch = FT_GEMV_D_BF16; };
+template <> struct WTr<FT_DT_FP8E4M3FN_B128> { static constexpr int kLoads = 2, kElem = 1, kBatch = FT_GEMV_D_FP8; };
 
 __device__ __forceinline__ u32x4_t ld16(const void *p) {
     return *reinterpret_cast<const u32x4_t *>(p);
+}
+__device__ __forceinline__ u32x4_t ld16_stream(const void *p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
 }
 
 // Element offset (within a 128-wide K block) of a lane's 16-byte weight load number c.
@@ -38,44 +65,60 @@ template <int WT> __device__ __forceinline__ int wofs(int c, int q) {
     else return c * 64 + q * 16;
 }
 
-// One 128-wide K block for one 16-row M tile: acc += A(rows, kblock) * B(kblock, 16 cols).
-// `a_row` points at the activation row of this lane's M row (nullptr = padding row) already
-// offset to the K block; activations are f32 for f32 weights, bf16 otherwise.
+// Activation loads of one 128-wide K block for one 16-row M tile, 16 bytes each, at the K
+// offsets the lane's weight operand uses (f32: 8 x 4 floats at c*16 + q*4; bf16: 4 x 8 at
+// c*32 + q*8; fp8 weights widened to bf16: 4 x 8 at (c/2)*64 + q*16 + (c%2)*8).  `a_row` points
+// at this lane's activation row offset to the K block; padding rows point at a real row and
+// their results are never stored, so the loads need no branch.
+template <int WT> struct ALd { static constexpr int n = WT == FT_DT_F32 ? 8 : 4; };
+
 template <int WT>
-__device__ __forceinline__ void mfma_kblock(const void *a_row, const u32x4_t (&w)[WTr<WT>::kLoads],
-                                            const u32x4_t (&wcvt)[4], int q, floatx4_t &acc) {
-    if constexpr (WT == FT_DT_F32) {
-        const float *a = static_cast<const float *>(a_row);
+__device__ __forceinline__ void aload(u32x4_t (&dst)[ALd<WT>::n], const uint8_t *a_row, int q) {
 #pragma unroll
-        for (int c = 0; c < 8; ++c) {
-            u32x4_t av = a ? ld16(a + c * 16 + q * 4) : u32x4_t{0, 0, 0, 0};
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(av[i]),
-                                                           __uint_as_float(w[c][i]), acc, 0, 0, 0);
-        }
-    } else if constexpr (WT == FT_DT_BF16) {
-        const uint16_t *a = static_cast<const uint16_t *>(a_row);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-            u32x4_t av = a ? ld16(a + c * 32 + q * 8) : u32x4_t{0, 0, 0, 0};
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av), as_bf16x8(w[c]), acc, 0, 0, 0);
-        }
-    } else {
-        const uint16_t *a = static_cast<const uint16_t *>(a_row);
-#pragma unroll
-        for (int c = 0; c < 2; ++c) {
-            u32x4_t a0 = a ? ld16(a + c * 64 + q * 16) : u32x4_t{0, 0, 0, 0};
-            u32x4_t a1 = a ? ld16(a + c * 64 + q * 16 + 8) : u32x4_t{0, 0, 0, 0};
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a0), as_bf16x8(wcvt[2 * c]), acc, 0, 0, 0);
-            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a1), as_bf16x8(wcvt[2 * c + 1]), acc, 0, 0, 0);
-        }
+    for (int c = 0; c < ALd<WT>::n; ++c) {
+        int ofs;
+        if constexpr (WT == FT_DT_F32) ofs = (c * 16 + q * 4) * 4;
+        else if constexpr (WT == FT_DT_BF16) ofs = (c * 32 + q * 8) * 2;
+        else ofs = ((c >> 1) * 64 + q * 16 + (c & 1) * 8) * 2;
+        dst[c] = ld16(a_row + ofs);
     }
 }
 
-template <int WT, int EPI>
+// acc += A(rows, kblock) * B(kblock, 16 cols) for one 16-row M tile.  `av` from aload; `w` the
+// lane's weight operand of the block (for fp8 already widened to 4 x 8 bf16).
+template <int WT>
+__device__ __forceinline__ void mfma_kblock(const u32x4_t (&av)[ALd<WT>::n], const u32x4_t *w,
+                                            floatx4_t &acc) {
+    if constexpr (WT == FT_DT_F32) {
+#pragma unroll
+        for (int c = 0; c < 8; ++c)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(av[c][i]),
+                                                           __uint_as_float(w[c][i]), acc, 0, 0, 0);
+    } else {
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+            acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(av[c]), as_bf16x8(w[c]), acc, 0, 0, 0);
+    }
+}
+
+// One work item = (group, NB x 16 weight rows).  The 4 waves of the workgroup split the item's
+// K blocks into contiguous quarters and meet in LDS; rows of the group are taken 16 at a time
+// (one MFMA M tile per pass).  Each activation load feeds the NB weight blocks of the item.
+template <int WT, int EPI, int NB>
 __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int tiles) {
-    __shared__ float s_red[kGemvWaves][kPassRows][16];
+    constexpr int D = WTr<WT>::kBatch, NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
+    constexpr int COLS = NB * 16;
+    __shared__ float s_red[kGemvWaves][16][COLS + 1];
+    if constexpr (EPI == EPI_GATEUP) {
+        // zero the output that the down projection accumulates into
+        const size_t n4 = static_cast<size_t>(a.T) * a.H / 4;
+        float4 *o4 = reinterpret_cast<float4 *>(a.out);
+        for (size_t i = static_cast<size_t>(blockIdx.x) * kGemvThreads + threadIdx.x; i < n4;
+             i += static_cast<size_t>(gridDim.x) * kGemvThreads)
+            o4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
     const int g = blockIdx.x / tiles, tile = blockIdx.x % tiles;
     if (g >= a.wv.grp_meta[0]) return;
     const int slot = a.wv.grp_slot[g], beg = a.wv.grp_beg[g], len = a.wv.grp_len[g];
@@ -83,152 +126,191 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
     const int K = EPI == EPI_GATEUP ? H : I;
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int n = lane & 15, q = lane >> 4;
-    // weight row of this lane's N column
-    const int wrow = EPI == EPI_GATEUP ? (n < 8 ? tile * 8 + n : I + tile * 8 + n - 8) : tile * 16 + n;
-    const size_t wstride = static_cast<size_t>(EPI == EPI_GATEUP ? 2 * I : H) * K;  // per slot
-    const uint8_t *wbase = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.w13 : a.w2) +
-                           (static_cast<size_t>(slot) * wstride + static_cast<size_t>(wrow) * K) *
-                               WTr<WT>::kElem;
-    const float *sbase = nullptr;
-    if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
-        const float *s = EPI == EPI_GATEUP ? a.s13 : a.s2;
-        const int nkb = K / 128, nrb = (EPI == EPI_GATEUP ? 2 * I : H) / 128;
-        sbase = s + (static_cast<size_t>(slot) * nrb + wrow / 128) * nkb;
-    }
+    const int nrows = EPI == EPI_GATEUP ? 2 * I : H;
     const int nkb = K / 128;
+    // weight row of this lane's N column in block b: a gate/up block pairs 8 gate rows with the
+    // 8 matching up rows, so SiLU(gate) * up of one h column stays inside the block
+    const uint8_t *wbase[NB];
+    const float *sbase[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
+        const int wrow = EPI == EPI_GATEUP ? (n < 8 ? col0 + n : I + col0 + n - 8) : col0 + n;
+        wbase[b] = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.w13 : a.w2) +
+                   (static_cast<size_t>(slot) * nrows + wrow) * static_cast<size_t>(K) * WTr<WT>::kElem;
+        sbase[b] = nullptr;
+        if constexpr (WT == FT_DT_FP8E4M3FN_B128)
+            sbase[b] = (EPI == EPI_GATEUP ? a.s13 : a.s2) +
+                       (static_cast<size_t>(slot) * (nrows / 128) + wrow / 128) * nkb;
+    }
     const size_t a_elem = (WT == FT_DT_F32) ? 4 : 2;
+    const int per = (nkb + kGemvWaves - 1) / kGemvWaves;
+    const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
 
-    for (int r0 = 0; r0 < len; r0 += kPassRows) {
-        // activation row pointers of this lane's M row in each M tile
-        const uint8_t *arow[kMTiles];
+    // One pass over the K blocks for MT 16-row M tiles starting at row r0 (MT chosen per pass).
+    auto pass = [&](auto mt_const, int r0, floatx4_t (&acc)[FT_GEMV_MT_MAX][NB]) {
+        constexpr int MT = decltype(mt_const)::value;
+        const uint8_t *arow[MT];
 #pragma unroll
-        for (int mt = 0; mt < kMTiles; ++mt) {
-            const int r = r0 + mt * 16 + n;
-            arow[mt] = nullptr;
-            if (r < len) {
-                if constexpr (EPI == EPI_GATEUP) {
-                    const int tok = a.wv.row_tok[beg + r];
-                    arow[mt] = static_cast<const uint8_t *>(a.x) + static_cast<size_t>(tok) * H * a_elem;
-                } else {
-                    arow[mt] = static_cast<const uint8_t *>(a.wv.h) + static_cast<size_t>(beg + r) * I * a_elem;
-                }
-            }
+        for (int mt = 0; mt < MT; ++mt) {
+            // this lane's activation row; padding rows repeat the last row (their sums are dropped)
+            const int rr = min(len - 1, r0 + mt * 16 + n);
+            if constexpr (EPI == EPI_GATEUP)
+                arow[mt] = static_cast<const uint8_t *>(a.x) + static_cast<size_t>(a.wv.row_tok[beg + rr]) * H * a_elem;
+            else
+                arow[mt] = static_cast<const uint8_t *>(a.wv.h) + static_cast<size_t>(beg + rr) * I * a_elem;
         }
-        const int nmt = min(kMTiles, (len - r0 + 15) / 16);
-        floatx4_t acc[kMTiles];
+        // Each iteration issues every load of a batch of D K blocks (activations, weights, fp8
+        // scales) before any MFMA consumes them, and consumes them all before the next batch:
+        // no load is carried across the loop back-edge (the wait-count insertion would drain
+        // such a pipeline at the loop header) and no load sits under a branch (the tail batch
+        // re-reads the last block and multiplies its contribution by zero).  The scheduling
+        // barrier keeps the compiler from interleaving the loads with the MFMAs that use them.
+        for (int kbb = kb0; kbb < kb1; kbb += D) {
+            u32x4_t av[D][MT][NA];
+            u32x4_t wv[D][NB][NL];
+            float sv[D][NB];
 #pragma unroll
-        for (int mt = 0; mt < kMTiles; ++mt) acc[mt] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-
-        for (int kb = wave; kb < nkb; kb += kGemvWaves) {
-            u32x4_t w[WTr<WT>::kLoads];
+            for (int d = 0; d < D; ++d) {
+                const int kb = min(kbb + d, kb1 - 1);
 #pragma unroll
-            for (int c = 0; c < WTr<WT>::kLoads; ++c)
-                w[c] = ld16(wbase + static_cast<size_t>(kb * 128 + wofs<WT>(c, q)) * WTr<WT>::kElem);
-            u32x4_t wcvt[4];
-            if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
+                for (int mt = 0; mt < MT; ++mt)
+                    aload<WT>(av[d][mt], arow[mt] + static_cast<size_t>(kb) * 128 * a_elem, q);
 #pragma unroll
-                for (int c = 0; c < 2; ++c) {
-                    wcvt[2 * c] = fp8x8_to_bf16x8(w[c][0], w[c][1]);
-                    wcvt[2 * c + 1] = fp8x8_to_bf16x8(w[c][2], w[c][3]);
+                for (int b = 0; b < NB; ++b) {
+#pragma unroll
+                    for (int c = 0; c < NL; ++c) {
+                        const uint8_t *p = wbase[b] + static_cast<size_t>(kb * 128 + wofs<WT>(c, q)) * WTr<WT>::kElem;
+                        wv[d][b][c] = FT_GEMV_NT_LOADS ? ld16_stream(p) : ld16(p);
+                    }
+                    if constexpr (WT == FT_DT_FP8E4M3FN_B128) sv[d][b] = sbase[b][kb];
                 }
             }
-            const size_t koff = static_cast<size_t>(kb) * 128 * a_elem;
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int mt = 0; mt < kMTiles; ++mt) {
-                if (mt < nmt) {
-                    const void *ap = arow[mt] ? arow[mt] + koff : nullptr;
+            for (int d = 0; d < D; ++d) {
+                const float keep = kbb + d < kb1 ? 1.f : 0.f;
+#pragma unroll
+                for (int b = 0; b < NB; ++b) {
+                    u32x4_t wc[4];
                     if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
+                        wc[0] = fp8x8_to_bf16x8(wv[d][b][0][0], wv[d][b][0][1]);
+                        wc[1] = fp8x8_to_bf16x8(wv[d][b][0][2], wv[d][b][0][3]);
+                        wc[2] = fp8x8_to_bf16x8(wv[d][b][1][0], wv[d][b][1][1]);
+                        wc[3] = fp8x8_to_bf16x8(wv[d][b][1][2], wv[d][b][1][3]);
+                    }
+                    const float sc = keep * (WT == FT_DT_FP8E4M3FN_B128 ? sv[d][b] : 1.f);
+#pragma unroll
+                    for (int mt = 0; mt < MT; ++mt) {
                         floatx4_t part{0.f, 0.f, 0.f, 0.f};
-                        mfma_kblock<WT>(ap, w, wcvt, q, part);
-                        const float sc = sbase[kb];
+                        if constexpr (WT == FT_DT_FP8E4M3FN_B128) mfma_kblock<WT>(av[d][mt], wc, part);
+                        else mfma_kblock<WT>(av[d][mt], wv[d][b], part);
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) acc[mt][i] += sc * part[i];
-                    } else {
-                        mfma_kblock<WT>(ap, w, wcvt, q, acc[mt]);
+                        for (int i = 0; i < 4; ++i) acc[mt][b][i] += sc * part[i];
                     }
                 }
             }
         }
-        // cross-wave reduction: lane holds D[m = 4q + i][n] of each M tile
+    };
+
+    for (int r0 = 0; r0 < len; r0 += 16 * FT_GEMV_MT_MAX) {
+        floatx4_t acc[FT_GEMV_MT_MAX][NB];
 #pragma unroll
-        for (int mt = 0; mt < kMTiles; ++mt)
+        for (int mt = 0; mt < FT_GEMV_MT_MAX; ++mt)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) s_red[wave][mt * 16 + 4 * q + i][n] = acc[mt][i];
-        __syncthreads();
-        if constexpr (EPI == EPI_GATEUP) {
-            // 64 rows x 8 columns of h per pass
-            for (int idx = threadIdx.x; idx < kPassRows * 8; idx += kGemvThreads) {
-                const int m = idx / 8, c = idx % 8;
-                const int r = r0 + m;
-                if (r < len) {
-                    float gsum = 0.f, usum = 0.f;
+            for (int b = 0; b < NB; ++b) acc[mt][b] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+        const int nmt = min(FT_GEMV_MT_MAX, (len - r0 + 15) / 16);
+        if (FT_GEMV_MT_MAX > 1 && nmt > 1) pass(std::integral_constant<int, FT_GEMV_MT_MAX>{}, r0, acc);
+        else pass(std::integral_constant<int, 1>{}, r0, acc);
+
+        // lane (n, q) holds rows 4q + i of column n of every block; the 4 K quarters meet in LDS
+        for (int mt = 0; mt < nmt; ++mt) {
+            const int rt = r0 + mt * 16;
 #pragma unroll
-                    for (int w = 0; w < kGemvWaves; ++w) {
-                        gsum += s_red[w][m][c];
-                        usum += s_red[w][m][c + 8];
+            for (int b = 0; b < NB; ++b)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float v = acc[0][b][i];
+#pragma unroll
+                    for (int j = 1; j < FT_GEMV_MT_MAX; ++j)
+                        if (j == mt) v = acc[j][b][i];
+                    s_red[wave][4 * q + i][b * 16 + n] = v;
+                }
+            __syncthreads();
+            if constexpr (EPI == EPI_GATEUP) {
+                // 16 rows x NB*8 h columns
+                for (int idx = threadIdx.x; idx < 16 * NB * 8; idx += kGemvThreads) {
+                    const int m = idx / (NB * 8), cc = idx % (NB * 8), b = cc / 8, c = cc % 8;
+                    const int r = rt + m;
+                    if (r < len) {
+                        float gs = 0.f, us = 0.f;
+#pragma unroll
+                        for (int w = 0; w < kGemvWaves; ++w) {
+                            gs += s_red[w][m][b * 16 + c];
+                            us += s_red[w][m][b * 16 + c + 8];
+                        }
+                        const float hv = silu_f32(gs) * us;
+                        const size_t o = static_cast<size_t>(beg + r) * I + (tile * NB + b) * 8 + c;
+                        if constexpr (WT == FT_DT_F32) static_cast<float *>(a.wv.h)[o] = hv;
+                        else static_cast<uint16_t *>(a.wv.h)[o] = f32_to_bf16(hv);
                     }
-                    const float hv = silu_f32(gsum) * usum;
-                    const size_t o = static_cast<size_t>(beg + r) * I + tile * 8 + c;
-                    if constexpr (WT == FT_DT_F32) static_cast<float *>(a.wv.h)[o] = hv;
-                    else static_cast<uint16_t *>(a.wv.h)[o] = f32_to_bf16(hv);
                 }
-            }
-        } else {
-            for (int idx = threadIdx.x; idx < kPassRows * 16; idx += kGemvThreads) {
-                const int m = idx / 16, c = idx % 16;
-                const int r = r0 + m;
-                if (r < len) {
-                    float s = 0.f;
+            } else {
+                // gate-weighted scatter-add of 16 rows x NB*16 output columns
+                for (int idx = threadIdx.x; idx < 16 * COLS; idx += kGemvThreads) {
+                    const int m = idx / COLS, c = idx % COLS;
+                    const int r = rt + m;
+                    if (r < len) {
+                        float sum = 0.f;
 #pragma unroll
-                    for (int w = 0; w < kGemvWaves; ++w) s += s_red[w][m][c];
-                    a.wv.y[static_cast<size_t>(beg + r) * H + tile * 16 + c] = a.wv.row_gate[beg + r] * s;
+                        for (int w = 0; w < kGemvWaves; ++w) sum += s_red[w][m][c];
+                        const int tok = a.wv.row_tok[beg + r];
+                        unsafeAtomicAdd(a.out + static_cast<size_t>(tok) * H + tile * COLS + c,
+                                        a.wv.row_gate[beg + r] * sum);
+                    }
                 }
             }
+            __syncthreads();
         }
-        __syncthreads();
     }
 }
 
-// out[t][c] = sum_j y[row(t, j)][c] over hit pairs in j order, then the shared expert's row.
-__global__ __launch_bounds__(256) void combine(ExpertArgs a) {
-    const int c = (blockIdx.x * 256 + threadIdx.x) * 4;
-    if (c >= a.H) return;
-    const int nh = a.wv.grp_meta[2];
-    for (int t = blockIdx.y; t < a.T; t += gridDim.y) {
-        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int j = 0; j < a.k; ++j) {
-            const int r = a.wv.pair_row[t * a.k + j];
-            if (r >= 0) {
-                const float4 v = *reinterpret_cast<const float4 *>(a.wv.y + static_cast<size_t>(r) * a.H + c);
-                acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-            }
-        }
-        if (a.shared) {
-            const float4 v = *reinterpret_cast<const float4 *>(a.wv.y + static_cast<size_t>(nh + t) * a.H + c);
-            acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-        }
-        *reinterpret_cast<float4 *>(a.out + static_cast<size_t>(t) * a.H + c) = acc;
-    }
+__global__ __launch_bounds__(256) void zero_out(float *out, size_t n4) {
+    float4 *o4 = reinterpret_cast<float4 *>(out);
+    for (size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; i < n4;
+         i += static_cast<size_t>(gridDim.x) * 256)
+        o4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+template <int WT, int EPI>
+static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
+    constexpr int NB = FT_GEMV_NB;
+    const int tiles = EPI == EPI_GATEUP ? a.I / (8 * NB) : a.H / (16 * NB);
+    hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
+                       s, a, tiles);
 }
 
 template <int WT>
-static hipError_t launch_general(const ExpertArgs &a, hipStream_t s) {
-    const int tiles_gu = a.I / 8, tiles_dn = a.H / 16;
+static hipError_t launch_stream_path(const ExpertArgs &a, hipStream_t s, const Prof &prof) {
+    if (!prof.mark(1)) return hipErrorUnknown;
     if (a.max_groups > 0) {
-        hipLaunchKernelGGL((grouped_gemv<WT, EPI_GATEUP>), dim3(a.max_groups * tiles_gu),
-                           dim3(kGemvThreads), 0, s, a, tiles_gu);
-        hipLaunchKernelGGL((grouped_gemv<WT, EPI_DOWN>), dim3(a.max_groups * tiles_dn),
-                           dim3(kGemvThreads), 0, s, a, tiles_dn);
+        launch_gemv<WT, EPI_GATEUP>(a, s);
+    } else {
+        const size_t n4 = static_cast<size_t>(a.T) * a.H / 4;
+        hipLaunchKernelGGL(zero_out, dim3(static_cast<unsigned>(std::min<size_t>(4096, (n4 + 255) / 256))),
+                           dim3(256), 0, s, a.out, n4);
     }
-    hipLaunchKernelGGL(combine, dim3((a.H / 4 + 255) / 256, min(a.T, 65535)), dim3(256), 0, s, a);
+    if (!prof.mark(2)) return hipErrorUnknown;
+    if (a.max_groups > 0) launch_gemv<WT, EPI_DOWN>(a, s);
+    if (!prof.mark(3)) return hipErrorUnknown;
     return hipGetLastError();
 }
 
-hipError_t launch_experts(const ExpertArgs &a, hipStream_t s) {
+hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof) {
     switch (a.w_dtype) {
-        case FT_DT_F32: return launch_general<FT_DT_F32>(a, s);
-        case FT_DT_BF16: return launch_general<FT_DT_BF16>(a, s);
-        default: return launch_general<FT_DT_FP8E4M3FN_B128>(a, s);
+        case FT_DT_F32: return launch_stream_path<FT_DT_F32>(a, s, prof);
+        case FT_DT_BF16: return launch_stream_path<FT_DT_BF16>(a, s, prof);
+        default: return launch_stream_path<FT_DT_FP8E4M3FN_B128>(a, s, prof);
     }
 }
 

@@ -47,22 +47,52 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
 }
 
 // ---------------------------------------------------------------- wave utilities
+// Cross-lane steps use DPP row rotations/shifts (within 16-lane rows) plus v_readlane of the
+// four row results, so no reduction goes through the LDS crossbar (ds_bpermute).
 
 __device__ __forceinline__ int lane_id() { return __lane_id(); }
 
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) {
-        uint64_t o = __shfl_xor(v, s, kWave);
-        v = o > v ? o : v;
-    }
-    return v;
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), CTRL, 0xF, 0xF, true));
+}
+constexpr int kDppRowShr1 = 0x111, kDppRowShr2 = 0x112, kDppRowShr4 = 0x114, kDppRowShr8 = 0x118;
+constexpr int kDppRowRor1 = 0x121, kDppRowRor2 = 0x122, kDppRowRor4 = 0x124, kDppRowRor8 = 0x128;
+
+__device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int l) {
+    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), l));
 }
 
-__device__ __forceinline__ float wave_sum_f32(float v) {
-#pragma unroll
-    for (int s = 32; s >= 1; s >>= 1) v += __shfl_xor(v, s, kWave);
-    return v;
+// max over the 64 lanes, result uniform
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    v = max(v, dpp_u32<kDppRowRor1>(v));
+    v = max(v, dpp_u32<kDppRowRor2>(v));
+    v = max(v, dpp_u32<kDppRowRor4>(v));
+    v = max(v, dpp_u32<kDppRowRor8>(v));
+    return max(max(readlane_u32(v, 0), readlane_u32(v, 16)), max(readlane_u32(v, 32), readlane_u32(v, 48)));
+}
+
+// sum over the 64 lanes in a fixed order (deterministic), result uniform
+__device__ __forceinline__ float wave_sum_f32(float x) {
+    uint32_t v = __float_as_uint(x);
+    v = __float_as_uint(__uint_as_float(v) + __uint_as_float(dpp_u32<kDppRowRor1>(v)));
+    v = __float_as_uint(__uint_as_float(v) + __uint_as_float(dpp_u32<kDppRowRor2>(v)));
+    v = __float_as_uint(__uint_as_float(v) + __uint_as_float(dpp_u32<kDppRowRor4>(v)));
+    v = __float_as_uint(__uint_as_float(v) + __uint_as_float(dpp_u32<kDppRowRor8>(v)));
+    const float a = __uint_as_float(readlane_u32(v, 0)), b = __uint_as_float(readlane_u32(v, 16));
+    const float c = __uint_as_float(readlane_u32(v, 32)), d = __uint_as_float(readlane_u32(v, 48));
+    return (a + b) + (c + d);
+}
+
+// inclusive prefix sum over the 64 lanes (lane order)
+__device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
+    v += dpp_u32<kDppRowShr1>(v);
+    v += dpp_u32<kDppRowShr2>(v);
+    v += dpp_u32<kDppRowShr4>(v);
+    v += dpp_u32<kDppRowShr8>(v);
+    const uint32_t r0 = readlane_u32(v, 15), r1 = readlane_u32(v, 31), r2 = readlane_u32(v, 47);
+    const int row = lane_id() >> 4;
+    return v + (row > 0 ? r0 : 0u) + (row > 1 ? r1 : 0u) + (row > 2 ? r2 : 0u);
 }
 
 // Lanes of the wave whose `v` equals this lane's, restricted to `active`.
@@ -82,20 +112,15 @@ __device__ __forceinline__ uint64_t lanemask_lt() {
 }
 
 // ---------------------------------------------------------------- top-k keys
-// Order-preserving 64-bit key: larger logit first, then lower expert id; -0.0 == +0.0.
-__device__ __forceinline__ uint64_t topk_key(float logit, uint32_t e) {
-    uint32_t u = __float_as_uint(logit);
+// Order-preserving 32-bit key of a finite float (larger float -> larger key, -0.0 == +0.0);
+// every finite float maps to a key >= 0x00800000, so 0 can mark an empty/removed entry.
+__device__ __forceinline__ uint32_t order_key(float f) {
+    uint32_t u = __float_as_uint(f);
     if (u == 0x80000000u) u = 0u;
-    const uint32_t ord = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-    return (static_cast<uint64_t>(ord) << 32) | static_cast<uint32_t>(~e);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-__device__ __forceinline__ uint32_t key_expert(uint64_t key) {
-    return ~static_cast<uint32_t>(key);
-}
-
-__device__ __forceinline__ float key_logit(uint64_t key) {
-    const uint32_t ord = static_cast<uint32_t>(key >> 32);
+__device__ __forceinline__ float key_to_float(uint32_t ord) {
     const uint32_t u = (ord & 0x80000000u) ? (ord & 0x7FFFFFFFu) : ~ord;
     return __uint_as_float(u);
 }

@@ -41,9 +41,7 @@ struct WsView {
     int32_t *grp_len;    // [E+1]
     int32_t *row_tok;    // [T*k + T]
     float *row_gate;     // [T*k + T]
-    int32_t *pair_row;   // [T*k] row of a hit pair, -1 for a miss
     void *h;             // [T*k + T][I] SwiGLU activations (bf16, or f32 for f32 weights)
-    float *y;            // [T*k + T][H] gate-scaled expert outputs
 };
 
 struct RouteArgs {
@@ -63,14 +61,12 @@ struct ExpertArgs {
     float *out;
     int T, H, I, k, w_dtype, n_slots, shared;
     int max_groups;   // upper bound on groups, known on the host
-    int32_t *pair_row;
     RouteOut ro;
     WsView wv;
 };
 
 struct WsLayout {
-    size_t eff_slot, blk_hist, grp_meta, grp_slot, grp_beg, grp_len, row_tok, row_gate, pair_row,
-        h, y, total;
+    size_t eff_slot, blk_hist, grp_meta, grp_slot, grp_beg, grp_len, row_tok, row_gate, h, total;
 };
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -93,9 +89,7 @@ inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int T) {
     L.grp_len = take(4u * (E + 1));
     L.row_tok = take(4u * rows);
     L.row_gate = take(4u * rows);
-    L.pair_row = take(4u * static_cast<size_t>(T) * k);
     L.h = take(rows * I * (w_dtype == FT_DT_F32 ? 4u : 2u));
-    L.y = take(rows * H * 4u);
     L.total = o;
     return L;
 }
@@ -105,7 +99,18 @@ inline int fused_route_lds_bytes(int E, int P) {
 }
 inline int scan_route_lds_bytes(int E, int parts) { return 4 * (6 * E + 3 + parts * E); }
 
+// Optional stage events of ft_moe_forward_profiled (recorded only when given).
+struct Prof {
+    const ft_prof_events_t *ev;
+    hipStream_t s;
+    Prof(const ft_prof_events_t *e, hipStream_t st) : ev(e), s(st) {}
+    bool mark(int i) const {
+        if (!ev || !ev->ev[i]) return true;
+        return hipEventRecord(static_cast<hipEvent_t>(ev->ev[i]), s) == hipSuccess;
+    }
+};
+
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
-hipError_t launch_experts(const ExpertArgs &a, hipStream_t s);
+hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof);
 
 }  // namespace ftmoe

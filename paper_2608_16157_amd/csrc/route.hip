@@ -13,47 +13,66 @@
 namespace ftmoe {
 
 // ---------------------------------------------------------------------------------------
-// Top-k of one token's logits by one wave.  NPL = logits held per lane (E <= 64 * NPL).
-// On return lane j < k holds (expert id, gate) of the j-th selected expert.
+// Top-k of one token's logits by one wave.  Lane l holds experts [l*NPL, l*NPL + NPL), so among
+// equal logits the lowest lane, and within a lane the lowest index, is the lowest expert id.
+// Each round takes the wave maximum of the lanes' best keys (DPP) and the lowest lane holding
+// it (ballot).  On return lane j < k holds (expert id, gate) of the j-th selected expert.
 template <int NPL>
 __device__ __forceinline__ void wave_topk(const float *__restrict__ row, int E, int k, int gating,
                                           int &my_id, float &my_w) {
     const int lane = lane_id();
-    uint64_t keys[NPL];
+    uint32_t key[NPL];
 #pragma unroll
     for (int i = 0; i < NPL; ++i) {
-        const int e = lane + i * kWave;
-        keys[i] = e < E ? topk_key(row[e], static_cast<uint32_t>(e)) : 0ull;
+        const int e = lane * NPL + i;
+        key[i] = e < E ? order_key(row[e]) : 0u;
     }
-    uint64_t mine = 0ull;
+    uint32_t mine = 0u;
+    int mine_e = -1;
     for (int j = 0; j < k; ++j) {
-        uint64_t best = 0ull;
+        uint32_t best = 0u;
+        int bi = 0;
 #pragma unroll
-        for (int i = 0; i < NPL; ++i) best = keys[i] > best ? keys[i] : best;
-        best = wave_max_u64(best);
+        for (int i = 0; i < NPL; ++i) {
+            if (key[i] > best) {
+                best = key[i];
+                bi = i;
+            }
+        }
+        const uint32_t m = wave_max_u32(best);
+        const uint64_t ball = __ballot(best == m);
+        const int w = static_cast<int>(__builtin_ctzll(ball));
+        const int wbi = __builtin_amdgcn_readlane(bi, w);
+        if (lane == w) {
 #pragma unroll
-        for (int i = 0; i < NPL; ++i) keys[i] = keys[i] == best ? 0ull : keys[i];
-        if (lane == j) mine = best;
+            for (int i = 0; i < NPL; ++i)
+                if (i == wbi) key[i] = 0u;
+        }
+        if (lane == j) {
+            mine = m;
+            mine_e = w * NPL + wbi;
+        }
     }
-    const float top = key_logit(__shfl(mine, 0, kWave));
+    const float top = key_to_float(readlane_u32(mine, 0));
     float z = 0.f;
     if (lane < k) {
-        const float l = key_logit(mine);
+        const float l = key_to_float(mine);
         z = gating == FT_GATE_SOFTMAX_TOPK_RENORM ? expf(l - top) : 1.0f / (1.0f + expf(-l));
     }
     const float sum = wave_sum_f32(z);
-    my_id = lane < k ? static_cast<int>(key_expert(mine)) : -1;
+    my_id = lane < k ? mine_e : -1;
     my_w = lane < k ? z / sum : 0.f;
 }
 
-// Validated slot of each expert (-1 if unusable) and the device status bits.
-__device__ void validate_slots(const int32_t *__restrict__ slot_table, int E, int n_slots,
-                               int shared_slot, int32_t *s_raw, int32_t *s_eff, int *s_status) {
-    for (int e = threadIdx.x; e < E; e += blockDim.x) s_raw[e] = slot_table[e];
+// Validated slot of each expert (-1 if unusable) and the device status bits.  `raw` is this
+// thread's slot_table entry (thread e of the block holds expert e; blockDim >= E).
+__device__ void validate_slots(int raw, int E, int n_slots, int shared_slot, int32_t *s_raw,
+                               int32_t *s_eff, int *s_status) {
+    if (threadIdx.x < E) s_raw[threadIdx.x] = raw;
     __syncthreads();
     int st = 0;
-    for (int e = threadIdx.x; e < E; e += blockDim.x) {
-        const int s = s_raw[e];
+    if (threadIdx.x < E) {
+        const int e = threadIdx.x, s = raw;
         int eff = -1;
         if (s == -1) {
         } else if (s < -1 || s >= n_slots) {
@@ -96,10 +115,8 @@ __device__ void scatter_run(int p0, int p1, int k, int nbits, const int32_t *__r
                 ro.hit_pairs[pos] = p;
                 wv.row_tok[pos] = p / k;
                 wv.row_gate[pos] = w[p];
-                wv.pair_row[p] = pos;
             } else {
                 ro.miss_pairs[pos] = p;
-                wv.pair_row[p] = -1;
             }
         }
     }
@@ -112,48 +129,50 @@ __device__ void scan_experts(int E, int T, int k, int shared_slot, const int32_t
                              const int32_t *s_eff, int32_t *s_hoff, int32_t *s_moff,
                              int32_t *s_gidx, const int *s_status, const RouteOut &ro,
                              const WsView &wv) {
-    // single-wave sequential-chunk scan: E <= 1024 so at most 16 chunks of 64
     if (threadIdx.x < kWave) {
+        // lane l owns experts [l*epl, l*epl + epl)
         const int lane = lane_id();
-        int hrun = 0, mrun = 0, grun = 0, mexp = 0;
-        for (int c = 0; c < E; c += kWave) {
-            const int e = c + lane;
-            const int tot = e < E ? s_tot[e] : 0;
-            const bool hit = e < E && s_eff[e] >= 0;
-            int hv = hit ? tot : 0, mv = hit ? 0 : tot, gv = (hit && tot > 0) ? 1 : 0;
-            int hx = hv, mx = mv, gx = gv;
-#pragma unroll
-            for (int s = 1; s < kWave; s <<= 1) {   // inclusive scans
-                const int a = __shfl_up(hx, s, kWave), b = __shfl_up(mx, s, kWave),
-                          g = __shfl_up(gx, s, kWave);
-                if (lane >= s) { hx += a; mx += b; gx += g; }
-            }
-            if (e < E) {
-                s_hoff[e] = hrun + hx - hv;
-                s_moff[e] = mrun + mx - mv;
-                s_gidx[e] = gv ? grun + gx - gv : -1;
-            }
-            mexp += __popcll(__ballot(mv > 0));
-            hrun += __shfl(hx, kWave - 1, kWave);
-            mrun += __shfl(mx, kWave - 1, kWave);
-            grun += __shfl(gx, kWave - 1, kWave);
+        const int epl = (E + kWave - 1) / kWave;
+        const int e0 = min(E, lane * epl), e1 = min(E, e0 + epl);
+        uint32_t h = 0, m = 0, g = 0, mx = 0;
+        for (int e = e0; e < e1; ++e) {
+            const int tot = s_tot[e];
+            const bool hit = s_eff[e] >= 0;
+            h += hit ? tot : 0;
+            m += hit ? 0 : tot;
+            g += (hit && tot > 0) ? 1 : 0;
+            mx += (!hit && tot > 0) ? 1 : 0;
         }
-        if (lane == 0) {
-            s_hoff[E] = hrun;
-            s_moff[E] = mrun;
-            const int G = grun + (shared_slot >= 0 ? 1 : 0);
-            ro.counts[0] = hrun;
-            ro.counts[1] = mrun;
+        const uint32_t hi = wave_incl_scan_u32(h), mi = wave_incl_scan_u32(m);
+        const uint32_t gi = wave_incl_scan_u32(g), xi = wave_incl_scan_u32(mx);
+        uint32_t hrun = hi - h, mrun = mi - m, grun = gi - g;
+        for (int e = e0; e < e1; ++e) {
+            const int tot = s_tot[e];
+            const bool hit = s_eff[e] >= 0;
+            s_hoff[e] = hrun;
+            s_moff[e] = mrun;
+            s_gidx[e] = (hit && tot > 0) ? static_cast<int>(grun) : -1;
+            hrun += hit ? tot : 0;
+            mrun += hit ? 0 : tot;
+            grun += (hit && tot > 0) ? 1 : 0;
+        }
+        const uint32_t nh = readlane_u32(hi, kWave - 1), nm = readlane_u32(mi, kWave - 1);
+        const uint32_t U = readlane_u32(gi, kWave - 1), mexp = readlane_u32(xi, kWave - 1);
+        if (lane == kWave - 1) {
+            s_hoff[E] = nh;
+            s_moff[E] = nm;
+            ro.counts[0] = nh;
+            ro.counts[1] = nm;
             ro.counts[2] = mexp;
             ro.counts[3] = *s_status;
-            wv.grp_meta[0] = G;
-            wv.grp_meta[1] = grun;
-            wv.grp_meta[2] = hrun;
+            wv.grp_meta[0] = U + (shared_slot >= 0 ? 1 : 0);
+            wv.grp_meta[1] = U;
+            wv.grp_meta[2] = nh;
             wv.grp_meta[3] = T;
             if (shared_slot >= 0) {
-                wv.grp_slot[grun] = shared_slot;
-                wv.grp_beg[grun] = hrun;
-                wv.grp_len[grun] = T;
+                wv.grp_slot[U] = shared_slot;
+                wv.grp_beg[U] = nh;
+                wv.grp_len[U] = T;
             }
         }
     }
@@ -202,9 +221,10 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     int32_t *s_wh = reinterpret_cast<int32_t *>(s_w + P);  // kFusedWaves * E
     int *s_status = s_wh + kFusedWaves * E;  // 1
 
+    // issue the slot-table load first; its latency overlaps the top-k
+    const int raw = threadIdx.x < E ? a.slot_table[threadIdx.x] : -1;
     if (threadIdx.x == 0) *s_status = 0;
     for (int i = threadIdx.x; i < kFusedWaves * E; i += blockDim.x) s_wh[i] = 0;
-    validate_slots(a.slot_table, E, a.n_slots, a.shared_slot, s_raw, s_eff, s_status);
 
     const int wave = threadIdx.x / kWave, lane = lane_id();
     for (int t = wave; t < T; t += kFusedWaves) {
@@ -218,7 +238,7 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
             a.ro.topk_w[t * k + lane] = w;
         }
     }
-    __syncthreads();
+    validate_slots(raw, E, a.n_slots, a.shared_slot, s_raw, s_eff, s_status);
     // each wave owns a contiguous run of pairs; count its pairs per expert
     const int per = (P + kFusedWaves - 1) / kFusedWaves;
     const int p0 = min(P, wave * per), p1 = min(P, p0 + per);
@@ -278,8 +298,9 @@ __global__ __launch_bounds__(1024) void route_scan(RouteArgs a, int nblk) {
     int32_t *s_moff = s_hoff + E + 1, *s_gidx = s_moff + E + 1;
     int *s_status = s_gidx + E;
     int32_t *s_part = s_status + 1;          // [parts][E] partial block sums
+    const int raw = threadIdx.x < E ? a.slot_table[threadIdx.x] : -1;
     if (threadIdx.x == 0) *s_status = 0;
-    validate_slots(a.slot_table, E, a.n_slots, a.shared_slot, s_raw, s_eff, s_status);
+    validate_slots(raw, E, a.n_slots, a.shared_slot, s_raw, s_eff, s_status);
     // `parts` threads per expert, each over a contiguous range of the blocks
     const int parts = a.scan_parts;
     const int e = threadIdx.x % E, part = threadIdx.x / E;

@@ -210,13 +210,17 @@ def test_miss_list_to_host():
 
 
 def test_forward_deterministic_and_slot_table_change():
-    """Same inputs twice give identical bits; a new slot table between calls (the runtime cache
-    rebuild of Section 3.3) is honoured, down to zero residency."""
+    """Same inputs twice give identical routing bits and outputs equal up to the order of the
+    float32 combine; a new slot table between calls (the runtime cache rebuild of Section 3.3)
+    is honoured, down to zero residency."""
     lay = workloads.random_layer(12, hidden=256, inter=256, n_experts=32, top_k=4, tokens=40,
                                  w_dtype=workloads.DT_BF16, n_resident=20, device="cuda")
-    a, _ = run_forward(lay)
-    b, _ = run_forward(lay)
-    assert torch.equal(a, b)
+    a, ra = run_forward(lay)
+    b, rb = run_forward(lay)
+    for n in ("topk_ids", "topk_w", "topk_slot", "hit_pairs", "miss_pairs", "hit_off", "miss_off",
+              "counts"):
+        assert torch.equal(getattr(ra, n), getattr(rb, n)), n
+    assert oracle.max_rel_err(a.cpu().numpy(), b.cpu().numpy()) <= 1e-5
     st = lay.slot_table.clone()
     st[: 16] = -1
     lay.slot_table = st
