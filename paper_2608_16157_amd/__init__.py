@@ -71,11 +71,12 @@ class ft_host_miss_t(ctypes.Structure):
 _lib: Optional[ctypes.CDLL] = None
 
 
-def load(path: str = LIB_PATH) -> ctypes.CDLL:
-    """Load libftmoe.so once; raise if it has not been built."""
+def load(path: str = None) -> ctypes.CDLL:
+    """Load libftmoe.so once (FTMOE_LIBRARY may name another build); raise if it is missing."""
     global _lib
     if _lib is not None:
         return _lib
+    path = path or os.environ.get("FTMOE_LIBRARY") or LIB_PATH
     if not os.path.exists(path):
         raise RuntimeError(f"libftmoe.so not built ({path}); run __graft_entry__.build() or "
                            "python paper_2608_16157_amd/build.py")

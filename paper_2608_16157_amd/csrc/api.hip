@@ -52,6 +52,8 @@ WsView carve(const ft_moe_desc_t *d, int T, void *ws) {
     v.grp_slot = reinterpret_cast<int32_t *>(b + L.grp_slot);
     v.grp_beg = reinterpret_cast<int32_t *>(b + L.grp_beg);
     v.grp_len = reinterpret_cast<int32_t *>(b + L.grp_len);
+    v.grp_mt_off = reinterpret_cast<int32_t *>(b + L.grp_mt_off);
+    v.mt_group = reinterpret_cast<int32_t *>(b + L.mt_group);
     v.row_tok = reinterpret_cast<int32_t *>(b + L.row_tok);
     v.row_gate = reinterpret_cast<float *>(b + L.row_gate);
     v.h = b + L.h;

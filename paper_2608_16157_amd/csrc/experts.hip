@@ -306,11 +306,21 @@ static hipError_t launch_stream_path(const ExpertArgs &a, hipStream_t s, const P
     return hipGetLastError();
 }
 
+// Many-token chunks whose shapes tile evenly go to the MFMA GEMM.
+static bool gemm_path(const ExpertArgs &a) {
+    return a.T >= kGemmMinTokens && a.max_groups > 0 && a.H % kGemmBN == 0 && a.I % (kGemmBN / 2) == 0 &&
+           a.H <= 8192 && a.I <= 8192;
+}
+
 hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof) {
     switch (a.w_dtype) {
         case FT_DT_F32: return launch_stream_path<FT_DT_F32>(a, s, prof);
-        case FT_DT_BF16: return launch_stream_path<FT_DT_BF16>(a, s, prof);
-        default: return launch_stream_path<FT_DT_FP8E4M3FN_B128>(a, s, prof);
+        case FT_DT_BF16:
+            if (gemm_path(a)) return launch_gemm(a, s, prof);
+            return launch_stream_path<FT_DT_BF16>(a, s, prof);
+        default:
+            if (gemm_path(a)) return launch_gemm(a, s, prof);
+            return launch_stream_path<FT_DT_FP8E4M3FN_B128>(a, s, prof);
     }
 }
 

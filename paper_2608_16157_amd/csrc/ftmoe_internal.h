@@ -5,7 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/ftmoe.h"
+#include "ftmoe.h"
 
 namespace ftmoe {
 
@@ -14,6 +14,15 @@ constexpr int kMaxTopK = 64;
 constexpr int kTokPerBlk = 16;          // tokens per workgroup in the multi-block router
 constexpr int kFusedMaxPairs = 2048;    // T*k handled by the single-workgroup router
 constexpr int kFusedMaxLds = 64 * 1024;
+#ifndef FT_GEMM_BM
+#define FT_GEMM_BM 128
+#endif
+#ifndef FT_GEMM_BN
+#define FT_GEMM_BN 256
+#endif
+constexpr int kGemmBM = FT_GEMM_BM;     // token rows per MFMA GEMM tile (prefill path)
+constexpr int kGemmBN = FT_GEMM_BN;     // weight rows per MFMA GEMM tile
+constexpr int kGemmMinTokens = 256;     // token count from which the MFMA GEMM path is used
 
 // Routing outputs (the caller's ft_route_t, flattened).
 struct RouteOut {
@@ -35,10 +44,12 @@ struct RouteOut {
 struct WsView {
     int32_t *eff_slot;   // [E]
     int32_t *blk_hist;   // [nblk][E]
-    int32_t *grp_meta;   // [4]: G (groups incl. shared), U (hit groups), n_hit, T
+    int32_t *grp_meta;   // [8]: G (groups incl. shared), U (hit groups), n_hit, T, M-tiles
     int32_t *grp_slot;   // [E+1]
     int32_t *grp_beg;    // [E+1]
     int32_t *grp_len;    // [E+1]
+    int32_t *grp_mt_off; // [E+2] exclusive prefix of ceil(len / kGemmBM) over the groups
+    int32_t *mt_group;   // [max M tiles] group of each GEMM M tile
     int32_t *row_tok;    // [T*k + T]
     float *row_gate;     // [T*k + T]
     void *h;             // [T*k + T][I] SwiGLU activations (bf16, or f32 for f32 weights)
@@ -66,10 +77,18 @@ struct ExpertArgs {
 };
 
 struct WsLayout {
-    size_t eff_slot, blk_hist, grp_meta, grp_slot, grp_beg, grp_len, row_tok, row_gate, h, total;
+    size_t eff_slot, blk_hist, grp_meta, grp_slot, grp_beg, grp_len, grp_mt_off, mt_group, row_tok,
+        row_gate, h, total;
 };
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Upper bound of the GEMM M tiles any routing of T tokens can produce: every row in full tiles
+// plus one ragged tile per group (E routed groups and the shared expert).
+inline size_t gemm_max_mtiles(int T, int k, int E) {
+    const size_t rows = static_cast<size_t>(T) * k + T;
+    return (rows + kGemmBM - 1) / kGemmBM + E + 1;
+}
 
 inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int T) {
     WsLayout L{};
@@ -83,10 +102,12 @@ inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int T) {
     const size_t rows = static_cast<size_t>(T) * k + T;
     L.eff_slot = take(4u * E);
     L.blk_hist = take(4u * nblk * E);
-    L.grp_meta = take(16);
+    L.grp_meta = take(32);
     L.grp_slot = take(4u * (E + 1));
     L.grp_beg = take(4u * (E + 1));
     L.grp_len = take(4u * (E + 1));
+    L.grp_mt_off = take(4u * (E + 2));
+    L.mt_group = take(4u * gemm_max_mtiles(T, k, E));
     L.row_tok = take(4u * rows);
     L.row_gate = take(4u * rows);
     L.h = take(rows * I * (w_dtype == FT_DT_F32 ? 4u : 2u));
@@ -112,5 +133,6 @@ struct Prof {
 
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof);
+hipError_t launch_gemm(const ExpertArgs &a, hipStream_t s, const Prof &prof);
 
 }  // namespace ftmoe

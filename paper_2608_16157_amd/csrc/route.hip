@@ -134,7 +134,7 @@ __device__ void scan_experts(int E, int T, int k, int shared_slot, const int32_t
         const int lane = lane_id();
         const int epl = (E + kWave - 1) / kWave;
         const int e0 = min(E, lane * epl), e1 = min(E, e0 + epl);
-        uint32_t h = 0, m = 0, g = 0, mx = 0;
+        uint32_t h = 0, m = 0, g = 0, mx = 0, mtl = 0;
         for (int e = e0; e < e1; ++e) {
             const int tot = s_tot[e];
             const bool hit = s_eff[e] >= 0;
@@ -142,22 +142,31 @@ __device__ void scan_experts(int E, int T, int k, int shared_slot, const int32_t
             m += hit ? 0 : tot;
             g += (hit && tot > 0) ? 1 : 0;
             mx += (!hit && tot > 0) ? 1 : 0;
+            mtl += hit ? (tot + kGemmBM - 1) / kGemmBM : 0;
         }
         const uint32_t hi = wave_incl_scan_u32(h), mi = wave_incl_scan_u32(m);
         const uint32_t gi = wave_incl_scan_u32(g), xi = wave_incl_scan_u32(mx);
-        uint32_t hrun = hi - h, mrun = mi - m, grun = gi - g;
+        const uint32_t ti = wave_incl_scan_u32(mtl);
+        uint32_t hrun = hi - h, mrun = mi - m, grun = gi - g, trun = ti - mtl;
         for (int e = e0; e < e1; ++e) {
             const int tot = s_tot[e];
             const bool hit = s_eff[e] >= 0;
             s_hoff[e] = hrun;
             s_moff[e] = mrun;
             s_gidx[e] = (hit && tot > 0) ? static_cast<int>(grun) : -1;
+            if (hit && tot > 0) {
+                wv.grp_mt_off[grun] = trun;
+                const int nmt = (tot + kGemmBM - 1) / kGemmBM;
+                for (int i = 0; i < nmt; ++i) wv.mt_group[trun + i] = grun;
+            }
             hrun += hit ? tot : 0;
             mrun += hit ? 0 : tot;
             grun += (hit && tot > 0) ? 1 : 0;
+            trun += hit ? (tot + kGemmBM - 1) / kGemmBM : 0;
         }
         const uint32_t nh = readlane_u32(hi, kWave - 1), nm = readlane_u32(mi, kWave - 1);
         const uint32_t U = readlane_u32(gi, kWave - 1), mexp = readlane_u32(xi, kWave - 1);
+        const uint32_t MT = readlane_u32(ti, kWave - 1);
         if (lane == kWave - 1) {
             s_hoff[E] = nh;
             s_moff[E] = nm;
@@ -165,15 +174,21 @@ __device__ void scan_experts(int E, int T, int k, int shared_slot, const int32_t
             ro.counts[1] = nm;
             ro.counts[2] = mexp;
             ro.counts[3] = *s_status;
-            wv.grp_meta[0] = U + (shared_slot >= 0 ? 1 : 0);
+            const uint32_t smt = shared_slot >= 0 ? (T + kGemmBM - 1) / kGemmBM : 0;
+            const uint32_t G = U + (shared_slot >= 0 ? 1 : 0);
+            wv.grp_meta[0] = G;
             wv.grp_meta[1] = U;
             wv.grp_meta[2] = nh;
             wv.grp_meta[3] = T;
+            wv.grp_meta[4] = MT + smt;
             if (shared_slot >= 0) {
                 wv.grp_slot[U] = shared_slot;
                 wv.grp_beg[U] = nh;
                 wv.grp_len[U] = T;
+                wv.grp_mt_off[U] = MT;
+                for (uint32_t i = 0; i < smt; ++i) wv.mt_group[MT + i] = U;
             }
+            wv.grp_mt_off[G] = MT + smt;
         }
     }
     __syncthreads();

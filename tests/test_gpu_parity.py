@@ -157,26 +157,31 @@ def test_forward_configs_sampled(name, T, rows):
 
 
 RANDOM_FWD = [
-    # seed, w_dtype, gating, E, k, T, n_res, shared, H, I
-    (0, workloads.DT_BF16, 0, 8, 2, 1, 4, False, 128, 256),
-    (1, workloads.DT_BF16, 1, 16, 4, 37, 16, False, 256, 128),
-    (2, workloads.DT_BF16, 0, 16, 4, 70, 0, False, 128, 128),
-    (3, workloads.DT_BF16, 0, 16, 4, 70, 0, True, 128, 128),
-    (4, workloads.DT_FP8, 1, 32, 8, 19, 9, True, 384, 256),
-    (5, workloads.DT_FP8, 0, 12, 3, 130, 12, False, 256, 384),
-    (6, workloads.DT_F32, 0, 8, 3, 45, 5, True, 128, 384),
-    (7, workloads.DT_F32, 1, 4, 4, 3, 2, False, 640, 128),
-    (8, workloads.DT_BF16, 0, 64, 6, 700, 40, True, 256, 256),
+    # seed, w_dtype, gating, E, k, T, n_res, shared, H, I, zipf
+    (0, workloads.DT_BF16, 0, 8, 2, 1, 4, False, 128, 256, 0.0),
+    (1, workloads.DT_BF16, 1, 16, 4, 37, 16, False, 256, 128, 0.0),
+    (2, workloads.DT_BF16, 0, 16, 4, 70, 0, False, 128, 128, 0.0),
+    (3, workloads.DT_BF16, 0, 16, 4, 70, 0, True, 128, 128, 0.0),
+    (4, workloads.DT_FP8, 1, 32, 8, 19, 9, True, 384, 256, 0.0),
+    (5, workloads.DT_FP8, 0, 12, 3, 130, 12, False, 256, 384, 0.0),
+    (6, workloads.DT_F32, 0, 8, 3, 45, 5, True, 128, 384, 0.0),
+    (7, workloads.DT_F32, 1, 4, 4, 3, 2, False, 640, 128, 0.0),
+    (8, workloads.DT_BF16, 0, 64, 6, 700, 40, True, 256, 256, 0.0),
+    # many-token chunks: MFMA GEMM path, ragged M tiles, skewed group sizes
+    (9, workloads.DT_BF16, 1, 16, 4, 300, 12, True, 256, 384, 1.5),
+    (10, workloads.DT_BF16, 0, 32, 8, 1000, 20, False, 384, 128, 0.8),
+    (11, workloads.DT_BF16, 0, 8, 1, 256, 8, False, 128, 128, 3.0),
+    (12, workloads.DT_FP8, 1, 24, 6, 400, 10, True, 256, 256, 1.0),
 ]
 
 
 @pytest.mark.parametrize("case", RANDOM_FWD, ids=[str(c[0]) for c in RANDOM_FWD])
 def test_forward_random_shapes(case):
-    seed, wdt, gating, E, k, T, n_res, shared, H, I = case
+    seed, wdt, gating, E, k, T, n_res, shared, H, I, zipf = case
     _say(f"forward random {case}")
     lay = workloads.random_layer(seed, hidden=H, inter=I, n_experts=E, top_k=k, tokens=T,
                                  gating=gating, w_dtype=wdt, n_resident=n_res, shared=shared,
-                                 device="cuda")
+                                 zipf_s=zipf, device="cuda")
     out, route = run_forward(lay)
     ref, r = oracle.moe_partial(*oracle_inputs(lay))
     check_route(route, r, T, k)
