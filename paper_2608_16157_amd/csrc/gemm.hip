@@ -6,24 +6,30 @@
 //   gate/up: h[rows of g] = silu(X_g W1^T) * (X_g W3^T)       tile = BM rows x BN/2 h columns
 //   down   : out[tok] += gate * (h_g W2^T)                    tile = BM rows x BN out columns
 //
-// Work decomposition.  One workgroup (8 waves, BM/64 x BN/64 over the tile, 64 x 64 each as
+// Work decomposition.  One workgroup of 4 waves (BM/64 x BN/64 over the tile, 64 x 64 each as
 // 2 x 2 MFMA 32x32x16 tiles, the bf16 MFMA shape with the highest measured throughput on
-// gfx950) per (group, BM-row M tile, N tile).  Tiles are enumerated on the device from
-// the per-group M-tile prefix the router writes: group-major, then N tile, then M tile, so the
-// M tiles sharing a weight tile run back to back, and the block -> tile map keeps consecutive
-// tiles on one XCD (workgroups are dealt to the 8 XCDs round-robin) to share its L2.
+// gfx950) per (group, BM-row M tile, N tile).  Two workgroups share a CU, so one multiplies
+// while the other waits at a stage barrier or runs its prologue or epilogue.  Tiles are
+// enumerated M-tile-major with the N tile fastest, through the per-M-tile group map the router
+// writes, so the N tiles of one M tile (sharing activation rows) and the M tiles of one group
+// (sharing weight tiles) run close together; the block -> tile map keeps consecutive tiles on
+// one XCD (workgroups are dealt to the 8 XCDs round-robin) to share its L2.
 //
 // Data movement.  A (activation rows, gathered through row_tok for gate/up) and B (weight rows,
 // kept in their storage format: bf16, or fp8 widened to bf16 only when read for the MFMA) go
 // straight from global memory into LDS with global_load_lds (16 bytes per lane), through a ring
-// of 3 stages of 64 K each, two stages in flight while one is multiplied.  Every LDS row keeps
-// its 16-byte chunks XOR-swizzled by the row index, so MFMA operand reads of consecutive rows
-// hit distinct banks.  The stage hand-off is an explicit vmcnt wait plus s_barrier (a
-// __syncthreads would drain every in-flight stage).
+// of NS stages of BK K-values, NS - 1 stages in flight while one is multiplied.  Every LDS row
+// keeps its 16-byte chunks XOR-swizzled by the row index, so MFMA operand reads of consecutive
+// rows hit distinct banks.  The stage hand-off is an explicit vmcnt wait plus s_barrier (a
+// __syncthreads would drain every stage in flight).  The ring is unrolled and every stage buffer
+// is an array of its own, so the compiler can tell the stage being read from the stages still
+// being written and adds no wait of its own.
 //
 // fp8 weights carry one float32 scale per 128 x 128 block: partial sums of each 128-wide K
 // block are scaled once and added to the accumulators.  The gate/up B tile puts each wave's 32
 // gate rows next to the 32 matching up rows, so SiLU(gate) * up is formed in registers.
+#include <type_traits>
+
 #include "ftmoe_device.h"
 #include "ftmoe_internal.h"
 
@@ -31,32 +37,50 @@ namespace ftmoe {
 
 constexpr int kBM = kGemmBM;          // token rows per tile
 constexpr int kBN = kGemmBN;          // weight rows per tile
+constexpr int kGemmThreads = 256;
+constexpr int kGemmWaves = kGemmThreads / kWave;
 constexpr int kWavesN = kBN / 64;     // waves across N, 64 columns each
 constexpr int kWavesM = kBM / 64;     // waves across M, 64 rows each
-constexpr int kBK = 64;               // K elements per stage
-constexpr int kStages = 3;
-constexpr int kGemmThreads = 512;
-constexpr int kGemmWaves = kGemmThreads / kWave;
-constexpr int kARowBytes = kBK * 2;   // bf16 activations: 128 bytes per row per stage
-constexpr int kAStage = kBM * kARowBytes;
-static_assert(kWavesN * kWavesM == kGemmThreads / 64, "8 waves of 64 x 64");
+static_assert(kWavesN * kWavesM == kGemmWaves, "4 waves of 64 x 64");
+#ifndef FT_GEMM_BAND
+#define FT_GEMM_BAND 8
+#endif
+constexpr int kBandM = FT_GEMM_BAND;  // M tiles that run together on each weight tile
 
 enum { GEMM_GATEUP = 0, GEMM_DOWN = 1 };
 
+// Per weight format: K values per stage and ring depth (two workgroups of either fit one CU's
+// LDS), bytes per weight element.
 template <int WT> struct GTr;
+#ifndef FT_GEMM_BF16_BK
+#define FT_GEMM_BF16_BK 32
+#endif
+#ifndef FT_GEMM_BF16_NS
+#define FT_GEMM_BF16_NS 4
+#endif
+#ifndef FT_GEMM_FP8_BK
+#define FT_GEMM_FP8_BK 64
+#endif
+#ifndef FT_GEMM_FP8_NS
+#define FT_GEMM_FP8_NS 3
+#endif
 template <> struct GTr<FT_DT_BF16> {
-    static constexpr int kRowBytes = kBK * 2;          // 128
-    static constexpr int kChunks = kRowBytes / 16;     // 8 chunks per row
-    static constexpr int kBStage = kBN * kRowBytes;
-    static constexpr int kBInstr = kBStage / 1024 / kGemmWaves;   // DMA instructions per wave
+    static constexpr int BK = FT_GEMM_BF16_BK, NS = FT_GEMM_BF16_NS, kWb = 2;
 };
 template <> struct GTr<FT_DT_FP8E4M3FN_B128> {
-    static constexpr int kRowBytes = kBK;              // 64
-    static constexpr int kChunks = kRowBytes / 16;     // 4
-    static constexpr int kBStage = kBN * kRowBytes;
-    static constexpr int kBInstr = kBStage / 1024 / kGemmWaves;
+    static constexpr int BK = FT_GEMM_FP8_BK, NS = FT_GEMM_FP8_NS, kWb = 1;
 };
-constexpr int kAInstr = kAStage / 1024 / kGemmWaves;
+
+template <int V> using ic = std::integral_constant<int, V>;
+
+// Calls f(ic<S>) for S = B .. E-1.
+template <int B, int E, class F>
+__device__ __forceinline__ void static_for(F &&f) {
+    if constexpr (B < E) {
+        f(ic<B>{});
+        static_for<B + 1, E>(f);
+    }
+}
 
 // Block index -> logical tile index such that logical tiles [x*q + min(x,r), ...) run on XCD x.
 __device__ __forceinline__ int xcd_remap(int b, int n) {
@@ -78,33 +102,63 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 
 // Workgroup barrier between pipeline stages.  The empty asm statements are compiler-level memory
 // fences: they keep LDS reads of a stage from being moved across the barrier, without the
-// wait-for-everything a __syncthreads fence would add.
+// wait-for-everything a __syncthreads fence adds.
 __device__ __forceinline__ void stage_barrier() {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
 }
 
-// 16-byte chunk position of chunk c in LDS row r.  A 128-byte row covers half of the 64 x 4-byte
-// banks, so rows r and r+1 already sit in opposite halves; XOR with (r / 2) mod 8 then gives the
-// 16 rows an MFMA operand read touches 16 distinct bank groups.  A 64-byte (fp8) row covers a
-// quarter of the banks, hence (r / 4) mod 4.
-__device__ __forceinline__ int swz128(int r, int c) { return c ^ ((r >> 1) & 7); }
-__device__ __forceinline__ int swz64(int r, int c) { return c ^ ((r >> 2) & 3); }
+// Position of 16-byte chunk c in LDS row r.  A 128-byte row covers half of the 64 x 4-byte banks
+// and a 64-byte row a quarter, so XOR with (r / 2) mod 8, resp. (r / 4) mod 4, puts the same
+// chunk of 16 consecutive rows into distinct bank groups.
+template <int ROW_BYTES>
+__device__ __forceinline__ int swz(int r, int c) {
+    static_assert(ROW_BYTES == 64 || ROW_BYTES == 128, "row size");
+    if constexpr (ROW_BYTES == 128) return c ^ ((r >> 1) & 7);
+    else return c ^ ((r >> 2) & 3);
+}
 
 __device__ __forceinline__ void dma16(const void *g, uint8_t *lds_block) {
     __builtin_amdgcn_global_load_lds(g, (lds_void_t *)(lds_block), 16, 0, 0);
 }
 
 template <int WT, int EPI>
-__global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm(ExpertArgs a, int ntn) {
-    using Tr = GTr<WT>;
-    // three separately declared stage buffers: with the loop unrolled by three every LDS read and
-    // every DMA target is a distinct object, so the compiler's wait-count pass can tell that the
-    // stage being read does not alias the stages still being written
-    __shared__ __attribute__((aligned(1024))) uint8_t sA0[kAStage], sA1[kAStage], sA2[kAStage];
-    __shared__ __attribute__((aligned(1024))) uint8_t sB0[Tr::kBStage], sB1[Tr::kBStage], sB2[Tr::kBStage];
-    static_assert(kStages == 3, "the stage ring is unrolled by three");
+__global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, int ntn) {
+    constexpr int BK = GTr<WT>::BK, NS = GTr<WT>::NS;
+    constexpr int ARB = BK * 2;                      // A row bytes per stage (bf16)
+    constexpr int BRB = BK * GTr<WT>::kWb;           // B row bytes per stage
+    constexpr int ASTAGE = kBM * ARB, BSTAGE = kBN * BRB;
+    constexpr int A_INSTR = ASTAGE / 1024 / kGemmWaves;   // 1 KB DMA instructions per wave
+    constexpr int B_INSTR = BSTAGE / 1024 / kGemmWaves;
+    constexpr int PER_STAGE = A_INSTR + B_INSTR;
+    static_assert(A_INSTR >= 1 && B_INSTR >= 1, "stage too small");
+    static_assert(NS >= 2 && NS <= 4, "ring depth");
+    static_assert((NS - 1) * PER_STAGE < 64, "vmcnt range");
+    // one array per stage (see the header comment); the fourth is unused with a 3-deep ring
+    __shared__ __attribute__((aligned(1024))) uint8_t sA0[ASTAGE], sA1[ASTAGE], sA2[ASTAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t sA3[NS > 3 ? ASTAGE : 16];
+    __shared__ __attribute__((aligned(1024))) uint8_t sB0[BSTAGE], sB1[BSTAGE], sB2[BSTAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t sB3[NS > 3 ? BSTAGE : 16];
+    constexpr int kMaxKb = 64;                       // K <= 8192
+    __shared__ float s_scale[kWavesN][2][kMaxKb];
+    __shared__ int32_t s_tok[kBM];
+    __shared__ float s_gate[kBM];
+    auto stA = [&](auto s) -> uint8_t * {
+        constexpr int S = decltype(s)::value;
+        if constexpr (S == 0) return sA0;
+        else if constexpr (S == 1) return sA1;
+        else if constexpr (S == 2) return sA2;
+        else return sA3;
+    };
+    auto stB = [&](auto s) -> uint8_t * {
+        constexpr int S = decltype(s)::value;
+        if constexpr (S == 0) return sB0;
+        else if constexpr (S == 1) return sB1;
+        else if constexpr (S == 2) return sB2;
+        else return sB3;
+    };
+
     const int t = threadIdx.x;
     if constexpr (EPI == GEMM_GATEUP) {
         // zero the output that the down projection accumulates into
@@ -117,11 +171,15 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm(ExpertArgs a, in
     const int L = xcd_remap(blockIdx.x, gridDim.x);
     const int MTT = a.wv.grp_meta[4];
     if (L >= MTT * ntn) return;
-    // tiles run M-tile-major with the N tile fastest: the N tiles of one M tile (sharing its
-    // activation rows) and the M tiles of one group (sharing its weight tiles) sit close together
-    const int mtg = L / ntn, nt = L % ntn;
-    const int g = a.wv.mt_group[mtg];
-    const int mt = mtg - a.wv.grp_mt_off[g];
+    // group g owns logical tiles [off_g * ntn, off_{g+1} * ntn), so L / ntn is one of its M tiles;
+    // inside the group, bands of up to kBandM M tiles, each band N-tile-major with the M tile
+    // fastest
+    const int g = a.wv.mt_group[L / ntn];
+    const int off = a.wv.grp_mt_off[g], mtc = a.wv.grp_mt_off[g + 1] - off;
+    const int local = L - off * ntn;
+    const int band = local / (kBandM * ntn), rem = local - band * (kBandM * ntn);
+    const int bm = min(kBandM, mtc - band * kBandM);
+    const int nt = rem / bm, mt = band * kBandM + rem % bm;
     const int slot = a.wv.grp_slot[g], beg = a.wv.grp_beg[g], len = a.wv.grp_len[g];
     const int H = a.H, I = a.I;
     const int K = EPI == GEMM_GATEUP ? H : I;
@@ -129,24 +187,27 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm(ExpertArgs a, in
     const int m0 = mt * kBM;
     const int wave = __builtin_amdgcn_readfirstlane(t / kWave), lane = lane_id();
 
-    // ---- DMA sources: this lane's rows in each of its 1 KB DMA instructions
-    const uint8_t *asrc[kAInstr];
+    // ---- DMA sources: this lane's 16 bytes in each of its 1 KB DMA instructions.  Lane i of
+    // an instruction writes LDS bytes [16 i, 16 i + 16) of its 1 KB block, i.e. row i / CHUNKS of
+    // the block at chunk position i % CHUNKS, so it fetches the chunk that belongs there.
+    constexpr int A_ROWS = 1024 / ARB, B_ROWS = 1024 / BRB;   // rows per DMA instruction
+    constexpr int A_CHUNKS = ARB / 16, B_CHUNKS = BRB / 16;
+    const uint8_t *asrc[A_INSTR];
 #pragma unroll
-    for (int ii = 0; ii < kAInstr; ++ii) {
-        const int row = (wave * kAInstr + ii) * 8 + lane / 8;
+    for (int ii = 0; ii < A_INSTR; ++ii) {
+        const int row = (wave * A_INSTR + ii) * A_ROWS + lane / A_CHUNKS;
         const int r = min(len - 1, m0 + row);      // padding rows repeat the last row; never stored
         const uint8_t *rowp;
         if constexpr (EPI == GEMM_GATEUP)
             rowp = static_cast<const uint8_t *>(a.x) + static_cast<size_t>(a.wv.row_tok[beg + r]) * H * 2;
         else
             rowp = static_cast<const uint8_t *>(a.wv.h) + static_cast<size_t>(beg + r) * I * 2;
-        asrc[ii] = rowp + (swz128(row, lane & 7) << 4);
+        asrc[ii] = rowp + (swz<ARB>(row, lane % A_CHUNKS) << 4);
     }
-    constexpr int kBRowsPerInstr = 1024 / Tr::kRowBytes;
-    const uint8_t *bsrc[Tr::kBInstr];
+    const uint8_t *bsrc[B_INSTR];
 #pragma unroll
-    for (int ii = 0; ii < Tr::kBInstr; ++ii) {
-        const int row = (wave * Tr::kBInstr + ii) * kBRowsPerInstr + lane / Tr::kChunks;
+    for (int ii = 0; ii < B_INSTR; ++ii) {
+        const int row = (wave * B_INSTR + ii) * B_ROWS + lane / B_CHUNKS;
         int wrow;
         if constexpr (EPI == GEMM_GATEUP) {
             const int wn = row >> 6, q = row & 63, hc0 = nt * (kBN / 2) + wn * 32;
@@ -154,40 +215,25 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm(ExpertArgs a, in
         } else {
             wrow = nt * kBN + row;
         }
-        const size_t wb = WT == FT_DT_BF16 ? 2 : 1;
-        const int chunk = WT == FT_DT_BF16 ? swz128(row, lane & 7) : swz64(row, lane & 3);
         bsrc[ii] = static_cast<const uint8_t *>(EPI == GEMM_GATEUP ? a.w13 : a.w2) +
-                   (static_cast<size_t>(slot) * nrows + wrow) * K * wb + (chunk << 4);
+                   (static_cast<size_t>(slot) * nrows + wrow) * K * GTr<WT>::kWb +
+                   (swz<BRB>(row, lane % B_CHUNKS) << 4);
     }
     auto issue = [&](int kt, uint8_t *dA, uint8_t *dB) {
 #pragma unroll
-        for (int ii = 0; ii < kAInstr; ++ii)
-            dma16(asrc[ii] + static_cast<size_t>(kt) * kARowBytes, dA + (wave * kAInstr + ii) * 1024);
+        for (int ii = 0; ii < A_INSTR; ++ii)
+            dma16(asrc[ii] + static_cast<size_t>(kt) * ARB, dA + (wave * A_INSTR + ii) * 1024);
 #pragma unroll
-        for (int ii = 0; ii < Tr::kBInstr; ++ii)
-            dma16(bsrc[ii] + static_cast<size_t>(kt) * Tr::kRowBytes, dB + (wave * Tr::kBInstr + ii) * 1024);
+        for (int ii = 0; ii < B_INSTR; ++ii)
+            dma16(bsrc[ii] + static_cast<size_t>(kt) * BRB, dB + (wave * B_INSTR + ii) * 1024);
     };
-    constexpr int kPerStage = kAInstr + Tr::kBInstr;
 
-    // ---- MFMA fragments
     const int wm = wave / kWavesN, wn = wave % kWavesN;
     const int fn = lane & 31, fq = lane >> 5;
+    const int nkb = K / 128;
     // fp8 block scales of each wave's columns (the gate and the up rows of a gate/up tile, or
     // the down tile's rows), one per 128-wide K block, staged in LDS before the pipeline starts:
-    // a vector load inside the loop would make the wait-count pass drain the DMA stages
-    constexpr int kMaxKb = 64;                      // K <= 8192
-    __shared__ float s_scale[kWavesN][2][kMaxKb];
-    // token and gate of each row of the tile (down projection epilogue), loaded with the prologue
-    __shared__ int32_t s_tok[kBM];
-    __shared__ float s_gate[kBM];
-    if constexpr (EPI == GEMM_DOWN) {
-        for (int i = t; i < kBM; i += kGemmThreads) {
-            const int r = min(len - 1, m0 + i);
-            s_tok[i] = a.wv.row_tok[beg + r];
-            s_gate[i] = a.wv.row_gate[beg + r];
-        }
-    }
-    const int nkb = K / 128;
+    // a vector load inside the loop would make the compiler drain the DMA stages
     if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
         const float *s = EPI == GEMM_GATEUP ? a.s13 : a.s2;
         for (int idx = t; idx < kWavesN * 2 * nkb; idx += kGemmThreads) {
@@ -201,8 +247,16 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm(ExpertArgs a, in
             }
             s_scale[w][which][kb] = s[(static_cast<size_t>(slot) * (nrows / 128) + r) * nkb + kb];
         }
-        __syncthreads();
     }
+    // token and gate of each row of the tile (down projection epilogue)
+    if constexpr (EPI == GEMM_DOWN) {
+        for (int i = t; i < kBM; i += kGemmThreads) {
+            const int r = min(len - 1, m0 + i);
+            s_tok[i] = a.wv.row_tok[beg + r];
+            s_gate[i] = a.wv.row_gate[beg + r];
+        }
+    }
+
     // 2 x 2 tiles of 32 x 32 per wave; for a gate/up tile, column tile 0 holds the wave's 32
     // gate columns and column tile 1 the matching up columns
     floatx16_t acc[2][2], part[2][2];
@@ -214,40 +268,41 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm(ExpertArgs a, in
             part[i][j] = floatx16_t{};
         }
 
-    const int nk = K / kBK;
-    // one stage: read slot (A, B) for K stage kt while the DMA for stage kt + 2 fills (dA, dB).
-    // Stage kt landed once this wave's DMA count allows only stage kt+1 to be outstanding and
-    // the barrier has passed (every wave's share of it landed, every wave finished reading
-    // stage kt-1); only then may stage kt+2 overwrite the slot stage kt-1 used.  Past the end
-    // the DMA re-reads the last stage into that free slot, keeping the counts constant.
-    auto step = [&](int kt, const uint8_t *A, const uint8_t *B, uint8_t *dA, uint8_t *dB) {
-        wait_vmcnt<(kStages - 2) * kPerStage>();
+    const int nk = K / BK;
+    // One pipeline step: multiply K stage kt from slot RS while the DMA of stage kt + NS - 1
+    // fills slot WS.  Stage kt has landed once this wave allows only stages kt+1 .. kt+NS-2 to be
+    // outstanding and the barrier has passed (every wave's share landed, and every wave is done
+    // reading stage kt-1, whose slot WS is); past the end the DMA re-reads the last stage into
+    // that free slot, which keeps the counts constant.
+    auto step = [&](int kt, auto rs, auto ws) {
+        wait_vmcnt<(NS - 2) * PER_STAGE>();
         wait_lgkmcnt0();
         stage_barrier();
-        issue(min(kt + kStages - 1, nk - 1), dA, dB);
+        issue(min(kt + NS - 1, nk - 1), stA(ws), stB(ws));
         if (kt < nk) {
+            const uint8_t *A = stA(rs);
+            const uint8_t *B = stB(rs);
             // all operand fragments of the stage are read before the first MFMA (distinct
-            // registers, fenced by a scheduling barrier), so the MFMAs wait on them one by one
-            // instead of stalling at every K step
-            constexpr int KS = kBK / 16;
+            // registers, fenced by a scheduling barrier)
+            constexpr int KS = BK / 16;
             u32x4_t af[KS][2], bf[KS][2];
             uint2 b8[KS][2];
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                // 32x32x16 MFMA operands: lane (r = lane % 32, kg = lane / 32) holds 8 K values
-                // of row r, chunk 2 ks + kg of the stage
+                // 32x32x16 MFMA operands: lane (r = lane % 32, kg = lane / 32) holds the 8 K
+                // values [16 ks + 8 kg, +8) of row r, i.e. 16-byte chunk 2 ks + kg of a bf16 row
                 const int c = ks * 2 + fq;
 #pragma unroll
                 for (int i = 0; i < 2; ++i) {
                     const int ra = wm * 64 + i * 32 + fn;
-                    af[ks][i] = *reinterpret_cast<const u32x4_t *>(A + ra * kARowBytes + (swz128(ra, c) << 4));
+                    af[ks][i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, c) << 4));
                     const int rb = wn * 64 + i * 32 + fn;
                     if constexpr (WT == FT_DT_BF16) {
-                        bf[ks][i] = *reinterpret_cast<const u32x4_t *>(B + rb * Tr::kRowBytes + (swz128(rb, c) << 4));
+                        bf[ks][i] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, c) << 4));
                     } else {
-                        const int kq = c * 8;                          // first of 8 fp8 bytes
-                        const int ch = swz64(rb, kq >> 4);
-                        b8[ks][i] = *reinterpret_cast<const uint2 *>(B + rb * Tr::kRowBytes + (ch << 4) + (kq & 15));
+                        const int kq = c * 8;                  // first of the 8 fp8 bytes
+                        b8[ks][i] = *reinterpret_cast<const uint2 *>(
+                            B + rb * BRB + (swz<BRB>(rb, kq >> 4) << 4) + (kq & 15));
                     }
                 }
             }
@@ -263,16 +318,17 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm(ExpertArgs a, in
 #pragma unroll
                     for (int j = 0; j < 2; ++j) {
                         if constexpr (WT == FT_DT_BF16)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(af[ks][i]), as_bf16x8(bf[ks][j]),
-                                                                                acc[i][j], 0, 0, 0);
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                as_bf16x8(af[ks][i]), as_bf16x8(bf[ks][j]), acc[i][j], 0, 0, 0);
                         else
-                            part[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(af[ks][i]), as_bf16x8(bf[ks][j]),
-                                                                                 part[i][j], 0, 0, 0);
+                            part[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                                as_bf16x8(af[ks][i]), as_bf16x8(bf[ks][j]), part[i][j], 0, 0, 0);
                     }
             }
             if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
-                if ((kt & 1) == 1) {            // end of a 128-wide K block: scale and fold
-                    const int kb = kt >> 1;
+                static_assert(128 % BK == 0, "K stages tile a scale block");
+                if (((kt + 1) * BK) % 128 == 0) {   // end of a 128-wide K block: scale and fold
+                    const int kb = ((kt + 1) * BK) / 128 - 1;
                     const float slo = s_scale[wn][0][kb], shi = s_scale[wn][1][kb];
 #pragma unroll
                     for (int i = 0; i < 2; ++i)
@@ -288,16 +344,17 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm(ExpertArgs a, in
         }
     };
 
-    // outstanding stores of the zeroing loop must not be counted against the DMA waits below;
-    // the barrier publishes the staged token / gate / scale tables
+    // outstanding stores of the zeroing loop must not count against the DMA waits below; the
+    // barrier publishes the staged scale / token / gate tables
     wait_vmcnt<0>();
     __syncthreads();
-    issue(0, sA0, sB0);
-    issue(min(1, nk - 1), sA1, sB1);
-    for (int kt = 0; kt < nk; kt += 3) {
-        step(kt + 0, sA0, sB0, sA2, sB2);
-        step(kt + 1, sA1, sB1, sA0, sB0);
-        step(kt + 2, sA2, sB2, sA1, sB1);
+    static_for<0, NS - 1>([&](auto s) { issue(min(decltype(s)::value, nk - 1), stA(s), stB(s)); });
+    for (int kt = 0; kt < nk; kt += NS) {
+        // stage kt + S sits in slot S; its step refills slot (S + NS - 1) mod NS
+        static_for<0, NS>([&](auto s) {
+            constexpr int S = decltype(s)::value;
+            step(kt + S, s, ic<(S + NS - 1) % NS>{});
+        });
     }
     wait_vmcnt<0>();   // the redundant tail stages
 
@@ -321,11 +378,10 @@ __global__ __launch_bounds__(kGemmThreads, 1) void grouped_gemm(ExpertArgs a, in
         for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                const int row = m0 + wm * 64 + i * 32 + (e >> 2) * 8 + 4 * fq + (e & 3);
-                if (row < len) {
-                    const int tok = s_tok[row - m0];
-                    const float gw = s_gate[row - m0];
-                    float *orow = a.out + static_cast<size_t>(tok) * H + nt * kBN + wn * 64 + fn;
+                const int rl = wm * 64 + i * 32 + (e >> 2) * 8 + 4 * fq + (e & 3);
+                if (m0 + rl < len) {
+                    float *orow = a.out + static_cast<size_t>(s_tok[rl]) * H + nt * kBN + wn * 64 + fn;
+                    const float gw = s_gate[rl];
 #pragma unroll
                     for (int j = 0; j < 2; ++j) unsafeAtomicAdd(orow + j * 32, gw * acc[i][j][e]);
                 }
