@@ -42,6 +42,19 @@ __device__ __forceinline__ u32x4_t fp8x8_to_bf16x8(uint32_t w0, uint32_t w1) {
                    pack_bf16_trunc(c[0], c[1]), pack_bf16_trunc(d[0], d[1])};
 }
 
+// 8 fp8 e4m3fn codes times one float32 block scale -> 8 bf16, each product (exact in float32)
+// rounded to nearest-even once
+typedef __bf16 bf16x2_vec_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32x4_t fp8x8_scaled_to_bf16x8(uint32_t w0, uint32_t w1, float s) {
+    auto pk = [s](floatx2_t f) {
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(f * s, bf16x2_vec_t));
+    };
+    return u32x4_t{pk(__builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w0), false)),
+                   pk(__builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w0), true)),
+                   pk(__builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w1), false)),
+                   pk(__builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w1), true))};
+}
+
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
     return __builtin_bit_cast(bf16x8_t, v);
 }

@@ -18,7 +18,7 @@ constexpr int kFusedMaxLds = 64 * 1024;
 #define FT_GEMM_BM 128
 #endif
 #ifndef FT_GEMM_BN
-#define FT_GEMM_BN 128
+#define FT_GEMM_BN 256
 #endif
 constexpr int kGemmBM = FT_GEMM_BM;     // token rows per MFMA GEMM tile (prefill path)
 constexpr int kGemmBN = FT_GEMM_BN;     // weight rows per MFMA GEMM tile

@@ -6,28 +6,35 @@
 //   gate/up: h[rows of g] = silu(X_g W1^T) * (X_g W3^T)       tile = BM rows x BN/2 h columns
 //   down   : out[tok] += gate * (h_g W2^T)                    tile = BM rows x BN out columns
 //
-// Work decomposition.  One workgroup of 4 waves (BM/64 x BN/64 over the tile, 64 x 64 each as
-// 2 x 2 MFMA 32x32x16 tiles, the bf16 MFMA shape with the highest measured throughput on
-// gfx950) per (group, BM-row M tile, N tile).  Two workgroups share a CU, so one multiplies
-// while the other waits at a stage barrier or runs its prologue or epilogue.  Tiles are
-// enumerated M-tile-major with the N tile fastest, through the per-M-tile group map the router
-// writes, so the N tiles of one M tile (sharing activation rows) and the M tiles of one group
-// (sharing weight tiles) run close together; the block -> tile map keeps consecutive tiles on
-// one XCD (workgroups are dealt to the 8 XCDs round-robin) to share its L2.
+// Work decomposition.  One workgroup of 4 waves per (group, BM-row M tile, BN-row N tile); each
+// wave computes all 128 rows of the tile for its own 64 columns, as 4 x 2 MFMA 32x32x16 tiles
+// (the bf16 MFMA shape with the highest measured throughput on gfx950), so every weight element
+// is read from LDS (and, for fp8, widened) by exactly one wave.  Two workgroups share a CU, so one
+// multiplies while the other waits at a stage barrier or runs its prologue or epilogue.  The tile
+// is as wide as two workgroups per CU allow because the kernel is bound by how fast L2 feeds the
+// CUs (global -> LDS traffic tops out near 25 bytes per clock per CU): a 128 x 256 tile moves 768
+// bytes per K step for 65536 flops, a third less per flop than 128 x 128, while the 128-row M
+// tile keeps the padding of the small expert groups in check.
+// Tiles are enumerated per group, in bands of up to kBandM M tiles, each band N-tile-major with
+// the M tile fastest, through the per-M-tile group map the router writes, so the tiles that
+// share a weight tile and those that share activation rows run at the same time; the block ->
+// tile map keeps consecutive tiles on one XCD (workgroups are dealt to the 8 XCDs round-robin)
+// to share its L2.
 //
 // Data movement.  A (activation rows, gathered through row_tok for gate/up) and B (weight rows,
-// kept in their storage format: bf16, or fp8 widened to bf16 only when read for the MFMA) go
-// straight from global memory into LDS with global_load_lds (16 bytes per lane), through a ring
-// of NS stages of BK K-values, NS - 1 stages in flight while one is multiplied.  Every LDS row
-// keeps its 16-byte chunks XOR-swizzled by the row index, so MFMA operand reads of consecutive
-// rows hit distinct banks.  The stage hand-off is an explicit vmcnt wait plus s_barrier (a
-// __syncthreads would drain every stage in flight).  The ring is unrolled and every stage buffer
-// is an array of its own, so the compiler can tell the stage being read from the stages still
-// being written and adds no wait of its own.
+// kept in their storage format, bf16 or fp8) go straight from global memory into LDS with
+// global_load_lds (16 bytes per lane), through a ring of NS stages of BK K-values, NS - 1 stages
+// in flight while one is multiplied.  Every LDS row keeps its 16-byte chunks XOR-swizzled by the
+// row index, so MFMA operand reads of consecutive rows hit distinct banks.  The stage hand-off is
+// an explicit vmcnt wait plus s_barrier (a __syncthreads would drain every stage in flight).  The
+// ring is unrolled and every stage buffer is an array of its own, so the compiler can tell the
+// stage being read from the stages still being written and adds no wait of its own.
 //
-// fp8 weights carry one float32 scale per 128 x 128 block: partial sums of each 128-wide K
-// block are scaled once and added to the accumulators.  The gate/up B tile puts each wave's 32
-// gate rows next to the 32 matching up rows, so SiLU(gate) * up is formed in registers.
+// fp8 weights carry one float32 scale per 128 x 128 block.  A wave's 64 columns lie in at most
+// two scale blocks (the gate and the up half of a gate/up tile, one block for down), so each fp8
+// weight is widened, multiplied by its block scale and rounded to bf16 as it is read for the
+// MFMA.  The gate/up B tile puts each wave's 32 gate rows next to the 32 matching up rows, so
+// SiLU(gate) * up is formed in registers.
 #include <type_traits>
 
 #include "ftmoe_device.h"
@@ -35,13 +42,15 @@
 
 namespace ftmoe {
 
-constexpr int kBM = kGemmBM;          // token rows per tile
-constexpr int kBN = kGemmBN;          // weight rows per tile
 constexpr int kGemmThreads = 256;
 constexpr int kGemmWaves = kGemmThreads / kWave;
-constexpr int kWavesN = kBN / 64;     // waves across N, 64 columns each
-constexpr int kWavesM = kBM / 64;     // waves across M, 64 rows each
-static_assert(kWavesN * kWavesM == kGemmWaves, "4 waves of 64 x 64");
+constexpr int kWavesM = 1, kWavesN = 4;
+constexpr int kWaveRows = 128, kWaveCols = 64;          // per-wave output tile
+constexpr int kMI = kWaveRows / 32, kNJ = kWaveCols / 32; // 32 x 32 MFMA tiles per wave
+constexpr int kBM = kGemmBM;                            // token rows per tile
+constexpr int kBN = kGemmBN;                            // weight rows per tile
+static_assert(kWavesM * kWavesN == kGemmWaves, "4 waves");
+static_assert(kBM == kWavesM * kWaveRows && kBN == kWavesN * kWaveCols, "tile = waves x wave tile");
 #ifndef FT_GEMM_BAND
 #define FT_GEMM_BAND 8
 #endif
@@ -51,19 +60,19 @@ enum { GEMM_GATEUP = 0, GEMM_DOWN = 1 };
 
 // Per weight format: K values per stage and ring depth (two workgroups of either fit one CU's
 // LDS), bytes per weight element.
-template <int WT> struct GTr;
 #ifndef FT_GEMM_BF16_BK
 #define FT_GEMM_BF16_BK 32
 #endif
 #ifndef FT_GEMM_BF16_NS
-#define FT_GEMM_BF16_NS 4
+#define FT_GEMM_BF16_NS 3
 #endif
 #ifndef FT_GEMM_FP8_BK
 #define FT_GEMM_FP8_BK 64
 #endif
 #ifndef FT_GEMM_FP8_NS
-#define FT_GEMM_FP8_NS 3
+#define FT_GEMM_FP8_NS 2
 #endif
+template <int WT> struct GTr;
 template <> struct GTr<FT_DT_BF16> {
     static constexpr int BK = FT_GEMM_BF16_BK, NS = FT_GEMM_BF16_NS, kWb = 2;
 };
@@ -109,14 +118,17 @@ __device__ __forceinline__ void stage_barrier() {
     asm volatile("" ::: "memory");
 }
 
-// Position of 16-byte chunk c in LDS row r.  A 128-byte row covers half of the 64 x 4-byte banks
-// and a 64-byte row a quarter, so XOR with (r / 2) mod 8, resp. (r / 4) mod 4, puts the same
-// chunk of 16 consecutive rows into distinct bank groups.
+// Position of 16-byte chunk c in LDS row r.  A 16-byte-per-lane LDS read serves 16 lanes (256
+// bytes, all 64 banks) per pass; the operand reads give those lanes 16 consecutive rows and one
+// chunk index, so the XOR spreads the same chunk of 16 consecutive rows over all 16 chunk
+// positions of a 256-byte window: a 128-byte row holds 8 chunks (XOR (r / 2) mod 8), a 64-byte
+// row 4 (XOR (r / 4) mod 4), a 32-byte row 2 (XOR (r / 8) mod 2).
 template <int ROW_BYTES>
 __device__ __forceinline__ int swz(int r, int c) {
-    static_assert(ROW_BYTES == 64 || ROW_BYTES == 128, "row size");
+    static_assert(ROW_BYTES == 32 || ROW_BYTES == 64 || ROW_BYTES == 128, "row size");
     if constexpr (ROW_BYTES == 128) return c ^ ((r >> 1) & 7);
-    else return c ^ ((r >> 2) & 3);
+    else if constexpr (ROW_BYTES == 64) return c ^ ((r >> 2) & 3);
+    else return c ^ ((r >> 3) & 1);
 }
 
 __device__ __forceinline__ void dma16(const void *g, uint8_t *lds_block) {
@@ -125,6 +137,7 @@ __device__ __forceinline__ void dma16(const void *g, uint8_t *lds_block) {
 
 template <int WT, int EPI>
 __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, int ntn) {
+    constexpr bool kFp8 = WT == FT_DT_FP8E4M3FN_B128;
     constexpr int BK = GTr<WT>::BK, NS = GTr<WT>::NS;
     constexpr int ARB = BK * 2;                      // A row bytes per stage (bf16)
     constexpr int BRB = BK * GTr<WT>::kWb;           // B row bytes per stage
@@ -135,10 +148,13 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
     static_assert(A_INSTR >= 1 && B_INSTR >= 1, "stage too small");
     static_assert(NS >= 2 && NS <= 4, "ring depth");
     static_assert((NS - 1) * PER_STAGE < 64, "vmcnt range");
-    // one array per stage (see the header comment); the fourth is unused with a 3-deep ring
-    __shared__ __attribute__((aligned(1024))) uint8_t sA0[ASTAGE], sA1[ASTAGE], sA2[ASTAGE];
+    static_assert(!kFp8 || 128 % BK == 0, "an fp8 K stage lies in one scale block");
+    // one array per stage (see the header comment); unused ones shrink to 16 bytes
+    __shared__ __attribute__((aligned(1024))) uint8_t sA0[ASTAGE], sA1[ASTAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t sA2[NS > 2 ? ASTAGE : 16];
     __shared__ __attribute__((aligned(1024))) uint8_t sA3[NS > 3 ? ASTAGE : 16];
-    __shared__ __attribute__((aligned(1024))) uint8_t sB0[BSTAGE], sB1[BSTAGE], sB2[BSTAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t sB0[BSTAGE], sB1[BSTAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t sB2[NS > 2 ? BSTAGE : 16];
     __shared__ __attribute__((aligned(1024))) uint8_t sB3[NS > 3 ? BSTAGE : 16];
     constexpr int kMaxKb = 64;                       // K <= 8192
     __shared__ float s_scale[kWavesN][2][kMaxKb];
@@ -204,14 +220,17 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
             rowp = static_cast<const uint8_t *>(a.wv.h) + static_cast<size_t>(beg + r) * I * 2;
         asrc[ii] = rowp + (swz<ARB>(row, lane % A_CHUNKS) << 4);
     }
+    // B tile row -> weight row.  gate/up: wave n's 64 rows are the 32 gate rows of h columns
+    // [hc0, hc0 + 32), hc0 = nt * BN/2 + 32 n, followed by the 32 matching up rows (I + hc0 ...).
     const uint8_t *bsrc[B_INSTR];
 #pragma unroll
     for (int ii = 0; ii < B_INSTR; ++ii) {
         const int row = (wave * B_INSTR + ii) * B_ROWS + lane / B_CHUNKS;
         int wrow;
         if constexpr (EPI == GEMM_GATEUP) {
-            const int wn = row >> 6, q = row & 63, hc0 = nt * (kBN / 2) + wn * 32;
-            wrow = q < 32 ? hc0 + q : I + hc0 + q - 32;
+            const int wn = row / kWaveCols, q = row % kWaveCols;
+            const int hc0 = nt * (kBN / 2) + wn * (kWaveCols / 2);
+            wrow = q < kWaveCols / 2 ? hc0 + q : I + hc0 + q - kWaveCols / 2;
         } else {
             wrow = nt * kBN + row;
         }
@@ -231,19 +250,19 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
     const int wm = wave / kWavesN, wn = wave % kWavesN;
     const int fn = lane & 31, fq = lane >> 5;
     const int nkb = K / 128;
-    // fp8 block scales of each wave's columns (the gate and the up rows of a gate/up tile, or
-    // the down tile's rows), one per 128-wide K block, staged in LDS before the pipeline starts:
-    // a vector load inside the loop would make the compiler drain the DMA stages
-    if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
+    // fp8 block scales of each wave's columns (gate half and up half of a gate/up tile; one
+    // block for down), one per 128-wide K block, staged in LDS before the pipeline starts: a
+    // vector load inside the loop would make the compiler drain the DMA stages
+    if constexpr (kFp8) {
         const float *s = EPI == GEMM_GATEUP ? a.s13 : a.s2;
         for (int idx = t; idx < kWavesN * 2 * nkb; idx += kGemmThreads) {
             const int w = idx / (2 * nkb), which = (idx / nkb) & 1, kb = idx % nkb;
             int r;
             if constexpr (EPI == GEMM_GATEUP) {
-                const int hc0 = nt * (kBN / 2) + w * 32;
+                const int hc0 = nt * (kBN / 2) + w * (kWaveCols / 2);
                 r = which == 0 ? hc0 / 128 : (I + hc0) / 128;
             } else {
-                r = (nt * kBN + w * 64) / 128;
+                r = (nt * kBN + w * kWaveCols) / 128;
             }
             s_scale[w][which][kb] = s[(static_cast<size_t>(slot) * (nrows / 128) + r) * nkb + kb];
         }
@@ -257,16 +276,13 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
         }
     }
 
-    // 2 x 2 tiles of 32 x 32 per wave; for a gate/up tile, column tile 0 holds the wave's 32
-    // gate columns and column tile 1 the matching up columns
-    floatx16_t acc[2][2], part[2][2];
+    // kMI x kNJ tiles of 32 x 32 per wave; for a gate/up tile, column tiles [0, kNJ/2) are the
+    // wave's gate columns and [kNJ/2, kNJ) the matching up columns
+    floatx16_t acc[kMI][kNJ];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < kMI; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            acc[i][j] = floatx16_t{};
-            part[i][j] = floatx16_t{};
-        }
+        for (int j = 0; j < kNJ; ++j) acc[i][j] = floatx16_t{};
 
     const int nk = K / BK;
     // One pipeline step: multiply K stage kt from slot RS while the DMA of stage kt + NS - 1
@@ -282,64 +298,49 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
         if (kt < nk) {
             const uint8_t *A = stA(rs);
             const uint8_t *B = stB(rs);
-            // all operand fragments of the stage are read before the first MFMA (distinct
-            // registers, fenced by a scheduling barrier)
             constexpr int KS = BK / 16;
-            u32x4_t af[KS][2], bf[KS][2];
-            uint2 b8[KS][2];
+            float sc[2] = {1.f, 1.f};
+            if constexpr (kFp8) {
+                const int kb = (kt * BK) / 128;
+                sc[0] = s_scale[wn][0][kb];
+                sc[1] = s_scale[wn][1][kb];
+            }
+            // 32x32x16 MFMA operands: lane (r = lane % 32, kg = lane / 32) holds 8 K values of
+            // row r for each operand; which 8 is free as long as A and B agree.  bf16 weights:
+            // sub-step ks takes K [16 ks + 8 kg, +8), i.e. 16-byte chunk 2 ks + kg of both rows.
+            // fp8 weights: a lane reads one 16-byte chunk of its weight row, 16 K values, for
+            // two sub-steps, so sub-step ks = 2 p + s takes K [32 p + 16 kg + 8 s, +8): weight
+            // chunk 2 p + kg (bytes 8 s ..), activation chunk 4 p + 2 kg + s.
+            u32x4_t b16[kNJ];
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                // 32x32x16 MFMA operands: lane (r = lane % 32, kg = lane / 32) holds the 8 K
-                // values [16 ks + 8 kg, +8) of row r, i.e. 16-byte chunk 2 ks + kg of a bf16 row
-                const int c = ks * 2 + fq;
+                const int ca = kFp8 ? 4 * (ks / 2) + 2 * fq + (ks % 2) : 2 * ks + fq;
+                u32x4_t af[kMI], bf[kNJ];
 #pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const int ra = wm * 64 + i * 32 + fn;
-                    af[ks][i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, c) << 4));
-                    const int rb = wn * 64 + i * 32 + fn;
-                    if constexpr (WT == FT_DT_BF16) {
-                        bf[ks][i] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, c) << 4));
+                for (int i = 0; i < kMI; ++i) {
+                    const int ra = wm * kWaveRows + i * 32 + fn;
+                    af[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, ca) << 4));
+                }
+#pragma unroll
+                for (int j = 0; j < kNJ; ++j) {
+                    const int rb = wn * kWaveCols + j * 32 + fn;
+                    if constexpr (!kFp8) {
+                        bf[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, ca) << 4));
                     } else {
-                        const int kq = c * 8;                  // first of the 8 fp8 bytes
-                        b8[ks][i] = *reinterpret_cast<const uint2 *>(
-                            B + rb * BRB + (swz<BRB>(rb, kq >> 4) << 4) + (kq & 15));
+                        if (ks % 2 == 0)
+                            b16[j] = *reinterpret_cast<const u32x4_t *>(
+                                B + rb * BRB + (swz<BRB>(rb, 2 * (ks / 2) + fq) << 4));
+                        const float s = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? sc[1] : sc[0];
+                        bf[j] = ks % 2 == 0 ? fp8x8_scaled_to_bf16x8(b16[j][0], b16[j][1], s)
+                                            : fp8x8_scaled_to_bf16x8(b16[j][2], b16[j][3], s);
                     }
                 }
-            }
-            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
+                for (int i = 0; i < kMI; ++i)
 #pragma unroll
-                    for (int i = 0; i < 2; ++i) bf[ks][i] = fp8x8_to_bf16x8(b8[ks][i].x, b8[ks][i].y);
-                }
-#pragma unroll
-                for (int i = 0; i < 2; ++i)
-#pragma unroll
-                    for (int j = 0; j < 2; ++j) {
-                        if constexpr (WT == FT_DT_BF16)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                as_bf16x8(af[ks][i]), as_bf16x8(bf[ks][j]), acc[i][j], 0, 0, 0);
-                        else
-                            part[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                                as_bf16x8(af[ks][i]), as_bf16x8(bf[ks][j]), part[i][j], 0, 0, 0);
-                    }
-            }
-            if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
-                static_assert(128 % BK == 0, "K stages tile a scale block");
-                if (((kt + 1) * BK) % 128 == 0) {   // end of a 128-wide K block: scale and fold
-                    const int kb = ((kt + 1) * BK) / 128 - 1;
-                    const float slo = s_scale[wn][0][kb], shi = s_scale[wn][1][kb];
-#pragma unroll
-                    for (int i = 0; i < 2; ++i)
-#pragma unroll
-                        for (int j = 0; j < 2; ++j) {
-                            const float sc = (EPI == GEMM_GATEUP && j == 1) ? shi : slo;
-#pragma unroll
-                            for (int e = 0; e < 16; ++e) acc[i][j][e] += sc * part[i][j][e];
-                            part[i][j] = floatx16_t{};
-                        }
-                }
+                    for (int j = 0; j < kNJ; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            as_bf16x8(af[i]), as_bf16x8(bf[j]), acc[i][j], 0, 0, 0);
             }
         }
     };
@@ -362,28 +363,30 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
     // column fn
     if constexpr (EPI == GEMM_GATEUP) {
         uint16_t *hout = static_cast<uint16_t *>(a.wv.h);
-        const int col = nt * (kBN / 2) + wn * 32 + fn;
+        const int col0 = nt * (kBN / 2) + wn * (kWaveCols / 2) + fn;
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < kMI; ++i)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                const int row = m0 + wm * 64 + i * 32 + (e >> 2) * 8 + 4 * fq + (e & 3);
+                const int row = m0 + wm * kWaveRows + i * 32 + (e >> 2) * 8 + 4 * fq + (e & 3);
                 if (row < len) {
-                    const float hv = silu_f32(acc[i][0][e]) * acc[i][1][e];
-                    hout[static_cast<size_t>(beg + row) * I + col] = f32_to_bf16(hv);
+                    uint16_t *hrow = hout + static_cast<size_t>(beg + row) * I + col0;
+#pragma unroll
+                    for (int j = 0; j < kNJ / 2; ++j)
+                        hrow[j * 32] = f32_to_bf16(silu_f32(acc[i][j][e]) * acc[i][j + kNJ / 2][e]);
                 }
             }
     } else {
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < kMI; ++i)
 #pragma unroll
             for (int e = 0; e < 16; ++e) {
-                const int rl = wm * 64 + i * 32 + (e >> 2) * 8 + 4 * fq + (e & 3);
+                const int rl = wm * kWaveRows + i * 32 + (e >> 2) * 8 + 4 * fq + (e & 3);
                 if (m0 + rl < len) {
-                    float *orow = a.out + static_cast<size_t>(s_tok[rl]) * H + nt * kBN + wn * 64 + fn;
+                    float *orow = a.out + static_cast<size_t>(s_tok[rl]) * H + nt * kBN + wn * kWaveCols + fn;
                     const float gw = s_gate[rl];
 #pragma unroll
-                    for (int j = 0; j < 2; ++j) unsafeAtomicAdd(orow + j * 32, gw * acc[i][j][e]);
+                    for (int j = 0; j < kNJ; ++j) unsafeAtomicAdd(orow + j * 32, gw * acc[i][j][e]);
                 }
             }
     }

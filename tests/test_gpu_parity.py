@@ -172,6 +172,9 @@ RANDOM_FWD = [
     (10, workloads.DT_BF16, 0, 32, 8, 1000, 20, False, 384, 128, 0.8),
     (11, workloads.DT_BF16, 0, 8, 1, 256, 8, False, 128, 128, 3.0),
     (12, workloads.DT_FP8, 1, 24, 6, 400, 10, True, 256, 256, 1.0),
+    (13, workloads.DT_BF16, 0, 16, 4, 700, 11, False, 512, 256, 1.0),
+    (14, workloads.DT_FP8, 1, 32, 8, 520, 13, True, 512, 384, 2.0),
+    (15, workloads.DT_BF16, 1, 8, 8, 260, 8, True, 768, 128, 0.0),
 ]
 
 
