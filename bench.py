@@ -79,8 +79,85 @@ def algorithmic_work(lay, route):
     hb = 4 if lay.w_dtype == 0 else 2
     gateup_bytes = (u_hit + shared) * S13 + T * H * xb + rows * I * hb
     flops = rows * 6 * H * I
-    return dict(layer_bytes=layer_bytes, gateup_bytes=gateup_bytes, flops=flops, u_hit=u_hit,
-                n_hit=n_hit, rows=rows)
+    return dict(layer_bytes=layer_bytes, gateup_bytes=gateup_bytes, flops=flops,
+                gateup_flops=rows * 4 * H * I, u_hit=u_hit, n_hit=n_hit, rows=rows)
+
+
+def kernel_source_sha() -> str:
+    """Hash of the HIP sources the library is built from (traffic figures are tied to it)."""
+    import glob
+    import hashlib
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2608_16157_amd", "csrc", "*"))):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def measured_traffic(key: str):
+    """HBM bytes per launch of the dominant kernel from the committed counter runs, or None when
+    they were taken on other kernel sources (or never)."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            rec = json.load(fh).get(key)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_sha") != kernel_source_sha():
+        return None
+    return rec.get("traffic_bytes")
+
+
+def calibrate_copy(mib: int, reps: int = 5):
+    """A plain elementwise copy kernel (y = 1 * x, fp32) of known size, for scaling the
+    FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    import torch
+    n = mib * (1 << 20) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(reps):
+        torch.mul(x, 1.0, out=y)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "copy", "bytes_read": 4 * n, "bytes_written": 4 * n,
+                      "launches": reps}), flush=True)
+
+
+def ingest_traffic(key, kernel_match, fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, cal_bytes):
+    """Per-launch HBM traffic of the kernel whose name contains kernel_match, from rocprofv3
+    --pmc FETCH_SIZE and WRITE_SIZE counter CSVs, each scaled by the same counter's reading for
+    the copy calibration kernel of cal_bytes read and cal_bytes written; merged into
+    profiles/traffic.json under key."""
+    import csv
+
+    def per_dispatch(path, match):
+        vals = []
+        for r in csv.DictReader(open(path)):
+            if match in r["Kernel_Name"]:
+                vals.append(float(r["Counter_Value"]))
+        if not vals:
+            raise SystemExit(f"no dispatch of {match!r} in {path}")
+        return sum(vals) / len(vals)
+
+    cal = "AUnaryFunctor<float, float, float"     # the y = 1 * x copy kernel
+    f_scale = cal_bytes / per_dispatch(cal_fetch_csv, cal)
+    w_scale = cal_bytes / per_dispatch(cal_write_csv, cal)
+    fetch = per_dispatch(fetch_csv, kernel_match) * f_scale
+    write = per_dispatch(write_csv, kernel_match) * w_scale
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            data = json.load(fh)
+    except (OSError, ValueError):
+        data = {}
+    data[key] = {"kernel": kernel_match, "source_sha": kernel_source_sha(),
+                 "fetch_bytes": round(fetch), "write_bytes": round(write),
+                 "traffic_bytes": round(fetch + write),
+                 "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)}
+    with open(TRAFFIC_FILE, "w") as fh:
+        json.dump(data, fh, indent=1, sort_keys=True)
+        fh.write("\n")
+    print(json.dumps({key: data[key]}), flush=True)
 
 
 def cpu_baseline(layers, budget_s):
@@ -93,19 +170,31 @@ def cpu_baseline(layers, budget_s):
         cores = max([i.get("num_threads", 1) for i in info] or [1])
     except Exception:
         cores = 1
-    done_tokens, elapsed, used = 0, 0.0, 0
-    for lay in layers:
-        inp = oracle_inputs(lay)          # host copy, outside the timed part
-        t0 = time.perf_counter()
-        oracle.moe_partial(*inp)
-        elapsed += time.perf_counter() - t0
-        done_tokens += lay.tokens
-        used += 1
+    # many-token chunks are sampled 64 tokens at a time (the oracle's per-token work does not
+    # depend on the chunk it sits in, apart from decoding each expert's weights once per call)
+    done_tokens, elapsed, calls = 0, 0.0, 0
+    for rnd in range(8):                  # cycle over the instances until the budget is spent
+        for lay in layers:
+            inp = oracle_inputs(lay)      # host copy, outside the timed part
+            chunk = lay.tokens if lay.tokens <= 64 else 64
+            for c0 in range(0, lay.tokens, chunk):
+                toks = None if chunk == lay.tokens else list(range(c0, min(lay.tokens, c0 + chunk)))
+                t0 = time.perf_counter()
+                oracle.moe_partial(*inp, tokens=toks)
+                elapsed += time.perf_counter() - t0
+                done_tokens += chunk if toks is None else len(toks)
+                calls += 1
+                if elapsed >= budget_s:
+                    break
+            if elapsed >= budget_s:
+                break
         if elapsed >= budget_s:
             break
-    return {"value": done_tokens / elapsed, "unit": "tokens/s", "cores": cores, "kind": "oracle",
-            "sample": f"{used} of the {len(layers)} layer instances ({done_tokens} tokens), "
-                      f"{elapsed:.1f} s of float64 oracle time"}
+    return {"value": round(done_tokens / elapsed, 2), "unit": "tokens/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{calls} oracle calls of <= {min(64, layers[0].tokens)} tokens cycling over the "
+                      f"{len(layers)} layer instances ({done_tokens} tokens), {elapsed:.1f} s of "
+                      f"float64 oracle time"}
 
 
 def main():
@@ -118,7 +207,17 @@ def main():
     ap.add_argument("--layers", type=int, default=16)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", type=int, metavar="MIB",
+                    help="run only a plain copy kernel of MIB MiB (counter calibration)")
+    ap.add_argument("--ingest-traffic", nargs=7,
+                    metavar=("KEY", "KERNEL", "FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV",
+                             "CAL_WRITE_CSV", "CAL_BYTES"),
+                    help="record per-launch HBM traffic from rocprofv3 counter CSVs and exit")
     args = ap.parse_args()
+    if args.ingest_traffic:
+        a = args.ingest_traffic
+        ingest_traffic(a[0], a[1], a[2], a[3], a[4], a[5], int(a[6]))
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -131,6 +230,9 @@ def main():
     import workloads
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
     ftm.load()
     cfg = workloads.CONFIGS[args.config]
     T = args.tokens
@@ -194,7 +296,24 @@ def main():
     gu_bytes = sum(w["gateup_bytes"] for w in step_work) / K
     stage_avg = [sum(s[j] for s in stage_ms) / K for j in range(ftm.FT_PROF_STAGES)]
 
-    achieved = gu_bytes / (gu_ms / 1e3) / 1e9
+    gu_flops = sum(w["gateup_flops"] for w in step_work) / K
+    mfma_path = T >= 256      # the library's many-token (MFMA GEMM) path
+    key = f"{args.config}:T{T}"
+    traffic = measured_traffic(key)
+    if mfma_path:
+        # fp8 weights are widened to bf16 in registers, so every contraction runs on bf16 MFMA
+        achieved = gu_flops / (gu_ms / 1e3) / 1e12
+        roof = {"kernel": "grouped gate/up GEMM + SiLU-mul (grouped_gemm<gate/up>)", "bound": "mfma",
+                "achieved": round(achieved, 1), "peak": MFMA_PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
+                "frac": round(achieved / MFMA_PEAK_TFLOPS["bf16"], 4),
+                "traffic": traffic, "flops_per_launch": round(gu_flops),
+                "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
+    else:
+        achieved = gu_bytes / (gu_ms / 1e3) / 1e9
+        roof = {"kernel": "grouped gate/up GEMV + SiLU-mul (grouped_gemv<gate/up>)", "bound": "hbm",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
     dtype = {0: "f32", 1: "bf16", 2: "fp8e4m3->bf16"}[cfg.w_dtype]
     res = {
         "metric": METRIC,
@@ -221,17 +340,7 @@ def main():
         "layer_tflops": round(layer_flops / (ms_step / 1e3) / 1e12, 2),
         "stage_ms": {"route": round(stage_avg[0], 5), "gate_up": round(stage_avg[1], 5),
                      "down": round(stage_avg[2], 5), "combine": round(stage_avg[3], 5)},
-        "roofline": {
-            "kernel": "grouped gate/up projection + SiLU-mul",
-            "bound": "hbm",
-            "achieved": round(achieved, 1),
-            "peak": HBM_PEAK_GBS,
-            "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
-            "bytes_per_launch": round(gu_bytes),
-            "ms_per_launch": round(gu_ms, 5),
-        },
+        "roofline": roof,
     }
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle", file=sys.stderr, flush=True)
