@@ -67,7 +67,12 @@ enum {
  *   n_experts (E): 1..1024 routed experts.   top_k (k): 1..min(E, 64).
  *   gating: FT_GATE_*.
  *   w_dtype: FT_DT_F32 with x_dtype FT_DT_F32, or FT_DT_BF16 / FT_DT_FP8E4M3FN_B128 with
- *            x_dtype FT_DT_BF16 (fp8 weights are dequantised exactly; activations stay bf16).
+ *            x_dtype FT_DT_BF16.  Activations stay bf16 and products accumulate in float32.
+ *            fp8 weights: with T < 256 tokens each code is widened exactly and the block scale
+ *            multiplies the float32 partial sum of its 128-wide K block; with T >= 256 (matrix
+ *            core path) each code times its block scale is rounded to bf16 once (relative
+ *            error at most 2^-9 per weight) before the bf16 matrix multiply.  The SwiGLU
+ *            activation between the two projections is rounded to bf16 (float32 for f32).
  *   n_slots: number of bank rows (cache slots) in the banks, >= 0.
  *   shared_slot: bank row of an always-resident shared expert with gate 1 for every token,
  *                or -1 for none.
