@@ -115,10 +115,6 @@ inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int T) {
     return L;
 }
 
-inline int fused_route_lds_bytes(int E, int P) {
-    return 4 * (6 * E + 2 + 2 * P + 16 * E + 1);
-}
-inline int scan_route_lds_bytes(int E, int parts) { return 4 * (6 * E + 3 + parts * E); }
 
 // Optional stage events of ft_moe_forward_profiled (recorded only when given).
 struct Prof {

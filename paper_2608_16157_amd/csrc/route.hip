@@ -15,18 +15,27 @@ namespace ftmoe {
 // ---------------------------------------------------------------------------------------
 // Top-k of one token's logits by one wave.  Lane l holds experts [l*NPL, l*NPL + NPL), so among
 // equal logits the lowest lane, and within a lane the lowest index, is the lowest expert id.
-// Each round takes the wave maximum of the lanes' best keys (DPP) and the lowest lane holding
-// it (ballot).  On return lane j < k holds (expert id, gate) of the j-th selected expert.
+// topk_load fetches a token's keys (callers load several tokens before selecting, so the memory
+// latency is paid once per batch); topk_select runs the k rounds: the wave maximum of the lanes'
+// best keys (DPP) and the lowest lane holding it (ballot).  On return lane j < k holds
+// (expert id, gate) of the j-th selected expert.
 template <int NPL>
-__device__ __forceinline__ void wave_topk(const float *__restrict__ row, int E, int k, int gating,
-                                          int &my_id, float &my_w) {
+__device__ __forceinline__ void topk_load(const float *__restrict__ row, int E, uint32_t (&key)[NPL]) {
     const int lane = lane_id();
-    uint32_t key[NPL];
+    float v[NPL];
 #pragma unroll
     for (int i = 0; i < NPL; ++i) {
         const int e = lane * NPL + i;
-        key[i] = e < E ? order_key(row[e]) : 0u;
+        v[i] = e < E ? row[e] : 0.f;
     }
+#pragma unroll
+    for (int i = 0; i < NPL; ++i) key[i] = lane * NPL + i < E ? order_key(v[i]) : 0u;
+}
+
+template <int NPL>
+__device__ __forceinline__ void topk_select(uint32_t (&key)[NPL], int k, int gating, int &my_id,
+                                            float &my_w) {
+    const int lane = lane_id();
     uint32_t mine = 0u;
     int mine_e = -1;
     for (int j = 0; j < k; ++j) {
@@ -64,28 +73,65 @@ __device__ __forceinline__ void wave_topk(const float *__restrict__ row, int E, 
     my_w = lane < k ? z / sum : 0.f;
 }
 
-// Validated slot of each expert (-1 if unusable) and the device status bits.  `raw` is this
-// thread's slot_table entry (thread e of the block holds expert e; blockDim >= E).
+template <int NPL>
+__device__ __forceinline__ void wave_topk(const float *__restrict__ row, int E, int k, int gating,
+                                          int &my_id, float &my_w) {
+    uint32_t key[NPL];
+    topk_load<NPL>(row, E, key);
+    topk_select<NPL>(key, k, gating, my_id, my_w);
+}
+
+// Slot-table validation helpers.  An expert's slot is usable iff it lies in [0, n_slots), is not
+// the shared expert's slot, and no other expert maps to it; unusable entries are treated as
+// misses and reported in the device status bits.  Duplicates are found by counting experts per
+// slot in LDS (slot_count, when n_slots <= kSlotCountCap), else by comparing against every
+// other expert.
+constexpr int kSlotCountCap = 4096;
+
+__device__ __forceinline__ void slot_count(int raw, int E, int n_slots, int32_t *s_cnt) {
+    if (threadIdx.x < E && n_slots <= kSlotCountCap && raw >= 0 && raw < n_slots)
+        atomicAdd(&s_cnt[raw], 1);
+}
+
+__device__ __forceinline__ int slot_check(int raw, int e, int E, int n_slots, int shared_slot,
+                                          const int32_t *s_cnt, const int32_t *s_raw, int &status) {
+    const int s = raw;
+    if (s == -1) return -1;
+    if (s < -1 || s >= n_slots) {
+        status |= FT_DEV_SLOT_RANGE;
+        return -1;
+    }
+    if (shared_slot >= 0 && s == shared_slot) {
+        status |= FT_DEV_SLOT_SHARED;
+        return -1;
+    }
+    bool dup;
+    if (n_slots <= kSlotCountCap) {
+        dup = s_cnt[s] > 1;
+    } else {
+        dup = false;
+        for (int o = 0; o < E; ++o) dup |= (o != e) & (s_raw[o] == s);
+    }
+    if (dup) {
+        status |= FT_DEV_SLOT_DUP;
+        return -1;
+    }
+    return s;
+}
+
+// Validated slot of each expert (-1 if unusable) and the device status bits, by the whole
+// block.  `raw` is this thread's slot_table entry (thread e of the block holds expert e;
+// blockDim >= E); s_cnt holds min(n_slots, kSlotCountCap) counters.
 __device__ void validate_slots(int raw, int E, int n_slots, int shared_slot, int32_t *s_raw,
-                               int32_t *s_eff, int *s_status) {
+                               int32_t *s_cnt, int32_t *s_eff, int *s_status) {
     if (threadIdx.x < E) s_raw[threadIdx.x] = raw;
+    if (n_slots <= kSlotCountCap)
+        for (int i = threadIdx.x; i < n_slots; i += blockDim.x) s_cnt[i] = 0;
+    __syncthreads();
+    slot_count(raw, E, n_slots, s_cnt);
     __syncthreads();
     int st = 0;
-    if (threadIdx.x < E) {
-        const int e = threadIdx.x, s = raw;
-        int eff = -1;
-        if (s == -1) {
-        } else if (s < -1 || s >= n_slots) {
-            st |= FT_DEV_SLOT_RANGE;
-        } else if (shared_slot >= 0 && s == shared_slot) {
-            st |= FT_DEV_SLOT_SHARED;
-        } else {
-            bool dup = false;
-            for (int o = 0; o < E; ++o) dup |= (o != e) & (s_raw[o] == s);
-            if (dup) st |= FT_DEV_SLOT_DUP; else eff = s;
-        }
-        s_eff[e] = eff;
-    }
+    if (threadIdx.x < E) s_eff[threadIdx.x] = slot_check(raw, threadIdx.x, E, n_slots, shared_slot, s_cnt, s_raw, st);
     if (st) atomicOr(s_status, st);
     __syncthreads();
 }
@@ -217,68 +263,228 @@ __device__ void scan_experts(int E, int T, int k, int shared_slot, const int32_t
 }
 
 // ---------------------------------------------------------------------------------------
-// Fused single-workgroup routing for T*k <= kFusedMaxPairs.
+// Fused single-workgroup routing for T*k <= kFusedMaxPairs (few tokens: decode).  Four
+// barriers separate five phases:
+//   A  slot-table entry per thread, zeroed counters, logits of each wave's first token batch;
+//   B  experts per slot counted; top-k per token (a wave per token, kTopkBatch tokens per wave
+//      with their logits loaded together);
+//   C  usable slot per expert; every 64-pair chunk (one wave) ranks its pairs among the pairs of
+//      the same expert with ballots and records its per-expert count;
+//   D  one wave scans the experts (hit/miss offsets, groups, GEMM tile map, counts) and writes
+//      them out while the other waves add up, for each of their pairs, the counts of the earlier
+//      chunks of the same expert;
+//   E  each pair's list position = expert offset + earlier chunks + rank in chunk.
+// The within-expert order is the pair index: the lists equal a stable counting sort.
 constexpr int kFusedThreads = 1024;
 constexpr int kFusedWaves = kFusedThreads / kWave;
+constexpr int kTopkBatch = 4;
+constexpr int kFusedPairsPerThread = kFusedMaxPairs / kFusedThreads;
 
 template <int NPL>
 __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     extern __shared__ int32_t lds[];
-    const int E = a.E, k = a.k, T = a.T, P = T * k;
-    int32_t *s_raw = lds;                    // E
-    int32_t *s_eff = s_raw + E;              // E
-    int32_t *s_tot = s_eff + E;              // E
-    int32_t *s_hoff = s_tot + E;             // E+1
-    int32_t *s_moff = s_hoff + E + 1;        // E+1
-    int32_t *s_gidx = s_moff + E + 1;        // E
-    int32_t *s_ids = s_gidx + E;             // P
-    float *s_w = reinterpret_cast<float *>(s_ids + P);   // P
-    int32_t *s_wh = reinterpret_cast<int32_t *>(s_w + P);  // kFusedWaves * E
-    int *s_status = s_wh + kFusedWaves * E;  // 1
+    const int E = a.E, k = a.k, T = a.T, P = T * k, nch = (P + kWave - 1) / kWave;
+    const int ncnt = a.n_slots <= kSlotCountCap ? a.n_slots : 0;
+    int32_t *s_raw = lds;                                   // E
+    int32_t *s_eff = s_raw + E;                             // E
+    int32_t *s_hoff = s_eff + E;                            // E+1
+    int32_t *s_moff = s_hoff + E + 1;                       // E+1
+    int32_t *s_ids = s_moff + E + 1;                        // P
+    float *s_w = reinterpret_cast<float *>(s_ids + P);      // P
+    int32_t *s_wh = reinterpret_cast<int32_t *>(s_w + P);   // [nch][E] pairs per chunk and expert
+    int32_t *s_cnt = s_wh + nch * E;                        // [ncnt] experts per slot
+    int *s_status = s_cnt + ncnt;                           // 1
+    const int tid = threadIdx.x, wave = tid / kWave, lane = lane_id();
 
-    // issue the slot-table load first; its latency overlaps the top-k
-    const int raw = threadIdx.x < E ? a.slot_table[threadIdx.x] : -1;
-    if (threadIdx.x == 0) *s_status = 0;
-    for (int i = threadIdx.x; i < kFusedWaves * E; i += blockDim.x) s_wh[i] = 0;
+    // ---- A
+    const int raw = tid < E ? a.slot_table[tid] : -1;
+    uint32_t key0[kTopkBatch][NPL];
+#pragma unroll
+    for (int b = 0; b < kTopkBatch; ++b) {
+        const int t = wave + b * kFusedWaves;
+        if (t < T) topk_load<NPL>(a.logits + static_cast<size_t>(t) * E, E, key0[b]);
+    }
+    for (int i = tid; i < nch * E; i += kFusedThreads) s_wh[i] = 0;
+    for (int i = tid; i < ncnt; i += kFusedThreads) s_cnt[i] = 0;
+    if (tid == 0) *s_status = 0;
+    if (tid < E) s_raw[tid] = raw;
+    __syncthreads();
 
-    const int wave = threadIdx.x / kWave, lane = lane_id();
-    for (int t = wave; t < T; t += kFusedWaves) {
+    // ---- B
+    slot_count(raw, E, a.n_slots, s_cnt);
+    auto select = [&](uint32_t (&key)[NPL], int t) {
         int id;
         float w;
-        wave_topk<NPL>(a.logits + static_cast<size_t>(t) * E, E, k, a.gating, id, w);
+        topk_select<NPL>(key, k, a.gating, id, w);
         if (lane < k) {
             s_ids[t * k + lane] = id;
             s_w[t * k + lane] = w;
             a.ro.topk_ids[t * k + lane] = id;
             a.ro.topk_w[t * k + lane] = w;
         }
+    };
+#pragma unroll
+    for (int b = 0; b < kTopkBatch; ++b) {
+        const int t = wave + b * kFusedWaves;
+        if (t < T) select(key0[b], t);
     }
-    validate_slots(raw, E, a.n_slots, a.shared_slot, s_raw, s_eff, s_status);
-    // each wave owns a contiguous run of pairs; count its pairs per expert
-    const int per = (P + kFusedWaves - 1) / kFusedWaves;
-    const int p0 = min(P, wave * per), p1 = min(P, p0 + per);
-    int32_t *wh = s_wh + wave * E;
-    for (int p = p0 + lane; p < p1; p += kWave) atomicAdd(&wh[s_ids[p]], 1);
-    __syncthreads();
-    // per expert: exclusive offsets of each wave's run, total
-    for (int e = threadIdx.x; e < E; e += blockDim.x) {
-        int run = 0;
-        for (int w = 0; w < kFusedWaves; ++w) {
-            const int c = s_wh[w * E + e];
-            s_wh[w * E + e] = run;
-            run += c;
+    for (int t0 = kTopkBatch * kFusedWaves; t0 < T; t0 += kTopkBatch * kFusedWaves) {
+        uint32_t key[kTopkBatch][NPL];
+#pragma unroll
+        for (int b = 0; b < kTopkBatch; ++b) {
+            const int t = t0 + wave + b * kFusedWaves;
+            if (t < T) topk_load<NPL>(a.logits + static_cast<size_t>(t) * E, E, key[b]);
         }
-        s_tot[e] = run;
+#pragma unroll
+        for (int b = 0; b < kTopkBatch; ++b) {
+            const int t = t0 + wave + b * kFusedWaves;
+            if (t < T) select(key[b], t);
+        }
     }
     __syncthreads();
-    scan_experts(E, T, k, a.shared_slot, s_tot, s_eff, s_hoff, s_moff, s_gidx, s_status, a.ro, a.wv);
-    __syncthreads();
-    for (int e = threadIdx.x; e < E; e += blockDim.x) {
-        const int b = s_eff[e] >= 0 ? s_hoff[e] : s_moff[e];
-        for (int w = 0; w < kFusedWaves; ++w) s_wh[w * E + e] += b;
+
+    // ---- C
+    if (tid < E) {
+        int st = 0;
+        s_eff[tid] = slot_check(raw, tid, E, a.n_slots, a.shared_slot, s_cnt, s_raw, st);
+        if (st) atomicOr(s_status, st);
+    }
+    // pair p = tid + i * kFusedThreads lies in chunk p / 64, which is this wave's
+    int pe[kFusedPairsPerThread], prank[kFusedPairsPerThread], pre[kFusedPairsPerThread];
+#pragma unroll
+    for (int i = 0; i < kFusedPairsPerThread; ++i) {
+        const int p = tid + i * kFusedThreads;
+        const bool act = p < P;
+        const uint64_t live = __ballot(act);
+        pe[i] = 0;
+        prank[i] = 0;
+        pre[i] = 0;
+        if (live == 0) continue;
+        const int e = act ? s_ids[p] : 0;
+        const uint64_t same = match_lanes(static_cast<uint32_t>(e), a.nbits, live);
+        const int rank = __popcll(same & lanemask_lt());
+        if (act && rank == __popcll(same) - 1) s_wh[(p / kWave) * E + e] = rank + 1;
+        pe[i] = e;
+        prank[i] = rank;
     }
     __syncthreads();
-    scatter_run(p0, p1, k, a.nbits, s_ids, s_w, s_eff, wh, a.ro, a.wv);
+
+    // ---- D
+    auto chunk_prefix = [&]() {
+#pragma unroll
+        for (int i = 0; i < kFusedPairsPerThread; ++i) {
+            const int p = tid + i * kFusedThreads;
+            if (p < P) {
+                int acc = 0;
+                for (int c = 0; c < p / kWave; ++c) acc += s_wh[c * E + pe[i]];
+                pre[i] = acc;
+            }
+        }
+    };
+    if (wave != 0) {
+        chunk_prefix();
+    } else {
+        // lane l owns experts [l*epl, l*epl + epl)
+        const int epl = (E + kWave - 1) / kWave;
+        const int e0 = min(E, lane * epl), e1 = min(E, e0 + epl);
+        uint32_t h = 0, m = 0, g = 0, mx = 0, mtl = 0;
+        for (int e = e0; e < e1; ++e) {
+            int tot = 0;
+            for (int c = 0; c < nch; ++c) tot += s_wh[c * E + e];
+            const bool hit = s_eff[e] >= 0;
+            h += hit ? tot : 0;
+            m += hit ? 0 : tot;
+            g += (hit && tot > 0) ? 1 : 0;
+            mx += (!hit && tot > 0) ? 1 : 0;
+            mtl += hit ? (tot + kGemmBM - 1) / kGemmBM : 0;
+        }
+        const uint32_t hi = wave_incl_scan_u32(h), mi = wave_incl_scan_u32(m);
+        const uint32_t gi = wave_incl_scan_u32(g), xi = wave_incl_scan_u32(mx);
+        const uint32_t ti = wave_incl_scan_u32(mtl);
+        uint32_t hrun = hi - h, mrun = mi - m, grun = gi - g, trun = ti - mtl;
+        for (int e = e0; e < e1; ++e) {
+            int tot = 0;
+            for (int c = 0; c < nch; ++c) tot += s_wh[c * E + e];
+            const int slot = s_eff[e];
+            const bool hit = slot >= 0;
+            s_hoff[e] = hrun;
+            s_moff[e] = mrun;
+            a.ro.hit_off[e] = hrun;
+            a.ro.miss_off[e] = mrun;
+            if (hit && tot > 0) {
+                a.wv.grp_slot[grun] = slot;
+                a.wv.grp_beg[grun] = hrun;
+                a.wv.grp_len[grun] = tot;
+                a.wv.grp_mt_off[grun] = trun;
+                const int nmt = (tot + kGemmBM - 1) / kGemmBM;
+                for (int i = 0; i < nmt; ++i) a.wv.mt_group[trun + i] = grun;
+            }
+            hrun += hit ? tot : 0;
+            mrun += hit ? 0 : tot;
+            grun += (hit && tot > 0) ? 1 : 0;
+            trun += hit ? (tot + kGemmBM - 1) / kGemmBM : 0;
+        }
+        const uint32_t nh = readlane_u32(hi, kWave - 1), nm = readlane_u32(mi, kWave - 1);
+        const uint32_t U = readlane_u32(gi, kWave - 1), mexp = readlane_u32(xi, kWave - 1);
+        const uint32_t MT = readlane_u32(ti, kWave - 1);
+        if (lane == kWave - 1) {
+            s_hoff[E] = nh;
+            s_moff[E] = nm;
+            a.ro.hit_off[E] = nh;
+            a.ro.miss_off[E] = nm;
+            a.ro.counts[0] = nh;
+            a.ro.counts[1] = nm;
+            a.ro.counts[2] = mexp;
+            a.ro.counts[3] = *s_status;
+            const int shared = a.shared_slot;
+            const uint32_t smt = shared >= 0 ? (T + kGemmBM - 1) / kGemmBM : 0;
+            const uint32_t G = U + (shared >= 0 ? 1 : 0);
+            a.wv.grp_meta[0] = G;
+            a.wv.grp_meta[1] = U;
+            a.wv.grp_meta[2] = nh;
+            a.wv.grp_meta[3] = T;
+            a.wv.grp_meta[4] = MT + smt;
+            if (shared >= 0) {
+                a.wv.grp_slot[U] = shared;
+                a.wv.grp_beg[U] = nh;
+                a.wv.grp_len[U] = T;
+                a.wv.grp_mt_off[U] = MT;
+                for (uint32_t i = 0; i < smt; ++i) a.wv.mt_group[MT + i] = U;
+            }
+            a.wv.grp_mt_off[G] = MT + smt;
+        }
+        chunk_prefix();
+    }
+    __syncthreads();
+
+    // ---- E
+    const int nh = s_hoff[E], nm = s_moff[E];
+#pragma unroll
+    for (int i = 0; i < kFusedPairsPerThread; ++i) {
+        const int p = tid + i * kFusedThreads;
+        if (p < P) {
+            const int e = pe[i], slot = s_eff[e];
+            const int pos = (slot >= 0 ? s_hoff[e] : s_moff[e]) + pre[i] + prank[i];
+            a.ro.topk_slot[p] = slot;
+            if (slot >= 0) {
+                a.ro.hit_pairs[pos] = p;
+                a.wv.row_tok[pos] = p / k;
+                a.wv.row_gate[pos] = s_w[p];
+            } else {
+                a.ro.miss_pairs[pos] = p;
+            }
+        }
+    }
+    for (int i = tid; i < P; i += kFusedThreads) {
+        if (i >= nh) a.ro.hit_pairs[i] = -1;
+        if (i >= nm) a.ro.miss_pairs[i] = -1;
+    }
+    if (a.shared_slot >= 0) {
+        for (int t = tid; t < T; t += kFusedThreads) {
+            a.wv.row_tok[nh + t] = t;
+            a.wv.row_gate[nh + t] = 1.0f;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -313,9 +519,10 @@ __global__ __launch_bounds__(1024) void route_scan(RouteArgs a, int nblk) {
     int32_t *s_moff = s_hoff + E + 1, *s_gidx = s_moff + E + 1;
     int *s_status = s_gidx + E;
     int32_t *s_part = s_status + 1;          // [parts][E] partial block sums
+    int32_t *s_cnt = s_part + a.scan_parts * E;   // [min(n_slots, kSlotCountCap)]
     const int raw = threadIdx.x < E ? a.slot_table[threadIdx.x] : -1;
     if (threadIdx.x == 0) *s_status = 0;
-    validate_slots(raw, E, a.n_slots, a.shared_slot, s_raw, s_eff, s_status);
+    validate_slots(raw, E, a.n_slots, a.shared_slot, s_raw, s_cnt, s_eff, s_status);
     // `parts` threads per expert, each over a contiguous range of the blocks
     const int parts = a.scan_parts;
     const int e = threadIdx.x % E, part = threadIdx.x / E;
@@ -381,7 +588,8 @@ __global__ __launch_bounds__(64) void route_scatter(RouteArgs a) {
 template <int NPL>
 static hipError_t launch_route_npl(RouteArgs a, hipStream_t s) {
     const int P = a.T * a.k;
-    const int fused_lds = fused_route_lds_bytes(a.E, P);
+    const int ncnt = a.n_slots <= kSlotCountCap ? a.n_slots : 0;
+    const int fused_lds = 4 * (4 * a.E + 2 + 2 * P + ((P + kWave - 1) / kWave) * a.E + ncnt + 1);
     if (P <= kFusedMaxPairs && fused_lds <= kFusedMaxLds) {
         hipLaunchKernelGGL(route_fused<NPL>, dim3(1), dim3(kFusedThreads), fused_lds, s, a);
         return hipGetLastError();
@@ -389,8 +597,8 @@ static hipError_t launch_route_npl(RouteArgs a, hipStream_t s) {
     const int nblk = (a.T + kTokPerBlk - 1) / kTokPerBlk;
     a.scan_parts = max(1, min(1024 / a.E, nblk));
     hipLaunchKernelGGL(route_tokens<NPL>, dim3(nblk), dim3(256), 0, s, a);
-    hipLaunchKernelGGL(route_scan, dim3(1), dim3(1024), scan_route_lds_bytes(a.E, a.scan_parts), s,
-                       a, nblk);
+    const int scan_lds = 4 * (6 * a.E + 3 + a.scan_parts * a.E + ncnt);
+    hipLaunchKernelGGL(route_scan, dim3(1), dim3(1024), scan_lds, s, a, nblk);
     hipLaunchKernelGGL(route_scatter, dim3(nblk), dim3(64), 0, s, a);
     return hipGetLastError();
 }
