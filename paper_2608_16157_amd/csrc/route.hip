@@ -23,54 +23,87 @@ template <int NPL>
 __device__ __forceinline__ void topk_load(const float *__restrict__ row, int E, uint32_t (&key)[NPL]) {
     const int lane = lane_id();
     float v[NPL];
+    // unconditional loads of a clamped index: no branch, so no wait is forced between tokens
 #pragma unroll
-    for (int i = 0; i < NPL; ++i) {
-        const int e = lane * NPL + i;
-        v[i] = e < E ? row[e] : 0.f;
+    for (int i = 0; i < NPL; ++i) v[i] = row[min(lane * NPL + i, E - 1)];
+    // out-of-range entries are masked arithmetically (a select would let the compiler sink the
+    // load into a branch again)
+#pragma unroll
+    for (int i = 0; i < NPL; ++i)
+        key[i] = order_key(v[i]) & (0u - static_cast<uint32_t>(lane * NPL + i < E));
+}
+
+template <int NPL, int NB>
+__device__ __forceinline__ void topk_select_n(uint32_t (&key)[NB][NPL], int k, int gating,
+                                              int (&my_id)[NB], float (&my_w)[NB]) {
+    // NB tokens' rounds interleaved: their reductions are independent, so the latencies of the
+    // DPP and readlane chains overlap
+    const int lane = lane_id();
+    uint32_t mine[NB];
+    int mine_e[NB];
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+        mine[b] = 0u;
+        mine_e[b] = -1;
+    }
+    for (int j = 0; j < k; ++j) {
+        uint32_t best[NB], m[NB];
+        int bi[NB];
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            best[b] = 0u;
+            bi[b] = 0;
+#pragma unroll
+            for (int i = 0; i < NPL; ++i) {
+                if (key[b][i] > best[b]) {
+                    best[b] = key[b][i];
+                    bi[b] = i;
+                }
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < NB; ++b) m[b] = wave_max_u32(best[b]);
+#pragma unroll
+        for (int b = 0; b < NB; ++b) {
+            const uint64_t ball = __ballot(best[b] == m[b]);
+            const int w = static_cast<int>(__builtin_ctzll(ball));
+            const int wbi = __builtin_amdgcn_readlane(bi[b], w);
+            if (lane == w) {
+#pragma unroll
+                for (int i = 0; i < NPL; ++i)
+                    if (i == wbi) key[b][i] = 0u;
+            }
+            if (lane == j) {
+                mine[b] = m[b];
+                mine_e[b] = w * NPL + wbi;
+            }
+        }
     }
 #pragma unroll
-    for (int i = 0; i < NPL; ++i) key[i] = lane * NPL + i < E ? order_key(v[i]) : 0u;
+    for (int b = 0; b < NB; ++b) {
+        const float top = key_to_float(readlane_u32(mine[b], 0));
+        float z = 0.f;
+        if (lane < k) {
+            const float l = key_to_float(mine[b]);
+            z = gating == FT_GATE_SOFTMAX_TOPK_RENORM ? expf(l - top) : 1.0f / (1.0f + expf(-l));
+        }
+        const float sum = wave_sum_f32(z);
+        my_id[b] = lane < k ? mine_e[b] : -1;
+        my_w[b] = lane < k ? z / sum : 0.f;
+    }
 }
 
 template <int NPL>
 __device__ __forceinline__ void topk_select(uint32_t (&key)[NPL], int k, int gating, int &my_id,
                                             float &my_w) {
-    const int lane = lane_id();
-    uint32_t mine = 0u;
-    int mine_e = -1;
-    for (int j = 0; j < k; ++j) {
-        uint32_t best = 0u;
-        int bi = 0;
+    uint32_t kk[1][NPL];
 #pragma unroll
-        for (int i = 0; i < NPL; ++i) {
-            if (key[i] > best) {
-                best = key[i];
-                bi = i;
-            }
-        }
-        const uint32_t m = wave_max_u32(best);
-        const uint64_t ball = __ballot(best == m);
-        const int w = static_cast<int>(__builtin_ctzll(ball));
-        const int wbi = __builtin_amdgcn_readlane(bi, w);
-        if (lane == w) {
-#pragma unroll
-            for (int i = 0; i < NPL; ++i)
-                if (i == wbi) key[i] = 0u;
-        }
-        if (lane == j) {
-            mine = m;
-            mine_e = w * NPL + wbi;
-        }
-    }
-    const float top = key_to_float(readlane_u32(mine, 0));
-    float z = 0.f;
-    if (lane < k) {
-        const float l = key_to_float(mine);
-        z = gating == FT_GATE_SOFTMAX_TOPK_RENORM ? expf(l - top) : 1.0f / (1.0f + expf(-l));
-    }
-    const float sum = wave_sum_f32(z);
-    my_id = lane < k ? mine_e : -1;
-    my_w = lane < k ? z / sum : 0.f;
+    for (int i = 0; i < NPL; ++i) kk[0][i] = key[i];
+    int id[1];
+    float w[1];
+    topk_select_n<NPL, 1>(kk, k, gating, id, w);
+    my_id = id[0];
+    my_w = w[0];
 }
 
 template <int NPL>
@@ -275,6 +308,16 @@ __device__ void scan_experts(int E, int T, int k, int shared_slot, const int32_t
 //      chunks of the same expert;
 //   E  each pair's list position = expert offset + earlier chunks + rank in chunk.
 // The within-expert order is the pair index: the lists equal a stable counting sort.
+// Waves of the fused router exchange data through LDS only, so its barriers wait for LDS
+// operations alone: outstanding global loads and stores do not hold a barrier up (a
+// __syncthreads would wait for every store of the phase to be acknowledged).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xF | (0x7 << 4) | (0x0 << 8) | (0x3 << 14));   // lgkmcnt(0)
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
+
 constexpr int kFusedThreads = 1024;
 constexpr int kFusedWaves = kFusedThreads / kWave;
 constexpr int kTopkBatch = 4;
@@ -283,6 +326,8 @@ constexpr int kFusedPairsPerThread = kFusedMaxPairs / kFusedThreads;
 template <int NPL>
 __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     extern __shared__ int32_t lds[];
+    // tokens per wave batch, within the 128 registers a 1024-thread workgroup leaves a lane
+    constexpr int NBT = NPL >= 16 ? 1 : (NPL >= 8 ? 2 : kTopkBatch);
     const int E = a.E, k = a.k, T = a.T, P = T * k, nch = (P + kWave - 1) / kWave;
     const int ncnt = a.n_slots <= kSlotCountCap ? a.n_slots : 0;
     int32_t *s_raw = lds;                                   // E
@@ -298,50 +343,68 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
 
     // ---- A
     const int raw = tid < E ? a.slot_table[tid] : -1;
-    uint32_t key0[kTopkBatch][NPL];
+    // tokens of this wave: wave, wave + 16, ...; the first NBT are loaded here
+    const int nmine = T > wave ? (T - wave + kFusedWaves - 1) / kFusedWaves : 0;
+    uint32_t key0[NBT][NPL];
 #pragma unroll
-    for (int b = 0; b < kTopkBatch; ++b) {
-        const int t = wave + b * kFusedWaves;
-        if (t < T) topk_load<NPL>(a.logits + static_cast<size_t>(t) * E, E, key0[b]);
-    }
+    for (int b = 0; b < NBT; ++b)
+        topk_load<NPL>(a.logits + static_cast<size_t>(min(wave + b * kFusedWaves, T - 1)) * E, E, key0[b]);
     for (int i = tid; i < nch * E; i += kFusedThreads) s_wh[i] = 0;
     for (int i = tid; i < ncnt; i += kFusedThreads) s_cnt[i] = 0;
     if (tid == 0) *s_status = 0;
     if (tid < E) s_raw[tid] = raw;
-    __syncthreads();
+    lds_barrier();
 
     // ---- B
     slot_count(raw, E, a.n_slots, s_cnt);
-    auto select = [&](uint32_t (&key)[NPL], int t) {
-        int id;
-        float w;
-        topk_select<NPL>(key, k, a.gating, id, w);
-        if (lane < k) {
+    auto put = [&](int t, int id, float w) {
+        if (t < T && lane < k) {
             s_ids[t * k + lane] = id;
             s_w[t * k + lane] = w;
-            a.ro.topk_ids[t * k + lane] = id;
-            a.ro.topk_w[t * k + lane] = w;
         }
     };
+    auto select_batch = [&](uint32_t (&key)[NBT][NPL], int tb, int n) {
+        // n (wave-uniform) of the batch's tokens are real; tokens tb + 16 b
+        int id[NBT];
+        float w[NBT];
+        if constexpr (NBT >= 4) {
+            if (n >= 3) {
+                topk_select_n<NPL, 4>(key, k, a.gating, id, w);
 #pragma unroll
-    for (int b = 0; b < kTopkBatch; ++b) {
-        const int t = wave + b * kFusedWaves;
-        if (t < T) select(key0[b], t);
-    }
-    for (int t0 = kTopkBatch * kFusedWaves; t0 < T; t0 += kTopkBatch * kFusedWaves) {
-        uint32_t key[kTopkBatch][NPL];
-#pragma unroll
-        for (int b = 0; b < kTopkBatch; ++b) {
-            const int t = t0 + wave + b * kFusedWaves;
-            if (t < T) topk_load<NPL>(a.logits + static_cast<size_t>(t) * E, E, key[b]);
+                for (int b = 0; b < NBT; ++b)
+                    if (b < n) put(tb + b * kFusedWaves, id[b], w[b]);
+                return;
+            }
         }
+        if constexpr (NBT >= 2) {
+            if (n >= 2) {
+                uint32_t k2[2][NPL];
 #pragma unroll
-        for (int b = 0; b < kTopkBatch; ++b) {
-            const int t = t0 + wave + b * kFusedWaves;
-            if (t < T) select(key[b], t);
+                for (int i = 0; i < NPL; ++i) {
+                    k2[0][i] = key[0][i];
+                    k2[1][i] = key[1][i];
+                }
+                int id2[2];
+                float w2[2];
+                topk_select_n<NPL, 2>(k2, k, a.gating, id2, w2);
+                put(tb, id2[0], w2[0]);
+                put(tb + kFusedWaves, id2[1], w2[1]);
+                return;
+            }
         }
+        topk_select<NPL>(key[0], k, a.gating, id[0], w[0]);
+        put(tb, id[0], w[0]);
+    };
+    if (nmine > 0) select_batch(key0, wave, min(nmine, NBT));
+    for (int b0 = NBT; b0 < nmine; b0 += NBT) {
+        uint32_t key[NBT][NPL];
+        const int tb = wave + b0 * kFusedWaves;
+#pragma unroll
+        for (int b = 0; b < NBT; ++b)
+            topk_load<NPL>(a.logits + static_cast<size_t>(min(tb + b * kFusedWaves, T - 1)) * E, E, key[b]);
+        select_batch(key, tb, min(nmine - b0, NBT));
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- C
     if (tid < E) {
@@ -367,7 +430,7 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
         pe[i] = e;
         prank[i] = rank;
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- D
     auto chunk_prefix = [&]() {
@@ -455,7 +518,7 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
         }
         chunk_prefix();
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- E
     const int nh = s_hoff[E], nm = s_moff[E];
@@ -478,6 +541,8 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     for (int i = tid; i < P; i += kFusedThreads) {
         if (i >= nh) a.ro.hit_pairs[i] = -1;
         if (i >= nm) a.ro.miss_pairs[i] = -1;
+        a.ro.topk_ids[i] = s_ids[i];
+        a.ro.topk_w[i] = s_w[i];
     }
     if (a.shared_slot >= 0) {
         for (int t = tid; t < T; t += kFusedThreads) {
