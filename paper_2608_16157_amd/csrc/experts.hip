@@ -21,8 +21,13 @@
 namespace ftmoe {
 
 // Tuning constants (measured on MI355X; see the design notes for the sweep).
+// weight rows per work item = 16 * NB; fp8 weights take wider items (their activation loads,
+// bf16, are twice the weight bytes per element, so one activation load should feed more rows)
 #ifndef FT_GEMV_NB
 #define FT_GEMV_NB 2
+#endif
+#ifndef FT_GEMV_NB_FP8
+#define FT_GEMV_NB_FP8 4
 #endif
 #ifndef FT_GEMV_MT_MAX
 #define FT_GEMV_MT_MAX 2
@@ -284,7 +289,7 @@ __global__ __launch_bounds__(256) void zero_out(float *out, size_t n4) {
 
 template <int WT, int EPI>
 static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
-    constexpr int NB = FT_GEMV_NB;
+    constexpr int NB = WT == FT_DT_FP8E4M3FN_B128 ? FT_GEMV_NB_FP8 : FT_GEMV_NB;
     const int tiles = EPI == EPI_GATEUP ? a.I / (8 * NB) : a.H / (16 * NB);
     hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
                        s, a, tiles);
