@@ -253,6 +253,91 @@ def moe_partial(desc: dict, banks: dict, logits, slot_table, x, tokens=None):
 
 
 # ----------------------------------------------------------------------------------------
+# Device-side cache control: the fill / CPU split of the misses and LRU victim selection
+# (Section 3.2, Eq. (miss-partition) to Eq. (dynamic-split) and the LRU residency space;
+# Section 4.1, device-side cache control)
+# ----------------------------------------------------------------------------------------
+#
+# Readings taken where the paper leaves the details open:
+# * q: for m >= 1 missing experts, q* = m B_P / B_H rounded half up, then at least 1, at most m,
+#   at most K (the LRU candidates one pass yields) and at most the number of evictable slots.
+#   When B_H <= B_P there is no residual host bandwidth and every miss is filled (q = m before
+#   the caps).  m = 0 gives q = 0.
+# * which misses are filled: the most demanded (routed pairs in this step) first, ties to the
+#   lower expert id; the rest execute on the CPU, listed by ascending id.
+# * recency: a slot's stamp is the last step its expert was demanded (hit or filled).  Victims
+#   are the least recently used slots that were not hit in this step and are not the shared
+#   expert's slot; empty slots count as oldest; equal stamps go to the lower slot id.  The i-th
+#   filled expert takes the i-th victim.
+# * a routing whose slot table was faulty (status != 0) changes nothing: every missing expert is
+#   left to the CPU.
+
+
+def fill_count(m: int, b_pcie: float, b_host: float, k_max: int, n_evictable: int) -> int:
+    """Number of misses served by cache fills, q (Section 3.2, Eq. (dynamic-split))."""
+    if m <= 0:
+        return 0
+    if b_host <= b_pcie:
+        q = m
+    else:
+        q = int(np.floor(m * (b_pcie / b_host) + 0.5))
+    q = max(1, q)
+    return min(q, m, k_max, n_evictable)
+
+
+def cache_plan(desc: dict, routing: dict, slot_table, slot_expert, slot_stamp, b_pcie: float,
+               b_host: float, k_max: int, step: int) -> dict:
+    """Fill / CPU split of one layer step's misses and the cache update it implies.
+
+    routing : the dict ``route`` returns for this step's logits and ``slot_table``
+    slot_expert [n_slots] int32 (-1 = empty), slot_stamp [n_slots] uint32: the cache state.
+    Returns q, m, the fill list (expert, slot, evicted expert), the CPU list, and the new
+    slot_table, slot_expert, slot_stamp and topk_slot.
+    """
+    E, k = desc["n_experts"], desc["top_k"]
+    n_slots, shared = desc["n_slots"], desc["shared_slot"]
+    hit_off, miss_off = routing["hit_off"], routing["miss_off"]
+    table = np.array(slot_table, dtype=np.int32).copy()
+    sexp = np.array(slot_expert, dtype=np.int32).copy()
+    stamp = np.array(slot_stamp, dtype=np.uint32).copy()
+    tslot = routing["topk_slot"].copy()
+    missing = [e for e in range(E) if miss_off[e + 1] > miss_off[e]]
+    m = len(missing)
+    out = dict(m=m, status=int(routing["status"]), fill_expert=[], fill_slot=[], evict_expert=[])
+    if routing["status"] != 0:
+        out.update(q=0, cpu_expert=sorted(missing), slot_table=table, slot_expert=sexp,
+                   slot_stamp=stamp, topk_slot=tslot)
+        return out
+    hit_slots = sorted({int(table[e]) for e in range(E) if hit_off[e + 1] > hit_off[e]})
+    old_stamp = stamp.copy()
+    for s in hit_slots:
+        stamp[s] = step
+    evictable = [s for s in range(n_slots) if s != shared and s not in hit_slots]
+    age = lambda s: (0 if sexp[s] < 0 else 1 + int(old_stamp[s]), s)
+    victims = sorted(evictable, key=age)
+    q = fill_count(m, b_pcie, b_host, k_max, len(evictable))
+    demand = {e: int(miss_off[e + 1] - miss_off[e]) for e in missing}
+    by_demand = sorted(missing, key=lambda e: (-demand[e], e))
+    fills, cpu = by_demand[:q], sorted(by_demand[q:])
+    for i, e in enumerate(fills):
+        v = victims[i]
+        old = int(sexp[v])
+        out["fill_expert"].append(e)
+        out["fill_slot"].append(v)
+        out["evict_expert"].append(old)
+        if old >= 0:
+            table[old] = -1
+        table[e] = v
+        sexp[v] = e
+        stamp[v] = step
+        for p in routing["miss_pairs"][miss_off[e]:miss_off[e + 1]]:
+            tslot[int(p) // k, int(p) % k] = v
+    out.update(q=q, cpu_expert=cpu, slot_table=table, slot_expert=sexp, slot_stamp=stamp,
+               topk_slot=tslot)
+    return out
+
+
+# ----------------------------------------------------------------------------------------
 # Error metric used by the parity tests
 # ----------------------------------------------------------------------------------------
 

@@ -328,3 +328,189 @@ def test_config_residency_counts():
     for name, n in want.items():
         cfg = CONFIGS[name]
         assert int(math.floor(cfg.resident_frac * cfg.n_experts + 1e-9)) == n
+
+
+# ---------------------------------------------------------------- device-side cache control
+
+def test_fill_count_closed_forms():
+    """q of Section 3.2 (Eq. (dynamic-split)) against hand-computed values for the bandwidth
+    ratios of Table 1, the at-least-one-fill rule, half-up rounding and the caps."""
+    cases = [
+        (4, 11.8, 47.5, 1),    # Fig. 2 example, RTX 4060 laptop: 0.99 -> 1
+        (4, 52.7, 77.3, 3),    # RTX 5090 server: 2.73 -> 3
+        (2, 52.7, 77.3, 1),    # 1.36 -> 1
+        (1, 52.7, 77.3, 1),    # 0.68 -> 1
+        (4, 25.1, 63.2, 2),    # RTX 4090: 1.59 -> 2
+        (8, 25.1, 63.2, 3),    # 3.18 -> 3
+        (5, 25.3, 56.7, 2),    # RTX 3090: 2.23 -> 2
+        (4, 49.0, 53.8, 4),    # RTX 5090 desktop: 3.64 -> 4
+        (3, 51.5, 178.0, 1),   # RTX PRO 6000: 0.87 -> 1
+        (16, 51.5, 178.0, 5),  # 4.63 -> 5
+        (2, 1.0, 4.0, 1),      # 0.5 rounds up
+        (6, 1.0, 4.0, 2),      # 1.5 -> 2
+        (10, 1.0, 4.0, 3),     # 2.5 -> 3
+        (3, 1.0, 100.0, 1),    # 0.03 -> at least one fill
+        (7, 5.0, 5.0, 7),      # B_H == B_P: no residual host bandwidth, fill everything
+        (7, 6.0, 5.0, 7),      # B_H < B_P
+        (0, 1.0, 4.0, 0),      # no miss, no fill
+    ]
+    for m, bp, bh, q in cases:
+        assert oracle.fill_count(m, bp, bh, 64, 1000) == q, (m, bp, bh)
+    assert oracle.fill_count(8, 6.0, 5.0, 3, 1000) == 3       # K caps
+    assert oracle.fill_count(8, 6.0, 5.0, 64, 2) == 2         # evictable slots cap
+    assert oracle.fill_count(3, 1.0, 100.0, 64, 0) == 0       # nothing evictable
+
+
+def _route_ranked(E, k, rank_order, slot_table, n_slots, shared_slot=-1):
+    logits = np.full((len(rank_order), E), -10.0, dtype=np.float32)
+    for t, order in enumerate(rank_order):
+        for j, e in enumerate(order):
+            logits[t, e] = 5.0 - j
+    desc = dict(n_experts=E, top_k=k, gating=0, n_slots=n_slots, shared_slot=shared_slot)
+    return desc, oracle.route(desc, logits, np.asarray(slot_table, np.int32))
+
+
+def test_cache_plan_fig2_golden():
+    with open(os.path.join(GOLDEN, "fig2_cache_plan.json")) as f:
+        g = json.load(f)
+    desc, r = _route_ranked(g["n_experts"], g["top_k"], g["logits_rank_order"], g["slot_table"],
+                            g["n_slots"])
+    plan = oracle.cache_plan(desc, r, g["slot_table"], g["slot_expert"], g["slot_stamp"],
+                             g["b_pcie"], g["b_host"], g["max_fill"], g["step"])
+    ex = g["expect"]
+    assert plan["m"] == ex["m"] and plan["q"] == ex["q"]
+    for key in ("fill_expert", "fill_slot", "evict_expert", "cpu_expert"):
+        assert list(plan[key]) == ex[key], key
+    assert plan["slot_table"].tolist() == ex["slot_table"]
+    assert plan["slot_expert"].tolist() == ex["slot_expert"]
+    assert plan["slot_stamp"].tolist() == ex["slot_stamp"]
+    assert plan["topk_slot"][0].tolist() == ex["topk_slot_token0"]
+
+
+def test_cache_plan_is_textbook_lru_for_single_requests():
+    """One token, top-1, every miss filled: the planner must behave exactly like a textbook
+    LRU cache of n_slots entries over the request sequence (hit -> most recent; miss -> evict
+    the least recently used once full)."""
+    from collections import OrderedDict
+    rng = np.random.default_rng(5)
+    E, C = 12, 5
+    table = np.full(E, -1, np.int32)
+    sexp = np.full(C, -1, np.int32)
+    stamp = np.zeros(C, np.uint32)
+    lru = OrderedDict()
+    hits = 0
+    for step in range(1, 301):
+        e = int(rng.zipf(1.5) - 1) % E
+        desc, r = _route_ranked(E, 1, [[e]], table, C)
+        plan = oracle.cache_plan(desc, r, table, sexp, stamp, 2.0, 1.0, 4, step)
+        table, sexp, stamp = plan["slot_table"], plan["slot_expert"], plan["slot_stamp"]
+        if e in lru:
+            lru.move_to_end(e)
+            hits += 1
+            assert plan["q"] == 0
+        else:
+            if len(lru) == C:
+                lru.popitem(last=False)
+            lru[e] = True
+            assert plan["q"] == 1 and plan["fill_expert"] == [e]
+        assert sorted(lru) == sorted(int(x) for x in np.nonzero(table >= 0)[0])
+    assert 0 < hits < 300
+
+
+def _plan_case(rng, E, k, T, n_slots, shared, K, bp, bh):
+    """Random cache state (a valid slot table) and routing."""
+    n_res = int(rng.integers(0, min(E, n_slots - (1 if shared else 0)) + 1))
+    res = rng.choice(E, n_res, replace=False)
+    routed_slots = [s for s in range(n_slots) if not (shared and s == n_slots - 1)]
+    slots = rng.choice(routed_slots, n_res, replace=False)
+    table = np.full(E, -1, np.int32)
+    sexp = np.full(n_slots, -1, np.int32)
+    table[res] = slots
+    sexp[slots] = res
+    stamp = rng.integers(0, 40, n_slots).astype(np.uint32)
+    logits = rng.standard_normal((T, E)).astype(np.float32)
+    desc = dict(n_experts=E, top_k=k, gating=0, n_slots=n_slots,
+                shared_slot=n_slots - 1 if shared else -1)
+    return desc, logits, table, sexp, stamp
+
+
+def test_cache_plan_properties_brute_force():
+    rng = np.random.default_rng(11)
+    for case in range(300):
+        E = int(rng.integers(1, 24))
+        k = int(rng.integers(1, E + 1))
+        T = int(rng.integers(1, 6))
+        shared = bool(rng.integers(0, 2))
+        n_slots = int(rng.integers(1, 16)) + (1 if shared else 0)
+        K = int(rng.integers(1, 6))
+        bp, bh = float(rng.uniform(1, 60)), float(rng.uniform(1, 80))
+        desc, logits, table, sexp, stamp = _plan_case(rng, E, k, T, n_slots, shared, K, bp, bh)
+        r = oracle.route(desc, logits, table)
+        step = 50
+        plan = oracle.cache_plan(desc, r, table, sexp, stamp, bp, bh, K, step)
+        ids = r["topk_ids"]
+        routed = set(int(e) for e in ids.ravel())
+        missing = sorted(e for e in routed if table[e] < 0)
+        hit_slots = {int(table[e]) for e in routed if table[e] >= 0}
+        assert plan["m"] == len(missing) == r["m_unique_miss"]
+        evictable = [s for s in range(n_slots) if s not in hit_slots and s != desc["shared_slot"]]
+        q = plan["q"]
+        assert q == oracle.fill_count(len(missing), bp, bh, K, len(evictable))
+        # victims: repeatedly take the oldest evictable slot (empty first, then stamp, then id)
+        pool, want = list(evictable), []
+        for _ in range(q):
+            best = None
+            for s in pool:
+                empty = sexp[s] < 0     # an empty slot's stamp carries no meaning
+                key = (0 if empty else 1, 0 if empty else int(stamp[s]), s)
+                if best is None or key < best[0]:
+                    best = (key, s)
+            want.append(best[1])
+            pool.remove(best[1])
+        assert list(plan["fill_slot"]) == want
+        # fills: repeatedly take the most demanded missing expert (lowest id on ties)
+        demand = {e: int(np.count_nonzero(ids == e)) for e in missing}
+        pool, wantf = list(missing), []
+        for _ in range(q):
+            e = max(pool, key=lambda x: (demand[x], -x))
+            wantf.append(e)
+            pool.remove(e)
+        assert list(plan["fill_expert"]) == wantf
+        assert list(plan["cpu_expert"]) == sorted(pool)
+        assert list(plan["evict_expert"]) == [int(sexp[s]) for s in want]
+        # the new state is a consistent bijection and only fills / evictions changed
+        nt, ns, nst = plan["slot_table"], plan["slot_expert"], plan["slot_stamp"]
+        for e in range(E):
+            if nt[e] >= 0:
+                assert ns[nt[e]] == e
+        for s in range(n_slots):
+            if ns[s] >= 0:
+                assert nt[ns[s]] == s
+            exp_stamp = step if (s in hit_slots or s in want) else stamp[s]
+            assert nst[s] == exp_stamp
+        for e, s in zip(wantf, want):
+            assert nt[e] == s
+        for e in set(range(E)) - set(wantf) - {int(sexp[s]) for s in want if sexp[s] >= 0}:
+            assert nt[e] == table[e]
+        # routed pairs of filled experts now name their slot; all others are unchanged
+        for t in range(T):
+            for j in range(k):
+                e = int(ids[t, j])
+                if e in wantf:
+                    assert plan["topk_slot"][t, j] == want[wantf.index(e)]
+                else:
+                    assert plan["topk_slot"][t, j] == r["topk_slot"][t, j]
+
+
+def test_cache_plan_faulty_table_changes_nothing():
+    E, n_slots = 6, 4
+    table = np.array([0, 0, 1, -1, -1, -1], np.int32)           # experts 0 and 1 share slot 0
+    sexp = np.array([0, 2, -1, -1], np.int32)
+    stamp = np.array([3, 4, 5, 6], np.uint32)
+    desc, r = _route_ranked(E, 2, [[0, 3], [1, 4]], table, n_slots)
+    assert r["status"] != 0
+    plan = oracle.cache_plan(desc, r, table, sexp, stamp, 1.0, 2.0, 4, 9)
+    assert plan["q"] == 0 and plan["fill_expert"] == []
+    assert plan["cpu_expert"] == [0, 1, 3, 4]
+    assert np.array_equal(plan["slot_table"], table) and np.array_equal(plan["slot_expert"], sexp)
+    assert np.array_equal(plan["slot_stamp"], stamp)
