@@ -200,6 +200,69 @@ ft_status_t ft_moe_forward_profiled(const ft_moe_desc_t *desc, const ft_banks_t 
 ft_status_t ft_miss_list_to_host(const ft_moe_desc_t *desc, const ft_route_t *route, int32_t T,
                                  const ft_host_miss_t *host, void *stream);
 
+/*
+ * Device-side cache control of one layer step (Section 3.2: the m distinct missing experts
+ * are split into q cache fills and m - q CPU executions with q* = m B_P / B_H, Eq.
+ * (dynamic-split), rounded, at least one fill; the residency space is LRU: a hit refreshes an
+ * expert's recency, a fill evicts the least recently demanded expert.  Section 4.1: one kernel
+ * classifies, derives q, takes the first q of the K least-recently-used candidate slots found in
+ * one pass, rewrites routed ids into slot ids and leaves a fixed-shape copy list with a valid
+ * count).  Runs on the routing of this step (ft_route_only / ft_moe_forward with the same
+ * slot_table) and updates the cache state in place; the copies themselves are the caller's.
+ *
+ * Rules (where the paper leaves them open):
+ *   q = 0 if m = 0; else q = round_half_up(m * b_pcie / b_host) (q = m if b_host <= b_pcie),
+ *       at least 1, at most m, max_fill and the number of evictable slots.
+ *   Filled first: the missing experts with the most routed pairs in this step, ties to the
+ *       lower expert id; the rest are listed for the CPU in ascending id.
+ *   Evictable: slots not hit in this step, other than shared_slot.  Victim order: empty slots
+ *       (slot_expert -1) first, then ascending stamp, ties to the lower slot id.  The i-th filled
+ *       expert takes the i-th victim.
+ *   If the routing reported slot-table faults (route counts[3] != 0) nothing changes and every
+ *   missing expert is listed for the CPU.
+ *
+ * Cache state (device, caller-owned, updated in place):
+ *   slot_table  [E] int32   expert -> slot or -1; filled experts get their slot, evicted
+ *                           experts get -1
+ *   slot_expert [n_slots] int32   slot -> expert or -1 (must be the inverse of slot_table)
+ *   slot_stamp  [n_slots] uint32  step at which the slot's expert was last demanded; hit and
+ *                           filled slots take `step`.  Stamps must grow with the steps.
+ *   route->topk_slot        routed pairs of filled experts take the new slot id; pairs left to
+ *                           the CPU keep FT_SLOT_MISS.  route->hit/miss lists are not changed.
+ * Plan outputs (device, caller-owned):
+ *   fill_expert, fill_slot, evict_expert [max_fill] int32: fill i copies expert fill_expert[i]
+ *       into slot fill_slot[i], replacing evict_expert[i] (-1 if the slot was empty); entries
+ *       from q on are -1
+ *   cpu_expert [E] int32: missing experts left to the CPU, ascending; entries from m - q on -1
+ *   counts [4] int32: q, m - q, m, route status
+ * Limits: n_slots <= 4096, 1 <= max_fill <= 64, b_pcie > 0 and b_host > 0 (same unit).
+ * T == 0 enqueues nothing.
+ */
+typedef struct {
+    int32_t *slot_expert;
+    uint32_t *slot_stamp;
+} ft_cache_state_t;
+
+typedef struct {
+    double b_pcie;      /* B_P: pinned host-to-GPU expert transfer bandwidth */
+    double b_host;      /* B_H: host expert-processing bandwidth */
+    int32_t max_fill;   /* K: LRU candidates per step */
+    uint32_t step;      /* current step (the stamp written to hit and filled slots) */
+} ft_cache_policy_t;
+
+typedef struct {
+    int32_t *fill_expert;
+    int32_t *fill_slot;
+    int32_t *evict_expert;
+    int32_t *cpu_expert;
+    int32_t *counts;
+} ft_fill_plan_t;
+
+ft_status_t ft_cache_plan(const ft_moe_desc_t *desc, const ft_route_t *route, int32_t T,
+                          int32_t *slot_table, const ft_cache_state_t *state,
+                          const ft_cache_policy_t *policy, const ft_fill_plan_t *plan,
+                          void *stream);
+
 /* Static string for a status code. */
 const char *ft_status_string(ft_status_t status);
 

@@ -10,6 +10,7 @@ of the C ABI declared in ``include/ftmoe.h``:
     ft_moe_forward_profiled(desc, banks, logits, slot_table, x, T, out_partial, route, ws,
                             events, stream=None)
     ft_miss_list_to_host(desc, route, T, host, stream=None)
+    ft_cache_plan(desc, route, T, slot_table, state, policy, plan, stream=None)
     ft_status_string(status) -> str
 
 ``desc`` is a dict with the ft_moe_desc_t fields; ``route`` a RouteBuffers; ``banks`` a dict
@@ -34,7 +35,7 @@ FT_SLOT_MISS = -1
 FT_DEV_SLOT_RANGE, FT_DEV_SLOT_DUP, FT_DEV_SLOT_SHARED = 1, 2, 4
 
 EXPORTED = ("ft_moe_workspace_bytes", "ft_route_only", "ft_moe_forward",
-            "ft_moe_forward_profiled", "ft_miss_list_to_host", "ft_status_string")
+            "ft_moe_forward_profiled", "ft_miss_list_to_host", "ft_cache_plan", "ft_status_string")
 FT_PROF_STAGES = 4
 
 
@@ -68,6 +69,20 @@ class ft_host_miss_t(ctypes.Structure):
                                                "topk_w")]
 
 
+class ft_cache_state_t(ctypes.Structure):
+    _fields_ = [("slot_expert", ctypes.c_void_p), ("slot_stamp", ctypes.c_void_p)]
+
+
+class ft_cache_policy_t(ctypes.Structure):
+    _fields_ = [("b_pcie", ctypes.c_double), ("b_host", ctypes.c_double),
+                ("max_fill", ctypes.c_int32), ("step", ctypes.c_uint32)]
+
+
+class ft_fill_plan_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("fill_expert", "fill_slot", "evict_expert",
+                                               "cpu_expert", "counts")]
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -96,6 +111,10 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ft_miss_list_to_host.restype = ctypes.c_int
     lib.ft_miss_list_to_host.argtypes = [P(ft_moe_desc_t), P(ft_route_t), ctypes.c_int32,
                                          P(ft_host_miss_t), ctypes.c_void_p]
+    lib.ft_cache_plan.restype = ctypes.c_int
+    lib.ft_cache_plan.argtypes = [P(ft_moe_desc_t), P(ft_route_t), ctypes.c_int32, ctypes.c_void_p,
+                                  P(ft_cache_state_t), P(ft_cache_policy_t), P(ft_fill_plan_t),
+                                  ctypes.c_void_p]
     lib.ft_status_string.restype = ctypes.c_char_p
     lib.ft_status_string.argtypes = [ctypes.c_int]
     _lib = lib
@@ -226,6 +245,43 @@ def ft_miss_list_to_host(desc: dict, route: RouteBuffers, T: int, host: HostMiss
     st = load().ft_miss_list_to_host(ctypes.byref(make_desc(desc)), ctypes.byref(route.c()), int(T),
                                      ctypes.byref(host.c()), _stream(stream))
     _check(st, "ft_miss_list_to_host")
+
+
+class CacheState:
+    """Device tensors behind one ft_cache_state_t: slot -> expert (-1 empty) and the slot stamps
+    (uint32 in the ABI; held as int32 here, stamps stay below 2**31)."""
+
+    def __init__(self, slot_expert: torch.Tensor, slot_stamp: torch.Tensor):
+        self.slot_expert = slot_expert
+        self.slot_stamp = slot_stamp
+
+    def c(self) -> ft_cache_state_t:
+        return ft_cache_state_t(_ptr(self.slot_expert), _ptr(self.slot_stamp))
+
+
+class FillPlanBuffers:
+    """Device tensors behind one ft_fill_plan_t (max_fill fills, n_experts CPU entries)."""
+
+    def __init__(self, max_fill: int, n_experts: int, device="cuda"):
+        i32 = dict(dtype=torch.int32, device=device)
+        self.fill_expert = torch.empty(max_fill, **i32)
+        self.fill_slot = torch.empty(max_fill, **i32)
+        self.evict_expert = torch.empty(max_fill, **i32)
+        self.cpu_expert = torch.empty(max(n_experts, 1), **i32)
+        self.counts = torch.empty(4, **i32)
+
+    def c(self) -> ft_fill_plan_t:
+        return ft_fill_plan_t(*[_ptr(getattr(self, n)) for n, _ in ft_fill_plan_t._fields_])
+
+
+def ft_cache_plan(desc: dict, route: RouteBuffers, T: int, slot_table: torch.Tensor,
+                  state: CacheState, b_pcie: float, b_host: float, max_fill: int, step: int,
+                  plan: FillPlanBuffers, stream=None) -> None:
+    pol = ft_cache_policy_t(float(b_pcie), float(b_host), int(max_fill), int(step))
+    st = load().ft_cache_plan(ctypes.byref(make_desc(desc)), ctypes.byref(route.c()), int(T),
+                              _ptr(slot_table), ctypes.byref(state.c()), ctypes.byref(pol),
+                              ctypes.byref(plan.c()), _stream(stream))
+    _check(st, "ft_cache_plan")
 
 
 def banks_of(layer) -> dict:

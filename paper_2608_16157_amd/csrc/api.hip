@@ -180,6 +180,52 @@ ft_status_t ft_moe_forward_profiled(const ft_moe_desc_t *desc, const ft_banks_t 
                         stream, events);
 }
 
+ft_status_t ft_cache_plan(const ft_moe_desc_t *desc, const ft_route_t *route, int32_t T,
+                          int32_t *slot_table, const ft_cache_state_t *state,
+                          const ft_cache_policy_t *policy, const ft_fill_plan_t *plan,
+                          void *stream) {
+    using namespace ftmoe;
+    if (!desc || !route || !slot_table || !state || !policy || !plan) return FT_ERR_NULL;
+    if (!desc_ok(desc)) return FT_ERR_SHAPE;
+    if (T < 0) return FT_ERR_SHAPE;
+    if (!state->slot_expert || !state->slot_stamp) return FT_ERR_NULL;
+    if (!plan->fill_expert || !plan->fill_slot || !plan->evict_expert || !plan->cpu_expert ||
+        !plan->counts)
+        return FT_ERR_NULL;
+    if (!route->hit_off || !route->miss_off || !route->miss_pairs || !route->topk_slot ||
+        !route->counts)
+        return FT_ERR_NULL;
+    if (desc->n_slots > kPlanMaxSlots || policy->max_fill < 1 || policy->max_fill > kPlanMaxFill)
+        return FT_ERR_SHAPE;
+    if (!(policy->b_pcie > 0.0) || !(policy->b_host > 0.0) || policy->b_pcie > 1e300 ||
+        policy->b_host > 1e300)
+        return FT_ERR_SHAPE;
+    if (T == 0) return FT_OK;
+    PlanArgs a{};
+    a.E = desc->n_experts;
+    a.k = desc->top_k;
+    a.n_slots = desc->n_slots;
+    a.shared_slot = desc->shared_slot;
+    a.K = policy->max_fill;
+    a.b_pcie = policy->b_pcie;
+    a.b_host = policy->b_host;
+    a.step = policy->step;
+    a.hit_off = route->hit_off;
+    a.miss_off = route->miss_off;
+    a.miss_pairs = route->miss_pairs;
+    a.route_counts = route->counts;
+    a.topk_slot = route->topk_slot;
+    a.slot_table = slot_table;
+    a.slot_expert = state->slot_expert;
+    a.slot_stamp = state->slot_stamp;
+    a.fill_expert = plan->fill_expert;
+    a.fill_slot = plan->fill_slot;
+    a.evict_expert = plan->evict_expert;
+    a.cpu_expert = plan->cpu_expert;
+    a.counts = plan->counts;
+    return launch_cache_plan(a, static_cast<hipStream_t>(stream)) == hipSuccess ? FT_OK : FT_ERR_HIP;
+}
+
 ft_status_t ft_miss_list_to_host(const ft_moe_desc_t *desc, const ft_route_t *route, int32_t T,
                                  const ft_host_miss_t *host, void *stream) {
     if (!desc || !route || !host) return FT_ERR_NULL;

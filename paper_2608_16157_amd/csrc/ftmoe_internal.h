@@ -127,7 +127,23 @@ struct Prof {
     }
 };
 
+// Device-side cache control of one layer step (cache.hip).
+constexpr int kPlanMaxFill = 64;      // most LRU candidates (K) per step
+constexpr int kPlanMaxSlots = 4096;   // most cache slots the planner handles
+
+struct PlanArgs {
+    int E, k, n_slots, shared_slot, K;
+    double b_pcie, b_host;
+    uint32_t step;
+    const int32_t *hit_off, *miss_off, *miss_pairs, *route_counts;
+    int32_t *topk_slot;
+    int32_t *slot_table, *slot_expert;
+    uint32_t *slot_stamp;
+    int32_t *fill_expert, *fill_slot, *evict_expert, *cpu_expert, *counts;
+};
+
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
+hipError_t launch_cache_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof);
 hipError_t launch_gemm(const ExpertArgs &a, hipStream_t s, const Prof &prof);
 

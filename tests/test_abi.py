@@ -103,3 +103,29 @@ def test_miss_list_to_host_rejects_nulls():
     r = ftm.ft_route_t(*[FAKE] * 8)
     h = ftm.ft_host_miss_t(None, FAKE, FAKE, FAKE, FAKE)
     assert lib.ft_miss_list_to_host(ctypes.byref(d), ctypes.byref(r), 4, ctypes.byref(h), None) == ftm.FT_ERR_NULL
+
+
+def test_cache_plan_rejects_before_enqueue():
+    """Host-side validation of ft_cache_plan (fake device pointers: nothing may be enqueued)."""
+    lib = ftm.load()
+    d = ftm.make_desc(_desc())
+    r = ftm.ft_route_t(*[FAKE] * 8)
+    st = ftm.ft_cache_state_t(FAKE, FAKE)
+    pl = ftm.ft_fill_plan_t(*[FAKE] * 5)
+
+    def call(desc=d, route=r, T=4, table=FAKE, state=st, pol=None, plan=pl):
+        pol = pol or ftm.ft_cache_policy_t(1.0, 2.0, 4, 1)
+        return lib.ft_cache_plan(ctypes.byref(desc), ctypes.byref(route), T, table,
+                                 ctypes.byref(state), ctypes.byref(pol), ctypes.byref(plan), None)
+
+    assert call(table=None) == ftm.FT_ERR_NULL
+    assert call(state=ftm.ft_cache_state_t(None, FAKE)) == ftm.FT_ERR_NULL
+    assert call(plan=ftm.ft_fill_plan_t(FAKE, FAKE, FAKE, None, FAKE)) == ftm.FT_ERR_NULL
+    assert call(route=ftm.ft_route_t(*([FAKE] * 7 + [None]))) == ftm.FT_ERR_NULL
+    assert call(T=-1) == ftm.FT_ERR_SHAPE
+    assert call(pol=ftm.ft_cache_policy_t(1.0, 2.0, 0, 1)) == ftm.FT_ERR_SHAPE
+    assert call(pol=ftm.ft_cache_policy_t(1.0, 2.0, 65, 1)) == ftm.FT_ERR_SHAPE
+    assert call(pol=ftm.ft_cache_policy_t(0.0, 2.0, 4, 1)) == ftm.FT_ERR_SHAPE
+    assert call(pol=ftm.ft_cache_policy_t(1.0, float("nan"), 4, 1)) == ftm.FT_ERR_SHAPE
+    assert call(desc=ftm.make_desc(_desc(n_slots=5000))) == ftm.FT_ERR_SHAPE
+    assert call(T=0) == ftm.FT_OK          # nothing to plan, nothing enqueued
