@@ -22,7 +22,10 @@ constexpr int kFusedMaxLds = 64 * 1024;
 #endif
 constexpr int kGemmBM = FT_GEMM_BM;     // token rows per MFMA GEMM tile (prefill path)
 constexpr int kGemmBN = FT_GEMM_BN;     // weight rows per MFMA GEMM tile
-constexpr int kGemmMinTokens = 256;     // token count from which the MFMA GEMM path is used
+#ifndef FT_GEMM_MIN_TOKENS
+#define FT_GEMM_MIN_TOKENS 256
+#endif
+constexpr int kGemmMinTokens = FT_GEMM_MIN_TOKENS;   // token count from which the MFMA GEMM path is used
 
 // Routing outputs (the caller's ft_route_t, flattened).
 struct RouteOut {

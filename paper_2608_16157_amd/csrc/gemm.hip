@@ -290,7 +290,10 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
     // outstanding and the barrier has passed (every wave's share landed, and every wave is done
     // reading stage kt-1, whose slot WS is); past the end the DMA re-reads the last stage into
     // that free slot, which keeps the counts constant.
-    auto step = [&](int kt, auto rs, auto ws) {
+    // ML: the 32-row MFMA sub-tiles of the M tile that hold at least one real row; the others
+    // hold padding only, so their operand reads and MFMAs are skipped
+    auto step = [&](int kt, auto rs, auto ws, auto ml) {
+        constexpr int ML = decltype(ml)::value;
         wait_vmcnt<(NS - 2) * PER_STAGE>();
         wait_lgkmcnt0();
         stage_barrier();
@@ -317,7 +320,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
                 const int ca = kFp8 ? 4 * (ks / 2) + 2 * fq + (ks % 2) : 2 * ks + fq;
                 u32x4_t af[kMI], bf[kNJ];
 #pragma unroll
-                for (int i = 0; i < kMI; ++i) {
+                for (int i = 0; i < ML; ++i) {
                     const int ra = wm * kWaveRows + i * 32 + fn;
                     af[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, ca) << 4));
                 }
@@ -336,7 +339,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
                     }
                 }
 #pragma unroll
-                for (int i = 0; i < kMI; ++i)
+                for (int i = 0; i < ML; ++i)
 #pragma unroll
                     for (int j = 0; j < kNJ; ++j)
                         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -350,13 +353,21 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
     wait_vmcnt<0>();
     __syncthreads();
     static_for<0, NS - 1>([&](auto s) { issue(min(decltype(s)::value, nk - 1), stA(s), stB(s)); });
-    for (int kt = 0; kt < nk; kt += NS) {
-        // stage kt + S sits in slot S; its step refills slot (S + NS - 1) mod NS
-        static_for<0, NS>([&](auto s) {
-            constexpr int S = decltype(s)::value;
-            step(kt + S, s, ic<(S + NS - 1) % NS>{});
-        });
-    }
+    auto mainloop = [&](auto ml) {
+        for (int kt = 0; kt < nk; kt += NS) {
+            // stage kt + S sits in slot S; its step refills slot (S + NS - 1) mod NS
+            static_for<0, NS>([&](auto s) {
+                constexpr int S = decltype(s)::value;
+                step(kt + S, s, ic<(S + NS - 1) % NS>{}, ml);
+            });
+        }
+    };
+    static_assert(kMI == 4, "one main loop per live sub-tile count");
+    const int mlive = __builtin_amdgcn_readfirstlane(min(kMI, (min(len - m0, kBM) + 31) / 32));
+    if (mlive >= 4) mainloop(ic<4>{});
+    else if (mlive == 3) mainloop(ic<3>{});
+    else if (mlive == 2) mainloop(ic<2>{});
+    else mainloop(ic<1>{});
     wait_vmcnt<0>();   // the redundant tail stages
 
     // ---- epilogue: element e of a 32 x 32 tile in lane (fn, fq) is row 8 (e / 4) + 4 fq + e % 4,
