@@ -263,6 +263,75 @@ ft_status_t ft_cache_plan(const ft_moe_desc_t *desc, const ft_route_t *route, in
                           const ft_cache_policy_t *policy, const ft_fill_plan_t *plan,
                           void *stream);
 
+/*
+ * CPU branch of a layer step (Section 3.2: the missing experts the split leaves to the CPU
+ * execute from the host expert pool, concurrently with the GPU, and the two partial sums add up
+ * to the exact layer output; Section 4.1: a native worker pool with SIMD kernels and in-kernel
+ * dequantisation).  HOST pointers, caller-owned; runs synchronously on the calling thread plus
+ * n_threads - 1 workers (n_threads <= 0: one per hardware thread).
+ *   host_pool   the complete expert pool in host memory, indexed by EXPERT id, in the bank
+ *               layout of ft_banks_t: w13 [E][2I][H], w2 [E][H][I], s13/s2 per expert (fp8)
+ *   x           [T][H] x_dtype;  topk_ids, topk_w [T][k]: this step's routing
+ *   experts     n_list distinct expert ids to evaluate (e.g. ft_fill_plan_t.cpu_expert)
+ *   out         [T][H] float32, overwritten: out[t] = sum over (t, j) with topk_ids[t][j] in
+ *               experts of topk_w[t][j] * FFN_e(x_t), every product accumulated in float32 and
+ *               every element summed in a fixed order (independent of n_threads)
+ * Returns FT_ERR_DTYPE if the host CPU lacks AVX2 and FMA.
+ */
+ft_status_t ft_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_pool, const void *x,
+                           int32_t T, const int32_t *topk_ids, const float *topk_w,
+                           const int32_t *experts, int32_t n_list, float *out, int32_t n_threads);
+
+/*
+ * Cache fills of one step (Section 3.2: the q planned experts are copied into their slots over
+ * PCIe, then execute on the GPU and stay resident; Section 4.1: one fixed-shape launch driven by
+ * the device-resident fill list and its valid count, applied to every bank at once since all
+ * banks share one expert -> slot mapping).  Copies, for every fill i < plan->counts[0], expert
+ * plan->fill_expert[i]'s rows of every bank from host_pool into slot plan->fill_slot[i] of
+ * dev_banks, reading the pool directly over PCIe; the host does not need to know q.
+ *   host_pool  the complete expert pool, indexed by EXPERT id, in the ft_banks_t layout, in
+ *              pinned host memory (hipHostMalloc; pageable memory returns FT_ERR_SHAPE)
+ *   dev_banks  the device slot banks (as for ft_moe_forward), 16-byte aligned
+ *   plan       the device plan ft_cache_plan wrote; max_fill as passed there
+ */
+ft_status_t ft_cache_fill(const ft_moe_desc_t *desc, const ft_banks_t *host_pool,
+                          const ft_banks_t *dev_banks, const ft_fill_plan_t *plan, int32_t max_fill,
+                          void *stream);
+
+/*
+ * Host staging of ft_moe_step_hybrid: pinned host buffers, caller-owned, capacity for T tokens.
+ */
+typedef struct {
+    int32_t *plan_counts;   /* [4] */
+    int32_t *cpu_expert;    /* [E] */
+    int32_t *topk_ids;      /* [T*k] */
+    float *topk_w;          /* [T*k] */
+    void *x;                /* [T][H] x_dtype */
+    float *cpu_out;         /* [T][H] the CPU partial */
+} ft_hybrid_host_t;
+
+/*
+ * One complete MoE layer step over the GPU expert cache and the host (Section 3.2): route on the
+ * current slot table, plan the cache (ft_cache_plan), fill the planned slots (ft_cache_fill),
+ * evaluate hits and fills on the GPU (ft_moe_forward on the updated slot table) while the host
+ * evaluates the experts the plan leaves to the CPU (ft_cpu_experts), then add the CPU partial to
+ * the GPU's: `out` receives the exact layer output over all routed experts (+ shared expert).
+ * Blocks the calling thread until the CPU branch is done; the GPU part (fills, evaluation, the
+ * copy of the CPU partial and the merge) is enqueued on `stream`, so `out`, the cache state and
+ * host->cpu_out must not be used or reused before the stream is synchronised.
+ *   slot_table, state  updated in place as by ft_cache_plan
+ *   out          [T][H] float32 device: the full layer output
+ *   cpu_out_dev  [T][H] float32 device scratch (16-byte aligned) for the CPU partial
+ *   route, plan, ws    as for the calls above; route holds the second (post-fill) routing
+ */
+ft_status_t ft_moe_step_hybrid(const ft_moe_desc_t *desc, const ft_banks_t *dev_banks,
+                               const ft_banks_t *host_pool, const float *logits, int32_t *slot_table,
+                               const ft_cache_state_t *state, const ft_cache_policy_t *policy,
+                               const void *x, int32_t T, float *out, float *cpu_out_dev,
+                               const ft_route_t *route, const ft_fill_plan_t *plan,
+                               const ft_hybrid_host_t *host, void *ws, size_t ws_bytes,
+                               int32_t n_threads, void *stream);
+
 /* Static string for a status code. */
 const char *ft_status_string(ft_status_t status);
 

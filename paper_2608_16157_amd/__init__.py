@@ -11,6 +11,10 @@ of the C ABI declared in ``include/ftmoe.h``:
                             events, stream=None)
     ft_miss_list_to_host(desc, route, T, host, stream=None)
     ft_cache_plan(desc, route, T, slot_table, state, policy, plan, stream=None)
+    ft_cpu_experts(desc, host_pool, x, T, topk_ids, topk_w, experts, out, n_threads=0)
+    ft_cache_fill(desc, host_pool, dev_banks, plan, max_fill, stream=None)
+    ft_moe_step_hybrid(desc, dev_banks, host_pool, logits, slot_table, state, policy, x, T, out,
+                       cpu_out_dev, route, plan, host, ws, n_threads=0, stream=None)
     ft_status_string(status) -> str
 
 ``desc`` is a dict with the ft_moe_desc_t fields; ``route`` a RouteBuffers; ``banks`` a dict
@@ -35,7 +39,8 @@ FT_SLOT_MISS = -1
 FT_DEV_SLOT_RANGE, FT_DEV_SLOT_DUP, FT_DEV_SLOT_SHARED = 1, 2, 4
 
 EXPORTED = ("ft_moe_workspace_bytes", "ft_route_only", "ft_moe_forward",
-            "ft_moe_forward_profiled", "ft_miss_list_to_host", "ft_cache_plan", "ft_status_string")
+            "ft_moe_forward_profiled", "ft_miss_list_to_host", "ft_cache_plan", "ft_cpu_experts",
+            "ft_cache_fill", "ft_moe_step_hybrid", "ft_status_string")
 FT_PROF_STAGES = 4
 
 
@@ -83,6 +88,11 @@ class ft_fill_plan_t(ctypes.Structure):
                                                "cpu_expert", "counts")]
 
 
+class ft_hybrid_host_t(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in ("plan_counts", "cpu_expert", "topk_ids", "topk_w", "x",
+                                               "cpu_out")]
+
+
 _lib: Optional[ctypes.CDLL] = None
 
 
@@ -115,6 +125,19 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ft_cache_plan.argtypes = [P(ft_moe_desc_t), P(ft_route_t), ctypes.c_int32, ctypes.c_void_p,
                                   P(ft_cache_state_t), P(ft_cache_policy_t), P(ft_fill_plan_t),
                                   ctypes.c_void_p]
+    lib.ft_cpu_experts.restype = ctypes.c_int
+    lib.ft_cpu_experts.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), ctypes.c_void_p, ctypes.c_int32,
+                                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                   ctypes.c_void_p, ctypes.c_int32]
+    lib.ft_cache_fill.restype = ctypes.c_int
+    lib.ft_cache_fill.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), P(ft_banks_t), P(ft_fill_plan_t),
+                                  ctypes.c_int32, ctypes.c_void_p]
+    lib.ft_moe_step_hybrid.restype = ctypes.c_int
+    lib.ft_moe_step_hybrid.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), P(ft_banks_t), ctypes.c_void_p,
+                                       ctypes.c_void_p, P(ft_cache_state_t), P(ft_cache_policy_t),
+                                       ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                       P(ft_route_t), P(ft_fill_plan_t), P(ft_hybrid_host_t),
+                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_void_p]
     lib.ft_status_string.restype = ctypes.c_char_p
     lib.ft_status_string.argtypes = [ctypes.c_int]
     _lib = lib
@@ -282,6 +305,63 @@ def ft_cache_plan(desc: dict, route: RouteBuffers, T: int, slot_table: torch.Ten
                               _ptr(slot_table), ctypes.byref(state.c()), ctypes.byref(pol),
                               ctypes.byref(plan.c()), _stream(stream))
     _check(st, "ft_cache_plan")
+
+
+def ft_cpu_experts(desc: dict, host_pool: dict, x: torch.Tensor, T: int, topk_ids: torch.Tensor,
+                   topk_w: torch.Tensor, experts: torch.Tensor, out: torch.Tensor,
+                   n_threads: int = 0) -> None:
+    """CPU branch on host tensors: ``host_pool`` holds w13, w2 (s13, s2) indexed by expert id."""
+    b = ft_banks_t(_ptr(host_pool.get("w13")), _ptr(host_pool.get("w2")), _ptr(host_pool.get("s13")),
+                   _ptr(host_pool.get("s2")))
+    st = load().ft_cpu_experts(ctypes.byref(make_desc(desc)), ctypes.byref(b), _ptr(x), int(T),
+                               _ptr(topk_ids), _ptr(topk_w), _ptr(experts), int(experts.numel()),
+                               _ptr(out), int(n_threads))
+    _check(st, "ft_cpu_experts")
+
+
+def _banks(b: dict) -> ft_banks_t:
+    return ft_banks_t(_ptr(b.get("w13")), _ptr(b.get("w2")), _ptr(b.get("s13")), _ptr(b.get("s2")))
+
+
+def ft_cache_fill(desc: dict, host_pool: dict, dev_banks: dict, plan: FillPlanBuffers, max_fill: int,
+                  stream=None) -> None:
+    st = load().ft_cache_fill(ctypes.byref(make_desc(desc)), ctypes.byref(_banks(host_pool)),
+                              ctypes.byref(_banks(dev_banks)), ctypes.byref(plan.c()), int(max_fill),
+                              _stream(stream))
+    _check(st, "ft_cache_fill")
+
+
+class HybridHostBuffers:
+    """Pinned host staging behind one ft_hybrid_host_t, for T tokens."""
+
+    def __init__(self, T: int, top_k: int, n_experts: int, hidden: int, x_dtype=torch.bfloat16):
+        kw = dict(pin_memory=True)
+        pk = max(T * top_k, 1)
+        self.plan_counts = torch.empty(4, dtype=torch.int32, **kw)
+        self.cpu_expert = torch.empty(n_experts, dtype=torch.int32, **kw)
+        self.topk_ids = torch.empty(pk, dtype=torch.int32, **kw)
+        self.topk_w = torch.empty(pk, dtype=torch.float32, **kw)
+        self.x = torch.empty(max(T, 1), hidden, dtype=x_dtype, **kw)
+        self.cpu_out = torch.empty(max(T, 1), hidden, dtype=torch.float32, **kw)
+
+    def c(self) -> ft_hybrid_host_t:
+        return ft_hybrid_host_t(*[_ptr(getattr(self, n)) for n, _ in ft_hybrid_host_t._fields_])
+
+
+def ft_moe_step_hybrid(desc: dict, dev_banks: dict, host_pool: dict, logits: torch.Tensor,
+                       slot_table: torch.Tensor, state: CacheState, b_pcie: float, b_host: float,
+                       max_fill: int, step: int, x: torch.Tensor, T: int, out: torch.Tensor,
+                       cpu_out_dev: torch.Tensor, route: RouteBuffers, plan: FillPlanBuffers,
+                       host: HybridHostBuffers, ws: torch.Tensor, n_threads: int = 0,
+                       stream=None) -> None:
+    pol = ft_cache_policy_t(float(b_pcie), float(b_host), int(max_fill), int(step))
+    st = load().ft_moe_step_hybrid(ctypes.byref(make_desc(desc)), ctypes.byref(_banks(dev_banks)),
+                                   ctypes.byref(_banks(host_pool)), _ptr(logits), _ptr(slot_table),
+                                   ctypes.byref(state.c()), ctypes.byref(pol), _ptr(x), int(T),
+                                   _ptr(out), _ptr(cpu_out_dev), ctypes.byref(route.c()),
+                                   ctypes.byref(plan.c()), ctypes.byref(host.c()), _ptr(ws),
+                                   ws.numel(), int(n_threads), _stream(stream))
+    _check(st, "ft_moe_step_hybrid")
 
 
 def banks_of(layer) -> dict:

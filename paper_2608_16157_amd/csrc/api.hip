@@ -1,6 +1,10 @@
 // C ABI entry points of libftmoe: host-side validation, workspace carving, kernel enqueue.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+#include <thread>
+#include <vector>
+
 #include "ftmoe_internal.h"
 
 using namespace ftmoe;
@@ -224,6 +228,148 @@ ft_status_t ft_cache_plan(const ft_moe_desc_t *desc, const ft_route_t *route, in
     a.cpu_expert = plan->cpu_expert;
     a.counts = plan->counts;
     return launch_cache_plan(a, static_cast<hipStream_t>(stream)) == hipSuccess ? FT_OK : FT_ERR_HIP;
+}
+
+ft_status_t ft_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_pool, const void *x,
+                           int32_t T, const int32_t *topk_ids, const float *topk_w,
+                           const int32_t *experts, int32_t n_list, float *out, int32_t n_threads) {
+    using namespace ftmoe;
+    if (!desc || !host_pool) return FT_ERR_NULL;
+    if (!desc_ok(desc)) return FT_ERR_SHAPE;
+    if (ft_status_t st = dtype_status(desc); st != FT_OK) return st;
+    if (T < 0 || n_list < 0 || n_list > desc->n_experts) return FT_ERR_SHAPE;
+    if (T == 0) return FT_OK;
+    if (!x || !topk_ids || !topk_w || !out || (n_list > 0 && !experts)) return FT_ERR_NULL;
+    if (n_list > 0 && (!host_pool->w13 || !host_pool->w2)) return FT_ERR_NULL;
+    if (desc->w_dtype == FT_DT_FP8E4M3FN_B128 && n_list > 0 && (!host_pool->s13 || !host_pool->s2))
+        return FT_ERR_NULL;
+    std::vector<char> seen(desc->n_experts, 0);
+    for (int i = 0; i < n_list; ++i) {
+        const int e = experts[i];
+        if (e < 0 || e >= desc->n_experts || seen[e]) return FT_ERR_SHAPE;
+        seen[e] = 1;
+    }
+    if (!__builtin_cpu_supports("avx2") || !__builtin_cpu_supports("fma")) return FT_ERR_DTYPE;
+    CpuExpertArgs a{};
+    a.E = desc->n_experts;
+    a.H = desc->hidden;
+    a.I = desc->inter;
+    a.k = desc->top_k;
+    a.T = T;
+    a.w_dtype = desc->w_dtype;
+    a.x_dtype = desc->x_dtype;
+    a.n_list = n_list;
+    a.n_threads = n_threads > 0 ? n_threads : std::max(1u, std::thread::hardware_concurrency());
+    a.w13 = host_pool->w13;
+    a.w2 = host_pool->w2;
+    a.s13 = host_pool->s13;
+    a.s2 = host_pool->s2;
+    a.x = x;
+    a.topk_ids = topk_ids;
+    a.topk_w = topk_w;
+    a.list = experts;
+    a.out = out;
+    cpu_experts(a);
+    return FT_OK;
+}
+
+ft_status_t ft_cache_fill(const ft_moe_desc_t *desc, const ft_banks_t *host_pool,
+                          const ft_banks_t *dev_banks, const ft_fill_plan_t *plan, int32_t max_fill,
+                          void *stream) {
+    using namespace ftmoe;
+    if (!desc || !host_pool || !dev_banks || !plan) return FT_ERR_NULL;
+    if (!desc_ok(desc)) return FT_ERR_SHAPE;
+    if (ft_status_t st = dtype_status(desc); st != FT_OK) return st;
+    if (max_fill < 1 || max_fill > kPlanMaxFill) return FT_ERR_SHAPE;
+    if (!plan->counts || !plan->fill_expert || !plan->fill_slot) return FT_ERR_NULL;
+    const bool fp8 = desc->w_dtype == FT_DT_FP8E4M3FN_B128;
+    const void *hp[4] = {host_pool->w13, host_pool->w2, fp8 ? host_pool->s13 : nullptr,
+                         fp8 ? host_pool->s2 : nullptr};
+    void *dp[4] = {const_cast<void *>(dev_banks->w13), const_cast<void *>(dev_banks->w2),
+                   fp8 ? const_cast<float *>(dev_banks->s13) : nullptr,
+                   fp8 ? const_cast<float *>(dev_banks->s2) : nullptr};
+    const size_t H = desc->hidden, I = desc->inter;
+    const size_t wb = desc->w_dtype == FT_DT_F32 ? 4 : (desc->w_dtype == FT_DT_BF16 ? 2 : 1);
+    const size_t rows[4] = {2 * I * H * wb, H * I * wb, fp8 ? (2 * I / 128) * (H / 128) * 4 : 0,
+                            fp8 ? (H / 128) * (I / 128) * 4 : 0};
+    FillArgs a{};
+    a.E = desc->n_experts;
+    a.n_slots = desc->n_slots;
+    a.plan_counts = plan->counts;
+    a.fill_expert = plan->fill_expert;
+    a.fill_slot = plan->fill_slot;
+    for (int b = 0; b < 4; ++b) {
+        a.row_bytes[b] = rows[b];
+        if (!rows[b]) continue;
+        if (!hp[b] || !dp[b]) return FT_ERR_NULL;
+        if (reinterpret_cast<uintptr_t>(hp[b]) % 16 || reinterpret_cast<uintptr_t>(dp[b]) % 16)
+            return FT_ERR_SHAPE;
+        // the pool must be pinned host memory the GPU can read (pageable memory is rejected)
+        void *mapped = nullptr;
+        if (hipHostGetDevicePointer(&mapped, const_cast<void *>(hp[b]), 0) != hipSuccess || !mapped)
+            return FT_ERR_SHAPE;
+        a.host[b] = static_cast<const uint8_t *>(mapped);
+        a.dev[b] = static_cast<uint8_t *>(dp[b]);
+    }
+    if (desc->n_slots == 0) return FT_OK;
+    return launch_cache_fill(a, max_fill, static_cast<hipStream_t>(stream)) == hipSuccess ? FT_OK : FT_ERR_HIP;
+}
+
+ft_status_t ft_moe_step_hybrid(const ft_moe_desc_t *desc, const ft_banks_t *dev_banks,
+                               const ft_banks_t *host_pool, const float *logits, int32_t *slot_table,
+                               const ft_cache_state_t *state, const ft_cache_policy_t *policy,
+                               const void *x, int32_t T, float *out, float *cpu_out_dev,
+                               const ft_route_t *route, const ft_fill_plan_t *plan,
+                               const ft_hybrid_host_t *host, void *ws, size_t ws_bytes,
+                               int32_t n_threads, void *stream) {
+    using namespace ftmoe;
+    if (!desc || !dev_banks || !host_pool || !state || !policy || !route || !plan || !host)
+        return FT_ERR_NULL;
+    if (T == 0) return desc_ok(desc) ? FT_OK : FT_ERR_SHAPE;
+    if (!out || !cpu_out_dev || !x || !host->plan_counts || !host->cpu_expert || !host->topk_ids ||
+        !host->topk_w || !host->x || !host->cpu_out)
+        return FT_ERR_NULL;
+    if (reinterpret_cast<uintptr_t>(cpu_out_dev) % 16) return FT_ERR_SHAPE;
+    const hipStream_t s = static_cast<hipStream_t>(stream);
+    // 1. routing and the cache plan on the current slot table
+    if (ft_status_t st = ft_route_only(desc, logits, slot_table, T, route, ws, ws_bytes, stream); st != FT_OK)
+        return st;
+    if (ft_status_t st = ft_cache_plan(desc, route, T, slot_table, state, policy, plan, stream); st != FT_OK)
+        return st;
+    // 2. what the CPU branch needs goes to the host, at full fixed capacity
+    const size_t pk = static_cast<size_t>(T) * desc->top_k;
+    const size_t xb = static_cast<size_t>(T) * desc->hidden * (desc->x_dtype == FT_DT_F32 ? 4 : 2);
+    const hipMemcpyKind d2h = hipMemcpyDeviceToHost;
+    if (hipMemcpyAsync(host->plan_counts, plan->counts, 4 * sizeof(int32_t), d2h, s) != hipSuccess ||
+        hipMemcpyAsync(host->cpu_expert, plan->cpu_expert, desc->n_experts * sizeof(int32_t), d2h, s) != hipSuccess ||
+        hipMemcpyAsync(host->topk_ids, route->topk_ids, pk * sizeof(int32_t), d2h, s) != hipSuccess ||
+        hipMemcpyAsync(host->topk_w, route->topk_w, pk * sizeof(float), d2h, s) != hipSuccess ||
+        hipMemcpyAsync(host->x, x, xb, d2h, s) != hipSuccess)
+        return FT_ERR_HIP;
+    hipEvent_t staged;
+    if (hipEventCreateWithFlags(&staged, hipEventDisableTiming) != hipSuccess) return FT_ERR_HIP;
+    if (hipEventRecord(staged, s) != hipSuccess) {
+        (void)hipEventDestroy(staged);
+        return FT_ERR_HIP;
+    }
+    // 3. the GPU fills the planned slots and evaluates hits and fills (the second routing sees
+    //    the updated slot table), while the host runs the CPU branch
+    ft_status_t st = ft_cache_fill(desc, host_pool, dev_banks, plan, policy->max_fill, stream);
+    if (st == FT_OK)
+        st = ft_moe_forward(desc, dev_banks, logits, slot_table, x, T, out, route, ws, ws_bytes, stream);
+    if (hipEventSynchronize(staged) != hipSuccess) st = st == FT_OK ? FT_ERR_HIP : st;
+    (void)hipEventDestroy(staged);
+    if (st != FT_OK) return st;
+    const int n_cpu = host->plan_counts[1];
+    if (n_cpu <= 0) return FT_OK;
+    st = ft_cpu_experts(desc, host_pool, host->x, T, host->topk_ids, host->topk_w, host->cpu_expert,
+                        n_cpu, host->cpu_out, n_threads);
+    if (st != FT_OK) return st;
+    // 4. exact merge: out += CPU partial
+    const size_t n = static_cast<size_t>(T) * desc->hidden;
+    if (hipMemcpyAsync(cpu_out_dev, host->cpu_out, n * sizeof(float), hipMemcpyHostToDevice, s) != hipSuccess)
+        return FT_ERR_HIP;
+    return launch_add_partial(out, cpu_out_dev, n, s) == hipSuccess ? FT_OK : FT_ERR_HIP;
 }
 
 ft_status_t ft_miss_list_to_host(const ft_moe_desc_t *desc, const ft_route_t *route, int32_t T,

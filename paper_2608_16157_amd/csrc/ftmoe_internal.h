@@ -145,6 +145,35 @@ struct PlanArgs {
     int32_t *fill_expert, *fill_slot, *evict_expert, *cpu_expert, *counts;
 };
 
+// Cache fills and the exact merge (fill.hip).
+constexpr size_t kFillChunk = 64 * 1024;   // bytes of one bank row a fill block copies
+struct FillArgs {
+    int E, n_slots;
+    const int32_t *plan_counts, *fill_expert, *fill_slot;
+    const uint8_t *host[4];   // pinned host pool (device-visible addresses): w13, w2, s13, s2
+    uint8_t *dev[4];          // device banks
+    size_t row_bytes[4];      // bytes of one expert's row in each bank (0 = bank absent)
+};
+hipError_t launch_cache_fill(const FillArgs &a, int max_fill, hipStream_t s);
+hipError_t launch_add_partial(float *out, const float *other, size_t n, hipStream_t s);
+
+// CPU branch of a layer step (host_experts.cpp).
+struct CpuBank {
+    const void *w;       // one expert's matrix, row-major
+    const float *s;      // its fp8 block scales, or null
+};
+struct CpuExpertArgs {
+    int E, H, I, k, T, w_dtype, x_dtype, n_list, n_threads;
+    const void *w13, *w2;            // host expert pool, [E][2I][H] and [E][H][I]
+    const float *s13, *s2;           // fp8 block scales per expert, or null
+    const void *x;                   // [T][H]
+    const int32_t *topk_ids;         // [T][k]
+    const float *topk_w;             // [T][k]
+    const int32_t *list;             // experts to evaluate (distinct ids)
+    float *out;                      // [T][H], overwritten
+};
+void cpu_experts(const CpuExpertArgs &a);
+
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_cache_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof);

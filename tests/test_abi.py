@@ -129,3 +129,34 @@ def test_cache_plan_rejects_before_enqueue():
     assert call(pol=ftm.ft_cache_policy_t(1.0, float("nan"), 4, 1)) == ftm.FT_ERR_SHAPE
     assert call(desc=ftm.make_desc(_desc(n_slots=5000))) == ftm.FT_ERR_SHAPE
     assert call(T=0) == ftm.FT_OK          # nothing to plan, nothing enqueued
+
+
+def test_fill_and_hybrid_reject_before_enqueue():
+    lib = ftm.load()
+    d = ftm.make_desc(_desc(w_dtype=1, x_dtype=1, hidden=128, inter=128))
+    b = ftm.ft_banks_t(FAKE, FAKE, None, None)
+    pl = ftm.ft_fill_plan_t(*[FAKE] * 5)
+    assert lib.ft_cache_fill(ctypes.byref(d), None, ctypes.byref(b), ctypes.byref(pl), 4, None) == ftm.FT_ERR_NULL
+    assert lib.ft_cache_fill(ctypes.byref(d), ctypes.byref(b), ctypes.byref(b), ctypes.byref(pl), 0, None) == ftm.FT_ERR_SHAPE
+    assert lib.ft_cache_fill(ctypes.byref(d), ctypes.byref(b), ctypes.byref(b), ctypes.byref(pl), 65, None) == ftm.FT_ERR_SHAPE
+    nb = ftm.ft_banks_t(None, FAKE, None, None)
+    assert lib.ft_cache_fill(ctypes.byref(d), ctypes.byref(nb), ctypes.byref(b), ctypes.byref(pl), 4, None) == ftm.FT_ERR_NULL
+    st = ftm.ft_cache_state_t(FAKE, FAKE)
+    pol = ftm.ft_cache_policy_t(1.0, 2.0, 4, 1)
+    r = ftm.ft_route_t(*[FAKE] * 8)
+    h = ftm.ft_hybrid_host_t(*[FAKE] * 6)
+    args = [ctypes.byref(d), ctypes.byref(b), ctypes.byref(b), FAKE, FAKE, ctypes.byref(st),
+            ctypes.byref(pol), FAKE, 4, FAKE, FAKE, ctypes.byref(r), ctypes.byref(pl), ctypes.byref(h),
+            FAKE, 1 << 20, 0, None]
+    a = list(args)
+    a[13] = ctypes.byref(ftm.ft_hybrid_host_t(FAKE, FAKE, FAKE, FAKE, FAKE, None))
+    assert lib.ft_moe_step_hybrid(*a) == ftm.FT_ERR_NULL
+    a = list(args)
+    a[10] = None
+    assert lib.ft_moe_step_hybrid(*a) == ftm.FT_ERR_NULL
+    a = list(args)
+    a[10] = FAKE + 4           # misaligned CPU-partial scratch
+    assert lib.ft_moe_step_hybrid(*a) == ftm.FT_ERR_SHAPE
+    a = list(args)
+    a[8] = 0
+    assert lib.ft_moe_step_hybrid(*a) == ftm.FT_OK

@@ -1,0 +1,170 @@
+"""Cache fills and the complete hybrid layer step (GPU hits and fills + CPU branch + exact merge)
+against the oracle.
+
+Every step routes on the current cache, plans, fills the planned slots from the pinned host pool,
+evaluates hits and fills on the GPU and the rest on the CPU, and merges: the output must equal the
+oracle's output of the full MoE layer (every expert), the cache state must equal the oracle's
+plan bit for bit, and every occupied slot must hold its expert's weights bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_16157_amd as ftm
+import workloads
+from tests._util import to_np_bits
+
+pytestmark = pytest.mark.gpu
+
+TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2}
+
+
+def _say(msg):
+    print(f"[gpu-hybrid] {msg}", flush=True)
+
+
+class Setup:
+    """Host pool (pinned, indexed by expert), device slot banks, cache state and buffers."""
+
+    def __init__(self, seed, wdt, gating, E, R, k, T, H, I, shared, K):
+        lay = workloads.random_layer(seed, hidden=H, inter=I, n_experts=E, top_k=k, tokens=T,
+                                     gating=gating, w_dtype=wdt, n_resident=E, shared=shared)
+        st = lay.slot_table.long()
+        fp8 = wdt == workloads.DT_FP8
+        self.pool = {"w13": lay.w13[st].contiguous().pin_memory(),
+                     "w2": lay.w2[st].contiguous().pin_memory(),
+                     "s13": lay.s13[st].contiguous().pin_memory() if fp8 else None,
+                     "s2": lay.s2[st].contiguous().pin_memory() if fp8 else None}
+        self.E, self.R, self.k, self.T, self.H, self.I, self.K = E, R, k, T, H, I, K
+        self.wdt, self.shared = wdt, shared
+        n_slots = R + (1 if shared else 0)
+        self.desc = dict(hidden=H, inter=I, n_experts=E, top_k=k, gating=gating, w_dtype=wdt,
+                         x_dtype=lay.x_dtype, n_slots=n_slots, shared_slot=R if shared else -1)
+        # device banks: garbage in every routed slot, the shared expert in its slot
+        self.dev = {}
+        for name in ("w13", "w2", "s13", "s2"):
+            src = getattr(lay, name)
+            if src is None:
+                self.dev[name] = None
+                continue
+            d = torch.empty((n_slots,) + tuple(src.shape[1:]), dtype=src.dtype, device="cuda")
+            d.view(torch.uint8).fill_(0x5A) if d.dtype != torch.float32 else d.fill_(7.0)
+            if shared:
+                d[R] = src[lay.shared_slot].cuda()
+            self.dev[name] = d
+        self.shared_rows = {n: (getattr(lay, n)[lay.shared_slot] if shared and getattr(lay, n) is not None
+                                else None) for n in ("w13", "w2", "s13", "s2")}
+        self.x_dtype = lay.x.dtype
+        self.table = torch.full((E,), -1, dtype=torch.int32, device="cuda")
+        self.state = ftm.CacheState(torch.full((n_slots,), -1, dtype=torch.int32, device="cuda"),
+                                    torch.zeros(n_slots, dtype=torch.int32, device="cuda"))
+        self.route = ftm.RouteBuffers(T, k, E)
+        self.plan = ftm.FillPlanBuffers(K, E)
+        self.ws = ftm.alloc_workspace(self.desc, T)
+        self.host = ftm.HybridHostBuffers(T, k, E, H, self.x_dtype)
+        self.out = torch.empty(T, H, dtype=torch.float32, device="cuda")
+        self.cpu_out_dev = torch.empty(T, H, dtype=torch.float32, device="cuda")
+
+    def oracle_full(self, logits, x):
+        """Output of the full layer: every routed expert resident (bank row = expert id), plus the
+        shared expert in row E."""
+        banks = {}
+        for n in ("w13", "w2", "s13", "s2"):
+            if self.pool[n] is None:
+                continue
+            rows = self.pool[n]
+            if self.shared:
+                rows = torch.cat([rows, self.shared_rows[n][None]], 0)
+            banks[n] = to_np_bits(rows)
+        d = dict(self.desc, n_slots=self.E + (1 if self.shared else 0),
+                 shared_slot=self.E if self.shared else -1)
+        ref, _ = oracle.moe_partial(d, banks, logits, np.arange(self.E, dtype=np.int32), to_np_bits(x))
+        return ref
+
+    def check_banks(self, sexp):
+        for s, e in enumerate(sexp.tolist()):
+            if e < 0 or (self.shared and s == self.R):
+                continue
+            for n in ("w13", "w2", "s13", "s2"):
+                if self.pool[n] is None:
+                    continue
+                got = self.dev[n][s].cpu()
+                want = self.pool[n][e]
+                assert torch.equal(got.view(torch.uint8), want.view(torch.uint8)), (n, s, e)
+
+
+def _logits(rng, T, E, rank):
+    return (rng.standard_normal((T, E)) - 1.1 * np.log(rank)[None, :]).astype(np.float32)
+
+
+CASES = [
+    # seed, w_dtype, gating, E, R (routed slots), k, T, H, I, shared, K, (B_P, B_H)
+    (0, workloads.DT_BF16, 0, 16, 5, 4, 3, 256, 256, False, 4, (11.8, 47.5)),
+    (1, workloads.DT_FP8, 1, 20, 6, 4, 2, 256, 384, True, 3, (52.7, 77.3)),
+    (2, workloads.DT_F32, 0, 8, 3, 2, 4, 128, 128, False, 2, (6.0, 5.0)),
+    (3, workloads.DT_BF16, 1, 24, 8, 6, 5, 384, 256, True, 8, (25.1, 63.2)),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[str(c[0]) for c in CASES])
+def test_hybrid_steps_match_full_layer(case):
+    seed, wdt, gating, E, R, k, T, H, I, shared, K, (bp, bh) = case
+    su = Setup(seed, wdt, gating, E, R, k, T, H, I, shared, K)
+    rng = np.random.default_rng(seed)
+    rank = rng.permutation(E) + 1
+    table = np.full(E, -1, np.int32)
+    sexp = np.full(su.desc["n_slots"], -1, np.int32)
+    stamp = np.zeros(su.desc["n_slots"], np.uint32)
+    n_cpu_steps = n_fill_steps = 0
+    for step in range(1, 11):
+        if step == 6:
+            rank = rng.permutation(E) + 1
+        logits = _logits(rng, T, E, rank)
+        x = torch.randn(T, H, generator=torch.Generator().manual_seed(seed * 100 + step)).to(su.x_dtype)
+        _say(f"case {seed} step {step}")
+        ftm.ft_moe_step_hybrid(su.desc, su.dev, su.pool, torch.tensor(logits, device="cuda"),
+                               su.table, su.state, bp, bh, K, step, x.cuda(), T, su.out,
+                               su.cpu_out_dev, su.route, su.plan, su.host, su.ws, n_threads=3)
+        torch.cuda.synchronize()
+        # cache state against the oracle's plan on the same routing
+        r = oracle.route(su.desc, logits, table)
+        plan = oracle.cache_plan(su.desc, r, table, sexp, stamp, bp, bh, K, step)
+        table, sexp, stamp = plan["slot_table"], plan["slot_expert"], plan["slot_stamp"]
+        assert np.array_equal(su.table.cpu().numpy(), table)
+        assert np.array_equal(su.state.slot_expert.cpu().numpy(), sexp)
+        assert np.array_equal(su.state.slot_stamp.cpu().numpy().astype(np.uint32), stamp)
+        assert su.plan.counts.cpu().tolist() == [plan["q"], plan["m"] - plan["q"], plan["m"], 0]
+        n_cpu_steps += plan["m"] > plan["q"]
+        n_fill_steps += plan["q"] > 0
+        su.check_banks(sexp)
+        # the merged output is the full layer's
+        ref = su.oracle_full(logits, x)
+        assert oracle.max_rel_err(su.out.cpu().numpy(), ref) <= TOL[wdt], step
+    assert n_fill_steps > 0
+    if bh > bp:
+        assert n_cpu_steps > 0
+
+
+def test_cache_fill_alone():
+    """ft_route_only + ft_cache_plan + ft_cache_fill: filled slots hold their experts, other slots
+    keep their bytes."""
+    su = Setup(7, workloads.DT_BF16, 0, 12, 6, 3, 4, 256, 128, False, 6)
+    rng = np.random.default_rng(7)
+    logits = torch.tensor(rng.standard_normal((4, 12)).astype(np.float32), device="cuda")
+    before = {n: su.dev[n].clone() for n in ("w13", "w2")}
+    ftm.ft_route_only(su.desc, logits, su.table, 4, su.route, su.ws)
+    ftm.ft_cache_plan(su.desc, su.route, 4, su.table, su.state, 52.7, 77.3, 6, 1, su.plan)
+    ftm.ft_cache_fill(su.desc, su.pool, su.dev, su.plan, 6)
+    torch.cuda.synchronize()
+    q = int(su.plan.counts[0])
+    assert q > 0
+    fe = su.plan.fill_expert.cpu().tolist()[:q]
+    fs = su.plan.fill_slot.cpu().tolist()[:q]
+    for n in ("w13", "w2"):
+        for s in range(su.desc["n_slots"]):
+            got = su.dev[n][s].cpu()
+            if s in fs:
+                assert torch.equal(got, su.pool[n][fe[fs.index(s)]])
+            else:
+                assert torch.equal(got, before[n][s].cpu())
