@@ -160,6 +160,141 @@ def ingest_traffic(key, kernel_match, fetch_csv, write_csv, cal_fetch_csv, cal_w
     print(json.dumps({key: data[key]}), flush=True)
 
 
+def _pool_tensors(cfg, E, device):
+    """Random expert weights of one layer shape, E experts, in the bank layout."""
+    import torch
+    H, I = cfg.hidden, cfg.inter
+    g = torch.Generator(device=device)
+    g.manual_seed(12345)
+    out = {}
+    if cfg.w_dtype == 2:
+        import workloads
+        w13 = torch.empty(E, 2 * I, H, dtype=torch.uint8, device=device)
+        w2 = torch.empty(E, H, I, dtype=torch.uint8, device=device)
+        s13 = torch.empty(E, 2 * I // 128, H // 128, dtype=torch.float32, device=device)
+        s2 = torch.empty(E, H // 128, I // 128, dtype=torch.float32, device=device)
+        for e in range(E):
+            w13[e], s13[e] = workloads.quantize_fp8_blocks(
+                torch.randn(2 * I, H, generator=g, device=device) * 0.02)
+            w2[e], s2[e] = workloads.quantize_fp8_blocks(torch.randn(H, I, generator=g, device=device) * 0.02)
+        out.update(w13=w13, w2=w2, s13=s13, s2=s2)
+    else:
+        dt = torch.bfloat16 if cfg.w_dtype == 1 else torch.float32
+        out["w13"] = (torch.randn(E, 2 * I, H, generator=g, device=device) * 0.02).to(dt)
+        out["w2"] = (torch.randn(E, H, I, generator=g, device=device) * 0.02).to(dt)
+        out["s13"] = out["s2"] = None
+    return out
+
+
+def measure_bandwidths(cfg_name, n_fill, reps):
+    """B_P: the fill kernel copying n_fill complete experts from the pinned host pool into
+    device slots; B_H: the CPU branch streaming n_fill experts' weights for one token."""
+    import torch
+    import paper_2608_16157_amd as ftm
+    import workloads
+    cfg = workloads.CONFIGS[cfg_name]
+    E = n_fill
+    dev = _pool_tensors(cfg, E, "cuda")
+    pool = {n: (t.cpu().pin_memory() if t is not None else None) for n, t in dev.items()}
+    for t in dev.values():
+        if t is not None:
+            t.zero_()
+    S, _ = expert_bytes(type("L", (), {"hidden": cfg.hidden, "inter": cfg.inter, "w_dtype": cfg.w_dtype})())
+    desc = dict(hidden=cfg.hidden, inter=cfg.inter, n_experts=E, top_k=min(cfg.top_k, E),
+                gating=cfg.gating, w_dtype=cfg.w_dtype, x_dtype=cfg.x_dtype, n_slots=E, shared_slot=-1)
+    plan = ftm.FillPlanBuffers(n_fill, E)
+    plan.fill_expert.copy_(torch.arange(n_fill, dtype=torch.int32))
+    plan.fill_slot.copy_(torch.arange(n_fill, dtype=torch.int32))
+    plan.counts.copy_(torch.tensor([n_fill, 0, n_fill, 0], dtype=torch.int32))
+    ftm.ft_cache_fill(desc, pool, dev, plan, n_fill)
+    torch.cuda.synchronize()
+    ok = all(torch.equal(dev[n].cpu(), pool[n]) for n in dev if dev[n] is not None)
+    hip = HipEvents()
+    stream = torch.cuda.current_stream().cuda_stream
+    a, b = hip.create(), hip.create()
+    hip.hip.hipEventRecord(a, stream)
+    for _ in range(reps):
+        ftm.ft_cache_fill(desc, pool, dev, plan, n_fill)
+    hip.hip.hipEventRecord(b, stream)
+    torch.cuda.synchronize()
+    t_fill = hip.elapsed_ms(a, b) / 1e3 / reps
+    # CPU branch: one token routed to all n_fill experts
+    k = n_fill
+    desc_c = dict(desc, top_k=k)
+    x = (torch.randn(1, cfg.hidden) * 1.0).to(torch.bfloat16 if cfg.x_dtype == 1 else torch.float32)
+    ids = torch.arange(k, dtype=torch.int32).reshape(1, k)
+    w = torch.full((1, k), 1.0 / k)
+    out = torch.empty(1, cfg.hidden)
+    lst = torch.arange(k, dtype=torch.int32)
+    ftm.ft_cpu_experts(desc_c, pool, x, 1, ids, w, lst, out)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        ftm.ft_cpu_experts(desc_c, pool, x, 1, ids, w, lst, out)
+    t_cpu = (time.perf_counter() - t0) / reps
+    print(json.dumps({
+        "measurement": "expert transfer (B_P) and host expert-processing (B_H) bandwidths",
+        "workload": f"{cfg_name} experts ({S} bytes each), {n_fill} experts per call",
+        "b_pcie_gbs": round(n_fill * S / t_fill / 1e9, 2), "fill_ms": round(t_fill * 1e3, 3),
+        "fill_copy_exact": ok,
+        "b_host_gbs": round(n_fill * S / t_cpu / 1e9, 2), "cpu_ms": round(t_cpu * 1e3, 3),
+        "cpu_threads": os.cpu_count(),
+    }), flush=True)
+
+
+def hybrid_decode(cfg_name, T, steps, warmup, n_slots, b_pcie, b_host, max_fill):
+    """Complete decode layer steps over the GPU expert cache and the host: route, plan, fill,
+    GPU evaluation of hits and fills, CPU branch for the rest, exact merge (wall clock per step,
+    the CPU branch included)."""
+    import numpy as np
+    import torch
+    import paper_2608_16157_amd as ftm
+    import workloads
+    cfg = workloads.CONFIGS[cfg_name]
+    E, H = cfg.n_experts, cfg.hidden
+    dev_pool = _pool_tensors(cfg, E, "cuda")
+    pool = {n: (t.cpu().pin_memory() if t is not None else None) for n, t in dev_pool.items()}
+    dev = {n: (torch.zeros((n_slots,) + tuple(t.shape[1:]), dtype=t.dtype, device="cuda")
+               if t is not None else None) for n, t in dev_pool.items()}
+    del dev_pool
+    desc = dict(hidden=H, inter=cfg.inter, n_experts=E, top_k=cfg.top_k, gating=cfg.gating,
+                w_dtype=cfg.w_dtype, x_dtype=cfg.x_dtype, n_slots=n_slots, shared_slot=-1)
+    table = torch.full((E,), -1, dtype=torch.int32, device="cuda")
+    state = ftm.CacheState(torch.full((n_slots,), -1, dtype=torch.int32, device="cuda"),
+                           torch.zeros(n_slots, dtype=torch.int32, device="cuda"))
+    route = ftm.RouteBuffers(T, cfg.top_k, E)
+    plan = ftm.FillPlanBuffers(max_fill, E)
+    ws = ftm.alloc_workspace(desc, T)
+    host = ftm.HybridHostBuffers(T, cfg.top_k, E, H, torch.bfloat16)
+    out = torch.empty(T, H, dtype=torch.float32, device="cuda")
+    cpu_dev = torch.empty(T, H, dtype=torch.float32, device="cuda")
+    g = torch.Generator(device="cuda")
+    g.manual_seed(77)
+    rank = torch.randperm(E, generator=g, device="cuda").float() + 1
+    bias = -cfg.zipf_s * torch.log(rank)
+    n = warmup + steps
+    logits = [torch.randn(T, E, generator=g, device="cuda") + bias[None, :] for _ in range(n)]
+    xs = [torch.randn(T, H, generator=g, device="cuda").to(torch.bfloat16) for _ in range(n)]
+    fills = cpus = misses = 0
+    for i in range(n):
+        if i == warmup:
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+        ftm.ft_moe_step_hybrid(desc, dev, pool, logits[i], table, state, b_pcie, b_host, max_fill,
+                               i + 1, xs[i], T, out, cpu_dev, route, plan, host, ws)
+        if i >= warmup:
+            c = host.plan_counts.tolist()
+            fills, cpus, misses = fills + c[0], cpus + c[1], misses + c[2]
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    print(json.dumps({
+        "measurement": "hybrid decode layer step (GPU expert cache + fills + CPU branch + merge)",
+        "workload": f"{cfg_name} shapes, T={T}, {n_slots} of {E} experts cacheable, Zipf "
+                    f"{cfg.zipf_s} routing, B_P={b_pcie} B_H={b_host} GB/s, K={max_fill}",
+        "tokens_per_s": round(T / dt, 1), "ms_per_step": round(dt * 1e3, 4),
+        "missing_experts_per_step": round(misses / steps, 2), "fills_per_step": round(fills / steps, 2),
+        "cpu_experts_per_step": round(cpus / steps, 2)}), flush=True)
+
+
 def cpu_baseline(layers, budget_s):
     """The float64 oracle on this host over a bounded sample of the same layer instances."""
     import oracle
@@ -207,6 +342,14 @@ def main():
     ap.add_argument("--layers", type=int, default=16)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--measure-bandwidths", action="store_true",
+                    help="measure B_P (fills over PCIe) and B_H (CPU branch) for --config, then exit")
+    ap.add_argument("--hybrid", action="store_true",
+                    help="time complete decode steps with fills and the CPU branch, then exit")
+    ap.add_argument("--slots", type=int, default=64, help="cache slots for --hybrid")
+    ap.add_argument("--b-pcie", type=float, default=50.0, help="B_P (GB/s) for --hybrid")
+    ap.add_argument("--b-host", type=float, default=60.0, help="B_H (GB/s) for --hybrid")
+    ap.add_argument("--max-fill", type=int, default=8, help="K for --hybrid")
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB",
                     help="run only a plain copy kernel of MIB MiB (counter calibration)")
     ap.add_argument("--ingest-traffic", nargs=7,
@@ -232,6 +375,13 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.measure_bandwidths:
+        measure_bandwidths(args.config, 8, 10)
+        return
+    if args.hybrid:
+        hybrid_decode(args.config, args.tokens, args.steps, args.warmup, args.slots, args.b_pcie,
+                      args.b_host, args.max_fill)
         return
     ftm.load()
     cfg = workloads.CONFIGS[args.config]
