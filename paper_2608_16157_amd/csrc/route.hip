@@ -68,11 +68,9 @@ __device__ __forceinline__ void topk_select_n(uint32_t (&key)[NB][NPL], int k, i
             const uint64_t ball = __ballot(best[b] == m[b]);
             const int w = static_cast<int>(__builtin_ctzll(ball));
             const int wbi = __builtin_amdgcn_readlane(bi[b], w);
-            if (lane == w) {
 #pragma unroll
-                for (int i = 0; i < NPL; ++i)
-                    if (i == wbi) key[b][i] = 0u;
-            }
+            for (int i = 0; i < NPL; ++i)
+                key[b][i] &= ~(0u - static_cast<uint32_t>((lane == w) & (i == wbi)));
             if (lane == j) {
                 mine[b] = m[b];
                 mine_e[b] = w * NPL + wbi;
