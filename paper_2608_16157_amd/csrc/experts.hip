@@ -41,6 +41,9 @@ namespace ftmoe {
 #ifndef FT_GEMV_D_FP8
 #define FT_GEMV_D_FP8 1
 #endif
+#ifndef FT_GEMV_LDS
+#define FT_GEMV_LDS 1
+#endif
 #ifndef FT_GEMV_NT_LOADS
 #define FT_GEMV_NT_LOADS 0
 #endif
@@ -61,6 +64,24 @@ __device__ __forceinline__ u32x4_t ld16(const void *p) {
 }
 __device__ __forceinline__ u32x4_t ld16_stream(const void *p) {
     return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
+}
+
+typedef __attribute__((address_space(3))) void gemv_lds_t;
+
+// Weight staging through LDS (FT_GEMV_LDS): a wave copies its own K block of the item's weight
+// rows into its own LDS region with global_load_lds, 16 bytes per lane and whole rows per
+// instruction (a 16x16x32 MFMA operand read straight from global memory would take only 64 bytes
+// of each of 16 rows per instruction), then reads the MFMA operands from there.  Within a row
+// the 16-byte chunks are XOR-swizzled by the row so that the operand reads of 16 rows hit 16
+// distinct bank groups: row bytes KB = 128 (fp8), 256 (bf16) or 512 (f32).
+__device__ __forceinline__ void gemv_dma16(const void *g, uint8_t *lds) {
+    __builtin_amdgcn_global_load_lds(g, (gemv_lds_t *)(lds), 16, 0, 0);
+}
+
+template <int KB>
+__device__ __forceinline__ int wswz(int row, int chunk) {
+    if constexpr (KB == 128) return chunk ^ ((row >> 1) & 7);
+    else return chunk ^ (row & 15);
 }
 
 // Element offset (within a 128-wide K block) of a lane's 16-byte weight load number c.
@@ -115,7 +136,13 @@ template <int WT, int EPI, int NB>
 __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int tiles) {
     constexpr int D = WTr<WT>::kBatch, NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
     constexpr int COLS = NB * 16;
-    __shared__ float s_red[kGemvWaves][16][COLS + 1];
+    constexpr int KB = 128 * WTr<WT>::kElem;                  // bytes of one row's K block
+    constexpr int STAGE = FT_GEMV_LDS ? D * NB * 16 * KB : 0; // per wave
+    constexpr int RED = kGemvWaves * 16 * (COLS + 1) * 4;
+    // the per-wave staging areas and the cross-wave reduction are disjoint: a wave writes its
+    // partial sums as soon as its own K range is done, while other waves may still be streaming
+    __shared__ __attribute__((aligned(1024))) uint8_t s_lds[kGemvWaves * STAGE + RED];
+    auto s_red = reinterpret_cast<float (*)[16][COLS + 1]>(s_lds + kGemvWaves * STAGE);
     if constexpr (EPI == EPI_GATEUP) {
         // zero the output that the down projection accumulates into
         const size_t n4 = static_cast<size_t>(a.T) * a.H / 4;
@@ -148,6 +175,26 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
             sbase[b] = (EPI == EPI_GATEUP ? a.s13 : a.s2) +
                        (static_cast<size_t>(slot) * (nrows / 128) + wrow / 128) * nkb;
     }
+    // global_load_lds sources: instruction c of block b covers rows [c * RPI, c * RPI + RPI) of
+    // the block's 16, LPR lanes per row; lane i fills LDS chunk i % LPR of its row, so it fetches
+    // the chunk the swizzle puts there
+    constexpr int LPR = KB / 16, RPI = 64 / LPR;
+    static_assert(!FT_GEMV_LDS || RPI * NL == 16, "one block is NL whole-row instructions");
+    const uint8_t *dsrc[NB][NL];
+    if constexpr (FT_GEMV_LDS) {
+#pragma unroll
+        for (int b = 0; b < NB; ++b)
+#pragma unroll
+            for (int c = 0; c < NL; ++c) {
+                const int j = c * RPI + lane / LPR;
+                const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
+                const int wr = EPI == EPI_GATEUP ? (j < 8 ? col0 + j : I + col0 + j - 8) : col0 + j;
+                dsrc[b][c] = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.w13 : a.w2) +
+                             (static_cast<size_t>(slot) * nrows + wr) * static_cast<size_t>(K) * WTr<WT>::kElem +
+                             wswz<KB>(j, lane % LPR) * 16;
+            }
+    }
+    uint8_t *wst = s_lds + wave * STAGE;
     const size_t a_elem = (WT == FT_DT_F32) ? 4 : 2;
     const int per = (nkb + kGemvWaves - 1) / kGemvWaves;
     const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
@@ -185,11 +232,30 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                 for (int b = 0; b < NB; ++b) {
 #pragma unroll
                     for (int c = 0; c < NL; ++c) {
-                        const uint8_t *p = wbase[b] + static_cast<size_t>(kb * 128 + wofs<WT>(c, q)) * WTr<WT>::kElem;
-                        wv[d][b][c] = FT_GEMV_NT_LOADS ? ld16_stream(p) : ld16(p);
+                        if constexpr (FT_GEMV_LDS) {
+                            gemv_dma16(dsrc[b][c] + static_cast<size_t>(kb) * KB,
+                                       wst + ((d * NB + b) * 16 * KB + c * 1024));
+                        } else {
+                            const uint8_t *p = wbase[b] + static_cast<size_t>(kb * 128 + wofs<WT>(c, q)) * WTr<WT>::kElem;
+                            wv[d][b][c] = FT_GEMV_NT_LOADS ? ld16_stream(p) : ld16(p);
+                        }
                     }
                     if constexpr (WT == FT_DT_FP8E4M3FN_B128) sv[d][b] = sbase[b][kb];
                 }
+            }
+            if constexpr (FT_GEMV_LDS) {
+                // this wave's staged rows have landed (its own DMA: no barrier needed); lane
+                // (n, q)'s operand chunk c is chunk 4 c + q of row n
+                __builtin_amdgcn_s_waitcnt(0x0 | (0x7 << 4) | (0xF << 8) | (0x0 << 14));   // vmcnt(0)
+                asm volatile("" ::: "memory");
+#pragma unroll
+                for (int d = 0; d < D; ++d)
+#pragma unroll
+                    for (int b = 0; b < NB; ++b)
+#pragma unroll
+                        for (int c = 0; c < NL; ++c)
+                            wv[d][b][c] = *reinterpret_cast<const u32x4_t *>(
+                                wst + (d * NB + b) * 16 * KB + n * KB + wswz<KB>(n, 4 * c + q) * 16);
             }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll

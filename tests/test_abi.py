@@ -160,3 +160,13 @@ def test_fill_and_hybrid_reject_before_enqueue():
     a = list(args)
     a[8] = 0
     assert lib.ft_moe_step_hybrid(*a) == ftm.FT_OK
+
+
+def test_library_has_no_undefined_library_symbols():
+    """Every kernel stub and internal function of libftmoe is defined in the library itself (a
+    kernel whose host stub the compiler dropped would only fail when first launched)."""
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--undefined-only", ftm.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    missing = [l for l in out.splitlines() if "ftmoe" in l]
+    assert not missing, missing
