@@ -295,6 +295,95 @@ def hybrid_decode(cfg_name, T, steps, warmup, n_slots, b_pcie, b_host, max_fill)
         "cpu_experts_per_step": round(cpus / steps, 2)}), flush=True)
 
 
+def prefill_pipeline(cfg_name, T, n_layers, reps):
+    """Full-layer double-buffered prefill (ft_prefill_layers): a T-token chunk through n_layers
+    MoE layers whose complete expert sets are loaded from pinned host memory, with the loads
+    overlapped against the evaluation and serialised, next to the loads alone and the
+    evaluation alone (HIP events on the evaluation stream)."""
+    import torch
+    import paper_2608_16157_amd as ftm
+    import workloads
+    cfg = workloads.CONFIGS[cfg_name]
+    E = cfg.n_experts
+    shared = cfg.shared_expert
+    n_slots = E + (1 if shared else 0)
+    n_pools = min(2, n_layers)           # two distinct layers' expert sets, cycled over the layers
+    pools, logits, xs = [], [], []
+    for l in range(n_pools):
+        lay = workloads.make_layer(cfg_name, T, layer=l, device="cuda", resident_frac=1.0)
+        order = lay.slot_table.tolist() + ([lay.shared_slot] if shared else [])
+        idx = torch.tensor(order, dtype=torch.long, device="cuda")
+        pool = {}
+        for n in ("w13", "w2", "s13", "s2"):
+            t = getattr(lay, n)
+            if t is None:
+                pool[n] = None
+                continue
+            pool[n] = torch.empty(t.shape, dtype=t.dtype, pin_memory=True)
+            pool[n].copy_(t.index_select(0, idx))
+        pools.append(pool)
+        logits.append(lay.logits)
+        xs.append(lay.x)
+        del lay, idx
+        torch.cuda.empty_cache()
+    desc = dict(hidden=cfg.hidden, inter=cfg.inter, n_experts=E, top_k=cfg.top_k, gating=cfg.gating,
+                w_dtype=cfg.w_dtype, x_dtype=cfg.x_dtype, n_slots=n_slots, shared_slot=E if shared else -1)
+    bufs = [{n: (torch.empty(t.shape, dtype=t.dtype, device="cuda") if t is not None else None)
+             for n, t in pools[0].items()} for _ in range(2)]
+    layer_bytes = sum(t.numel() * t.element_size() for t in pools[0].values() if t is not None)
+    table = torch.arange(E, dtype=torch.int32, device="cuda")
+    route = ftm.RouteBuffers(T, cfg.top_k, E)
+    ws = ftm.alloc_workspace(desc, T)
+    outs = [torch.empty(T, cfg.hidden, device="cuda") for _ in range(n_layers)]
+    hl = [pools[l % n_pools] for l in range(n_layers)]
+    lg = [logits[l % n_pools] for l in range(n_layers)]
+    xl = [xs[l % n_pools] for l in range(n_layers)]
+    copy_stream = torch.cuda.Stream()
+    hip = HipEvents()
+    stream = torch.cuda.current_stream().cuda_stream
+    a, b = hip.create(), hip.create()
+
+    def timed(fn):
+        fn()                                  # warm-up
+        torch.cuda.synchronize()
+        hip.hip.hipEventRecord(a, stream)
+        for _ in range(reps):
+            fn()
+        hip.hip.hipEventRecord(b, stream)
+        torch.cuda.synchronize()
+        return hip.elapsed_ms(a, b) / reps / n_layers
+
+    def loads_only():
+        for l in range(n_layers):
+            for n, t in hl[l].items():
+                if t is not None:
+                    bufs[l % 2][n].copy_(t, non_blocking=True)
+
+    def compute_only():
+        for l in range(n_layers):
+            ftm.ft_moe_forward(desc, bufs[l % 2], lg[l], table, xl[l], T, outs[l], route, ws)
+
+    t_overlap = timed(lambda: ftm.ft_prefill_layers(desc, hl, bufs, table, lg, xl, T, outs, route, ws,
+                                                    overlap=True, copy_stream=copy_stream))
+    t_serial = timed(lambda: ftm.ft_prefill_layers(desc, hl, bufs, table, lg, xl, T, outs, route, ws,
+                                                   overlap=False))
+    t_load = timed(loads_only)
+    t_comp = timed(compute_only)
+    print(json.dumps({
+        "measurement": "full-layer double-buffered prefill (ft_prefill_layers)",
+        "workload": f"{cfg_name} shapes, T={T} tokens, {n_layers} MoE layers, every layer's "
+                    f"{n_slots} experts ({layer_bytes} bytes) loaded from pinned host memory, "
+                    f"{n_pools} distinct layers' weights cycled",
+        "ms_per_layer_overlap": round(t_overlap, 3), "ms_per_layer_serial": round(t_serial, 3),
+        "ms_per_layer_loads_only": round(t_load, 3), "ms_per_layer_compute_only": round(t_comp, 3),
+        "load_gbs": round(layer_bytes / (t_load / 1e3) / 1e9, 2),
+        "tokens_per_s_overlap": round(T / (t_overlap * n_layers / 1e3), 1),
+        "tokens_per_s_serial": round(T / (t_serial * n_layers / 1e3), 1),
+        "serial_cost_frac": round(1 - t_overlap / t_serial, 4),
+        "hidden_compute_frac": round((t_serial - t_overlap) / t_comp, 4) if t_comp > 0 else None,
+    }), flush=True)
+
+
 def cpu_baseline(layers, budget_s):
     """The float64 oracle on this host over a bounded sample of the same layer instances."""
     import oracle
@@ -350,6 +439,9 @@ def main():
     ap.add_argument("--b-pcie", type=float, default=50.0, help="B_P (GB/s) for --hybrid")
     ap.add_argument("--b-host", type=float, default=60.0, help="B_H (GB/s) for --hybrid")
     ap.add_argument("--max-fill", type=int, default=8, help="K for --hybrid")
+    ap.add_argument("--prefill-pipeline", action="store_true",
+                    help="time full-layer double-buffered prefill over --layers layers (overlapped "
+                         "and serialised), then exit")
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB",
                     help="run only a plain copy kernel of MIB MiB (counter calibration)")
     ap.add_argument("--ingest-traffic", nargs=7,
@@ -378,6 +470,9 @@ def main():
         return
     if args.measure_bandwidths:
         measure_bandwidths(args.config, 8, 10)
+        return
+    if args.prefill_pipeline:
+        prefill_pipeline(args.config, args.tokens, args.layers, max(1, args.steps))
         return
     if args.hybrid:
         hybrid_decode(args.config, args.tokens, args.steps, args.warmup, args.slots, args.b_pcie,

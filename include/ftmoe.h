@@ -332,6 +332,40 @@ ft_status_t ft_moe_step_hybrid(const ft_moe_desc_t *desc, const ft_banks_t *dev_
                                const ft_hybrid_host_t *host, void *ws, size_t ws_bytes,
                                int32_t n_threads, void *stream);
 
+/*
+ * Full-layer double-buffered prefill of one chunk of T tokens through n_layers MoE layers whose
+ * complete expert sets live in host memory (Section 3.3, prefill: prefill routes nearly every
+ * expert of a layer, so experts are not fetched on demand; two full-layer buffers from the slot
+ * pool take turns, a transfer stream loading all experts of layer l + 1 into one, before that
+ * layer's routing is known, while the GPU evaluates layer l from the other.  Section 5,
+ * "Pipelined prefill": with the second buffer disabled the transfers serialise against the
+ * evaluation).
+ *   host_layers  [n_layers] HOST array of expert pools in PINNED host memory (hipHostMalloc;
+ *                pageable memory returns FT_ERR_SHAPE), each n_slots rows in the ft_banks_t layout:
+ *                the complete expert set of that layer, shared expert included
+ *   dev_buf      [2] HOST array of device full-layer buffers (distinct, n_slots rows each,
+ *                16-byte aligned); the call leaves the last two layers' experts in them
+ *   slot_table   [E] device: row of expert e in a full-layer buffer, the same for every layer
+ *                (the identity when the pools hold the experts in id order)
+ *   logits, x, out  [n_layers] HOST arrays of device pointers: layer l's router logits [T][E],
+ *                hidden states [T][H] (x_dtype) and output [T][H] float32, as for ft_moe_forward
+ *   route, ws    as for ft_moe_forward, reused by every layer (route holds the last layer's routing)
+ *   overlap      1: layer l + 1 loads on copy_stream while layer l is evaluated on stream
+ *                   (copy_stream must be a different, non-NULL stream);
+ *                0: load l, evaluate l, load l + 1, ... all on stream (copy_stream unused)
+ * Layer l's output equals ft_moe_forward of layer l with every expert resident.  The loads are
+ * DMA-engine copies (hipMemcpyAsync) and take no compute unit from the evaluation.  Everything
+ * is enqueued without blocking the host; the loads start after the work already on `stream`,
+ * and the last evaluation waits for the last load, so synchronising `stream` covers all of it.
+ * Host arrays are read during the call only.
+ */
+ft_status_t ft_prefill_layers(const ft_moe_desc_t *desc, int32_t n_layers,
+                              const ft_banks_t *host_layers, const ft_banks_t *dev_buf,
+                              const int32_t *slot_table, const float *const *logits,
+                              const void *const *x, int32_t T, float *const *out,
+                              const ft_route_t *route, void *ws, size_t ws_bytes, int32_t overlap,
+                              void *stream, void *copy_stream);
+
 /* Static string for a status code. */
 const char *ft_status_string(ft_status_t status);
 

@@ -15,6 +15,8 @@ of the C ABI declared in ``include/ftmoe.h``:
     ft_cache_fill(desc, host_pool, dev_banks, plan, max_fill, stream=None)
     ft_moe_step_hybrid(desc, dev_banks, host_pool, logits, slot_table, state, policy, x, T, out,
                        cpu_out_dev, route, plan, host, ws, n_threads=0, stream=None)
+    ft_prefill_layers(desc, host_layers, dev_bufs, slot_table, logits, x, T, out, route, ws,
+                      overlap=True, stream=None, copy_stream=None)
     ft_status_string(status) -> str
 
 ``desc`` is a dict with the ft_moe_desc_t fields; ``route`` a RouteBuffers; ``banks`` a dict
@@ -40,7 +42,7 @@ FT_DEV_SLOT_RANGE, FT_DEV_SLOT_DUP, FT_DEV_SLOT_SHARED = 1, 2, 4
 
 EXPORTED = ("ft_moe_workspace_bytes", "ft_route_only", "ft_moe_forward",
             "ft_moe_forward_profiled", "ft_miss_list_to_host", "ft_cache_plan", "ft_cpu_experts",
-            "ft_cache_fill", "ft_moe_step_hybrid", "ft_status_string")
+            "ft_cache_fill", "ft_moe_step_hybrid", "ft_prefill_layers", "ft_status_string")
 FT_PROF_STAGES = 4
 
 
@@ -138,6 +140,11 @@ def load(path: str = None) -> ctypes.CDLL:
                                        ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
                                        P(ft_route_t), P(ft_fill_plan_t), P(ft_hybrid_host_t),
                                        ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_void_p]
+    lib.ft_prefill_layers.restype = ctypes.c_int
+    lib.ft_prefill_layers.argtypes = [P(ft_moe_desc_t), ctypes.c_int32, P(ft_banks_t), P(ft_banks_t),
+                                      ctypes.c_void_p, P(ctypes.c_void_p), P(ctypes.c_void_p),
+                                      ctypes.c_int32, P(ctypes.c_void_p), P(ft_route_t), ctypes.c_void_p,
+                                      ctypes.c_size_t, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
     lib.ft_status_string.restype = ctypes.c_char_p
     lib.ft_status_string.argtypes = [ctypes.c_int]
     _lib = lib
@@ -367,3 +374,22 @@ def ft_moe_step_hybrid(desc: dict, dev_banks: dict, host_pool: dict, logits: tor
 def banks_of(layer) -> dict:
     """The bank tensors of a synthetic layer object (w13, w2, s13, s2 attributes)."""
     return {"w13": layer.w13, "w2": layer.w2, "s13": layer.s13, "s2": layer.s2}
+
+
+def ft_prefill_layers(desc: dict, host_layers: list, dev_bufs: list, slot_table: torch.Tensor,
+                      logits: list, x: list, T: int, out: list, route: RouteBuffers, ws: torch.Tensor,
+                      overlap: bool = True, stream=None, copy_stream=None) -> None:
+    """``host_layers``: one dict of pinned host tensors (w13, w2, s13, s2) per layer;
+    ``dev_bufs``: two dicts of device tensors; ``logits``, ``x``, ``out``: one device tensor per
+    layer.  ``copy_stream``: a torch stream or raw handle, required when ``overlap``."""
+    n = len(host_layers)
+    if not (len(logits) == len(x) == len(out) == n) or len(dev_bufs) != 2:
+        raise ValueError("one logits, x and out tensor per layer and two device buffers")
+    hl = (ft_banks_t * max(n, 1))(*[_banks(h) for h in host_layers])
+    db = (ft_banks_t * 2)(*[_banks(d) for d in dev_bufs])
+    arr = lambda ts: (ctypes.c_void_p * max(n, 1))(*[_ptr(t) for t in ts])
+    cs = None if copy_stream is None else _stream(copy_stream)
+    st = load().ft_prefill_layers(ctypes.byref(make_desc(desc)), n, hl, db, _ptr(slot_table),
+                                  arr(logits), arr(x), int(T), arr(out), ctypes.byref(route.c()),
+                                  _ptr(ws), ws.numel(), 1 if overlap else 0, _stream(stream), cs)
+    _check(st, "ft_prefill_layers")

@@ -91,6 +91,28 @@ RouteArgs route_args(const ft_moe_desc_t *d, const float *logits, const int32_t 
 
 }  // namespace
 
+namespace ftmoe {
+
+ft_status_t check_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
+                          const int32_t *slot_table, const void *x, int32_t T, const float *out_partial,
+                          const ft_route_t *route, const void *ws, size_t ws_bytes) {
+    if (ft_status_t s = check_common(desc, logits, slot_table, T, route, const_cast<void *>(ws), ws_bytes);
+        s != FT_OK)
+        return s;
+    if (!banks) return FT_ERR_NULL;
+    if (T == 0) return FT_OK;
+    if (!x || !out_partial) return FT_ERR_NULL;
+    if (desc->n_slots > 0 && (!banks->w13 || !banks->w2)) return FT_ERR_NULL;
+    if (desc->w_dtype == FT_DT_FP8E4M3FN_B128 && desc->n_slots > 0 && (!banks->s13 || !banks->s2))
+        return FT_ERR_NULL;
+    const uintptr_t al = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(out_partial) |
+                         reinterpret_cast<uintptr_t>(banks->w13) | reinterpret_cast<uintptr_t>(banks->w2);
+    if (al % 16) return FT_ERR_SHAPE;
+    return FT_OK;
+}
+
+}  // namespace ftmoe
+
 extern "C" {
 
 size_t ft_moe_workspace_bytes(const ft_moe_desc_t *desc, int32_t max_tokens) {
@@ -119,17 +141,10 @@ ft_status_t forward_impl(const ft_moe_desc_t *desc, const ft_banks_t *banks, con
                          const int32_t *slot_table, const void *x, int32_t T, float *out_partial,
                          const ft_route_t *route, void *ws, size_t ws_bytes, void *stream,
                          const ft_prof_events_t *events) {
-    if (ft_status_t s = check_common(desc, logits, slot_table, T, route, ws, ws_bytes); s != FT_OK)
+    if (ft_status_t s = check_forward(desc, banks, logits, slot_table, x, T, out_partial, route, ws, ws_bytes);
+        s != FT_OK)
         return s;
-    if (!banks) return FT_ERR_NULL;
     if (T == 0) return FT_OK;
-    if (!x || !out_partial) return FT_ERR_NULL;
-    if (desc->n_slots > 0 && (!banks->w13 || !banks->w2)) return FT_ERR_NULL;
-    if (desc->w_dtype == FT_DT_FP8E4M3FN_B128 && desc->n_slots > 0 && (!banks->s13 || !banks->s2))
-        return FT_ERR_NULL;
-    const uintptr_t al = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(out_partial) |
-                         reinterpret_cast<uintptr_t>(banks->w13) | reinterpret_cast<uintptr_t>(banks->w2);
-    if (al % 16) return FT_ERR_SHAPE;
     const hipStream_t s = static_cast<hipStream_t>(stream);
     Prof prof(events, s);
     const WsView wv = carve(desc, T, ws);

@@ -157,6 +157,11 @@ struct FillArgs {
 hipError_t launch_cache_fill(const FillArgs &a, int max_fill, hipStream_t s);
 hipError_t launch_add_partial(float *out, const float *other, size_t n, hipStream_t s);
 
+// Every host-checkable condition of ft_moe_forward (FT_OK when the call would be enqueued).
+ft_status_t check_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
+                          const int32_t *slot_table, const void *x, int32_t T, const float *out_partial,
+                          const ft_route_t *route, const void *ws, size_t ws_bytes);
+
 // CPU branch of a layer step (host_experts.cpp).
 struct CpuBank {
     const void *w;       // one expert's matrix, row-major

@@ -170,3 +170,46 @@ def test_library_has_no_undefined_library_symbols():
                          text=True, check=True).stdout
     missing = [l for l in out.splitlines() if "ftmoe" in l]
     assert not missing, missing
+
+
+def _prefill_call(desc, n_layers=2, T=4, overlap=1, copy_stream=FAKE + 8, stream=FAKE, null=None,
+                  ws_bytes=1 << 40, same_buf=False):
+    """ft_prefill_layers with fake device pointers; ``null`` names one argument to pass as NULL."""
+    lib = ftm.load()
+    n = max(n_layers, 1)
+    bank = lambda base: ftm.ft_banks_t(base, base + 0x100, base + 0x200, base + 0x300)
+    hl = (ftm.ft_banks_t * n)(*[bank(FAKE * (l + 3)) for l in range(n)])
+    db = (ftm.ft_banks_t * 2)(bank(FAKE), bank(FAKE if same_buf else 2 * FAKE))
+    arr = lambda: (ctypes.c_void_p * n)(*([FAKE] * n))
+    logits, x, out = arr(), arr(), arr()
+    if null == "x_layer":
+        x[n - 1] = None
+    if null == "dev_w2":
+        db[1].w2 = None
+    r = ftm.ft_route_t(*[FAKE] * 8)
+    args = dict(hl=hl, db=db, logits=logits, x=x, out=out, route=ctypes.byref(r))
+    if null in args:
+        args[null] = None
+    return lib.ft_prefill_layers(ctypes.byref(ftm.make_desc(desc)), n_layers, args["hl"], args["db"],
+                                 FAKE, args["logits"], args["x"], T, args["out"], args["route"], FAKE,
+                                 ws_bytes, overlap, stream, copy_stream)
+
+
+@pytest.mark.parametrize("kw,want", [
+    ({"n_layers": 0}, ftm.FT_OK),
+    ({"T": 0}, ftm.FT_OK),
+    ({"n_layers": -1}, ftm.FT_ERR_SHAPE),
+    ({"overlap": 2}, ftm.FT_ERR_SHAPE),
+    ({"copy_stream": None}, ftm.FT_ERR_SHAPE),           # overlap needs its own transfer stream
+    ({"copy_stream": FAKE}, ftm.FT_ERR_SHAPE),           # ... distinct from the evaluation stream
+    ({"same_buf": True}, ftm.FT_ERR_SHAPE),              # the two buffers must be distinct
+    ({"null": "hl"}, ftm.FT_ERR_NULL),
+    ({"null": "db"}, ftm.FT_ERR_NULL),
+    ({"null": "route"}, ftm.FT_ERR_NULL),
+    ({"null": "x_layer"}, ftm.FT_ERR_NULL),
+    ({"null": "dev_w2"}, ftm.FT_ERR_NULL),
+    ({"ws_bytes": 64}, ftm.FT_ERR_CAPACITY),
+])
+def test_prefill_layers_rejects_before_enqueue(kw, want):
+    assert _prefill_call(_desc(), **kw) == want
+    assert _prefill_call(_desc(hidden=100), **kw) in (ftm.FT_ERR_SHAPE, ftm.FT_ERR_NULL, want)
