@@ -384,6 +384,45 @@ def prefill_pipeline(cfg_name, T, n_layers, reps):
     }), flush=True)
 
 
+def placement_replay(n_prefill, n_decode, fractions, n_layers):
+    """Decode miss rates of the device cache's global LRU (every miss filled, and the q* split
+    at the B_P / B_H measured on this host) against a prefill-time placement and a routing-blind
+    placement, at equal capacity, replayed through ft_route_only / ft_cache_plan over synthetic
+    routing traces with short-range locality (one trace per layer, n_layers layers)."""
+    import torch
+    import workloads
+    from paper_2608_16157_amd import replay as rp
+    bw = {"qwen3_decode": (53.92, 82.74), "dsv3_decode": (55.5, 44.9)}
+    rows = []
+    t0 = time.perf_counter()
+    for name in ("qwen3_decode", "dsv3_decode"):
+        c = workloads.CONFIGS[name]
+        desc = dict(hidden=c.hidden, inter=c.inter, n_experts=c.n_experts, top_k=c.top_k,
+                    gating=c.gating, w_dtype=c.w_dtype, x_dtype=c.x_dtype, n_slots=0, shared_slot=-1)
+        traces = [workloads.routing_trace(name, n_prefill, n_decode, layer=l, device="cuda")
+                  for l in range(n_layers)]
+        for f in fractions:
+            C = max(c.top_k, int(f * c.n_experts))
+            rates = {}
+            for pol in rp.POLICIES:
+                miss = 0
+                for tr in traces:
+                    r = rp.replay(desc, tr, n_prefill, C, pol, *bw[name], k_max=c.top_k)
+                    miss += int(r["misses"].sum())
+                rates[pol] = round(miss / (n_layers * n_decode * c.top_k), 4)
+            rows.append({"workload": name, "capacity": C, "capacity_frac": round(C / c.n_experts, 3),
+                         "miss_rate": rates})
+            print(json.dumps(rows[-1]), file=sys.stderr, flush=True)
+    print(json.dumps({
+        "measurement": "decode expert-read miss rate by placement policy (routing-trace replay)",
+        "workload": f"synthetic routing traces: {n_prefill} prefill + {n_decode} decode tokens per "
+                    f"layer, {n_layers} layers, topic segments of mean 64 tokens over 8 Zipf "
+                    f"popularity rankings; B_P/B_H for 'split' as measured on this host",
+        "policies": {"lru": "global LRU, every miss filled", "split": "global LRU with the q* split",
+                     "prefill": "fixed top-C of the prefill routing", "blind": "fixed experts 0..C-1"},
+        "results": rows, "seconds": round(time.perf_counter() - t0, 1)}), flush=True)
+
+
 def cpu_baseline(layers, budget_s):
     """The float64 oracle on this host over a bounded sample of the same layer instances."""
     import oracle
@@ -442,6 +481,9 @@ def main():
     ap.add_argument("--prefill-pipeline", action="store_true",
                     help="time full-layer double-buffered prefill over --layers layers (overlapped "
                          "and serialised), then exit")
+    ap.add_argument("--replay", action="store_true",
+                    help="replay synthetic decode routing traces under each placement policy "
+                         "(--layers traces per workload), then exit")
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB",
                     help="run only a plain copy kernel of MIB MiB (counter calibration)")
     ap.add_argument("--ingest-traffic", nargs=7,
@@ -470,6 +512,9 @@ def main():
         return
     if args.measure_bandwidths:
         measure_bandwidths(args.config, 8, 10)
+        return
+    if args.replay:
+        placement_replay(1024, 2048, (0.11, 0.25, 0.37, 0.5, 0.75), min(args.layers, 4))
         return
     if args.prefill_pipeline:
         prefill_pipeline(args.config, args.tokens, args.layers, max(1, args.steps))

@@ -338,6 +338,68 @@ def cache_plan(desc: dict, routing: dict, slot_table, slot_expert, slot_stamp, b
 
 
 # ----------------------------------------------------------------------------------------
+# Placement replay over a routing trace (Section 5, "Expert locality", Figure 4b): the decode
+# cache's global LRU against placements fixed before decode, at equal capacity
+# ----------------------------------------------------------------------------------------
+#
+# Readings:
+# * a trace is n_prefill prefill tokens followed by decode tokens of one layer; decode routes
+#   one token per step.
+# * 'prefill' placement: the C experts with the most routed pairs over the prefill tokens, ties
+#   to the lower id, fixed for the whole decode (a placement chosen at prefill time).
+# * 'blind' placement: experts 0 .. C-1, fixed (a routing-blind split; expert ids carry no
+#   popularity in the synthetic traces).
+# * 'lru': the decode cache starts from the prefill placement (the experts that survive prefill
+#   seed decode) and every miss is filled (q = m), evicting the least recently demanded.
+# * 'split': as 'lru', but each step's misses are split by Eq. (dynamic-split); the experts left
+#   to the CPU are not cached.
+# * initial recency: slot i holds the i-th placed expert with stamp C - i, so the most demanded
+#   prefill expert is evicted last; decode step t (from 0) writes stamp C + 1 + t.
+# * a miss is a routed (token, expert) pair whose expert is not resident when the token is
+#   routed; the miss rate is misses / (decode tokens * k).
+
+
+def placement(desc: dict, prefill_logits, capacity: int, policy: str) -> list:
+    """Experts placed in slots 0 .. capacity-1 before decode, in slot order."""
+    E, k = desc["n_experts"], desc["top_k"]
+    if policy == "blind":
+        return list(range(capacity))
+    ids = route_topk(np.asarray(prefill_logits, dtype=np.float32), k)
+    counts = np.bincount(ids.ravel(), minlength=E)
+    order = sorted(range(E), key=lambda e: (-int(counts[e]), e))
+    return order[:capacity]
+
+
+def replay(desc: dict, logits, n_prefill: int, capacity: int, policy: str, b_pcie: float = 1.0,
+           b_host: float = 1.0, k_max: int = 64) -> dict:
+    """Per-step miss pairs of the decode tokens of one trace under a placement policy.
+
+    desc: the layer (n_slots and shared_slot are replaced by capacity and -1).
+    Returns misses [n_decode] int64 and the final slot_table, slot_expert, slot_stamp."""
+    logits = np.asarray(logits, dtype=np.float32)
+    E, k = desc["n_experts"], desc["top_k"]
+    d = dict(desc, n_slots=capacity, shared_slot=-1)
+    placed = placement(d, logits[:n_prefill], capacity, "blind" if policy == "blind" else "prefill")
+    table = np.full(E, -1, dtype=np.int32)
+    sexp = np.full(capacity, -1, dtype=np.int32)
+    stamp = np.zeros(capacity, dtype=np.uint32)
+    for i, e in enumerate(placed):
+        table[e], sexp[i], stamp[i] = i, e, capacity - i
+    if policy == "lru":
+        b_pcie, b_host = 1.0, 1.0          # B_H <= B_P: every miss is filled
+    misses = []
+    for t in range(n_prefill, logits.shape[0]):
+        r = route(d, logits[t:t + 1], table)
+        misses.append(int(r["n_miss"]))
+        if policy in ("lru", "split"):
+            step = capacity + 1 + (t - n_prefill)
+            p = cache_plan(d, r, table, sexp, stamp, b_pcie, b_host, k_max, step)
+            table, sexp, stamp = p["slot_table"], p["slot_expert"], p["slot_stamp"]
+    return dict(misses=np.array(misses, dtype=np.int64), slot_table=table, slot_expert=sexp,
+                slot_stamp=stamp)
+
+
+# ----------------------------------------------------------------------------------------
 # Error metric used by the parity tests
 # ----------------------------------------------------------------------------------------
 

@@ -514,3 +514,100 @@ def test_cache_plan_faulty_table_changes_nothing():
     assert plan["cpu_expert"] == [0, 1, 3, 4]
     assert np.array_equal(plan["slot_table"], table) and np.array_equal(plan["slot_expert"], sexp)
     assert np.array_equal(plan["slot_stamp"], stamp)
+
+
+# ---------------------------------------------------------------------------------------------
+# Placement replay (Section 5, expert locality): pins of oracle.placement / oracle.replay
+# ---------------------------------------------------------------------------------------------
+
+def _trace(seed, E, k, T, s=1.0, topics=3, seg=8):
+    """Small routing trace with topic segments (independent of workloads.routing_trace)."""
+    rng = np.random.default_rng(seed)
+    biases = [-s * np.log(rng.permutation(E) + 1.0) for _ in range(topics)]
+    logits = rng.standard_normal((T, E)).astype(np.float32)
+    t = 0
+    while t < T:
+        n = int(rng.integers(1, 2 * seg))
+        logits[t:t + n] += biases[int(rng.integers(topics))].astype(np.float32)
+        t += n
+    return logits
+
+
+def _desc_replay(E, k, gating=0):
+    return dict(hidden=128, inter=128, n_experts=E, top_k=k, gating=gating, w_dtype=0, x_dtype=0,
+                n_slots=0, shared_slot=-1)
+
+
+def _brute_topk(row, k):
+    # sort (logit desc, id asc) by Python tuple comparison
+    return [e for _, e in sorted((-float(v), e) for e, v in enumerate(row))][:k]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_replay_lru_top1_is_textbook_lru(seed):
+    """With one routed expert per token, the 'lru' replay is a textbook LRU cache seeded with the
+    prefill placement (the most demanded prefill expert most recent)."""
+    from collections import Counter, OrderedDict
+    E, C, P, N = 12, 4, 30, 120
+    logits = _trace(seed, E, 1, P + N)
+    got = oracle.replay(_desc_replay(E, 1), logits, P, C, "lru")["misses"]
+    cnt = Counter(_brute_topk(r, 1)[0] for r in logits[:P])
+    placed = sorted(range(E), key=lambda e: (-cnt[e], e))[:C]
+    cache = OrderedDict((e, None) for e in reversed(placed))   # last = most recent
+    want = []
+    for r in logits[P:]:
+        e = _brute_topk(r, 1)[0]
+        if e in cache:
+            cache.move_to_end(e)
+            want.append(0)
+        else:
+            want.append(1)
+            cache.popitem(last=False)
+            cache[e] = None
+    assert got.tolist() == want
+
+
+@pytest.mark.parametrize("policy", ["prefill", "blind"])
+@pytest.mark.parametrize("seed", range(4))
+def test_replay_static_policies_count_nonresident_pairs(policy, seed):
+    """A fixed placement misses exactly the routed pairs whose expert is outside the placed set."""
+    from collections import Counter
+    E, k, C, P, N = 16, 3, 6, 40, 60
+    logits = _trace(seed, E, k, P + N)
+    got = oracle.replay(_desc_replay(E, k), logits, P, C, policy)["misses"]
+    if policy == "blind":
+        placed = set(range(C))
+    else:
+        cnt = Counter(e for r in logits[:P] for e in _brute_topk(r, k))
+        placed = set(sorted(range(E), key=lambda e: (-cnt[e], e))[:C])
+    want = [sum(e not in placed for e in _brute_topk(r, k)) for r in logits[P:]]
+    assert got.tolist() == want
+
+
+def test_replay_full_capacity_and_fast_pcie():
+    """C = E never misses under any policy; with B_P >= B_H the split fills every miss, so it is
+    the LRU replay."""
+    E, k, P, N = 10, 2, 20, 50
+    logits = _trace(9, E, k, P + N)
+    for pol in ("lru", "split", "prefill", "blind"):
+        assert oracle.replay(_desc_replay(E, k), logits, P, E, pol)["misses"].sum() == 0
+    a = oracle.replay(_desc_replay(E, k), logits, P, 5, "lru")
+    b = oracle.replay(_desc_replay(E, k), logits, P, 5, "split", b_pcie=3.0, b_host=2.0)
+    assert a["misses"].tolist() == b["misses"].tolist()
+    assert np.array_equal(a["slot_expert"], b["slot_expert"])
+    # a slow link leaves misses to the CPU: the first decode step (same seed state) misses the
+    # same pairs
+    c = oracle.replay(_desc_replay(E, k), logits, P, 5, "split", b_pcie=1.0, b_host=4.0)
+    assert c["misses"][0] == a["misses"][0]
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_replay_lru_top1_inclusion(seed):
+    """LRU is a stack algorithm: with one request per step and nested seeds (the placement for C
+    is a prefix of the one for C + 1), misses never grow with capacity."""
+    E, P, N = 14, 30, 150
+    logits = _trace(100 + seed, E, 1, P + N)
+    m = [int(oracle.replay(_desc_replay(E, 1), logits, P, C, "lru")["misses"].sum())
+         for C in range(1, E + 1)]
+    assert all(a >= b for a, b in zip(m, m[1:])), m
+    assert m[-1] == 0

@@ -231,6 +231,31 @@ def make_layer(name: str, tokens: int, layer: int = 0, device="cpu", **kw) -> La
     return make_layer_from(CONFIGS[name], tokens, layer, device, **kw)
 
 
+def routing_trace(name: str, n_prefill: int, n_decode: int, layer: int = 0, n_topics: int = 8,
+                  mean_segment: float = 64.0, device="cpu") -> torch.Tensor:
+    """Router logits [n_prefill + n_decode][E] of one layer over a prefill and the decode that
+    follows it, with short-range locality: the tokens come in segments of geometric length
+    (mean ``mean_segment``), each segment drawn from one of ``n_topics`` popularity rankings
+    chosen at random, and every logit is N(0, 1) - s ln(rank) with the config's Zipf s."""
+    cfg = CONFIGS[name]
+    g = torch.Generator(device="cpu")
+    g.manual_seed(layer_seed(cfg.seed + 101, n_prefill + n_decode, layer))
+    E, T = cfg.n_experts, n_prefill + n_decode
+    bias = []
+    for _ in range(n_topics):
+        r = torch.empty(E, dtype=torch.float32)
+        r[torch.randperm(E, generator=g)] = torch.arange(1, E + 1, dtype=torch.float32)
+        bias.append(-cfg.zipf_s * torch.log(r))
+    logits = torch.randn(T, E, generator=g, dtype=torch.float32)
+    t = 0
+    while t < T:
+        n = int(torch.empty(1).geometric_(1.0 / mean_segment, generator=g).item())   # >= 1
+        topic = int(torch.randint(n_topics, (1,), generator=g))
+        logits[t:t + n] += bias[topic][None, :]
+        t += n
+    return logits.to(device)
+
+
 def random_layer(seed: int, *, hidden: int, inter: int, n_experts: int, top_k: int, tokens: int,
                  gating: int = GATE_SOFTMAX, w_dtype: int = DT_BF16, n_resident: Optional[int] = None,
                  shared: bool = False, zipf_s: float = 0.0, device="cpu",
