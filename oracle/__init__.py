@@ -37,6 +37,7 @@ GATE_SIGMOID = 1
 DT_F32 = 0
 DT_BF16 = 1
 DT_FP8 = 2
+DT_MXFP4 = 3
 
 STATUS_SLOT_RANGE = 1     # a slot outside [-1, n_slots)
 STATUS_SLOT_DUP = 2       # two experts share one slot
@@ -80,11 +81,50 @@ def fp8_blocks_to_f64(codes: np.ndarray, scales: np.ndarray) -> np.ndarray:
     return v * s
 
 
+def e2m1_value(code: int) -> float:
+    """OCP FP4 E2M1: 1 sign, 2 exponent (bias 1), 1 mantissa bit; exponent 0 is subnormal
+    (m/2); every code is finite."""
+    s = -1.0 if code & 0x8 else 1.0
+    e = (code >> 1) & 0x3
+    m = code & 0x1
+    if e == 0:
+        return s * (m / 2.0)
+    return s * (1.0 + m / 2.0) * 2.0 ** (e - 1)
+
+
+E2M1_TABLE = np.array([e2m1_value(c) for c in range(16)], dtype=np.float64)
+
+
+def e8m0_value(code: int) -> float:
+    """OCP E8M0 scale: 2^(code - 127); code 255 is NaN."""
+    return float("nan") if code == 255 else 2.0 ** (int(code) - 127)
+
+
+E8M0_TABLE = np.array([e8m0_value(c) for c in range(256)], dtype=np.float64)
+
+
+def mxfp4_to_f64(packed: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """Dequantise an MXFP4 matrix: packed [R][C/2] bytes holding E2M1 codes, element 2j in the
+    low nibble of byte j and element 2j+1 in the high nibble, with one E8M0 scale per 32
+    consecutive elements of a row (scales [R][C/32])."""
+    b = np.ascontiguousarray(packed).view(np.uint8)
+    r, half = b.shape
+    codes = np.empty((r, 2 * half), dtype=np.uint8)
+    codes[:, 0::2] = b & 0xF
+    codes[:, 1::2] = b >> 4
+    v = E2M1_TABLE[codes]
+    s = np.repeat(E8M0_TABLE[np.ascontiguousarray(scales).view(np.uint8)], 32, axis=1)
+    assert s.shape == v.shape
+    return v * s
+
+
 def decode_weight(bank: np.ndarray, w_dtype: int, scales=None) -> np.ndarray:
     if w_dtype == DT_F32:
         return bank.astype(np.float64)
     if w_dtype == DT_BF16:
         return bf16_bits_to_f64(bank)
+    if w_dtype == DT_MXFP4:
+        return mxfp4_to_f64(bank, scales)
     return fp8_blocks_to_f64(bank, scales)
 
 
@@ -220,7 +260,8 @@ def moe_partial(desc: dict, banks: dict, logits, slot_table, x, tokens=None):
 
     desc   : hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot
     banks  : w13 [n_slots][2I][H], w2 [n_slots][H][I] (float32 arrays, bf16 bit patterns as
-             uint16, or fp8 codes as uint8) and for fp8 s13, s2 block scales
+             uint16, fp8 codes as uint8, or MXFP4 code pairs as uint8 [..][K/2]) and for fp8 s13, s2
+             float32 block scales, for MXFP4 uint8 E8M0 scales [..][K/32]
     logits : [T][E] float32; slot_table : [E] int32; x : [T][H] (float32 or bf16 bits as uint16)
     tokens : optional list of token indices; only those rows are evaluated (others stay 0)
 

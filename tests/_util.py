@@ -27,6 +27,16 @@ def decode_bank_torch(bank: torch.Tensor, w_dtype: int, scales=None) -> torch.Te
         return bank.double()
     if w_dtype == 1:
         return bank.to(torch.float64)
+    if w_dtype == 3:
+        # MXFP4: split the nibbles, decode E2M1 arithmetically (sign, 2-bit exponent with bias
+        # 1, 1-bit mantissa; exponent 0 subnormal) and E8M0 through torch's own dtype
+        b = bank.to(torch.int64)
+        codes = torch.stack([b & 0xF, b >> 4], dim=-1).reshape(b.shape[0], -1)
+        sign = torch.where(codes >= 8, -1.0, 1.0).double()
+        e, m = (codes >> 1) & 3, (codes & 1).double()
+        mag = torch.where(e == 0, m * 0.5, (1.0 + m * 0.5) * torch.pow(2.0, (e - 1).double()))
+        s = scales.contiguous().view(torch.float8_e8m0fnu).to(torch.float64).repeat_interleave(32, 1)
+        return sign * mag * s
     v = bank.view(torch.float8_e4m3fn).to(torch.float64)
     s = scales.double().repeat_interleave(128, 0).repeat_interleave(128, 1)
     return v * s

@@ -28,6 +28,49 @@ def test_e4m3fn_table_matches_torch_for_all_256_codes():
     assert ours[0x7E] == 448.0 and ours[0x01] == 2.0 ** -9 and ours[0x80] == 0.0
 
 
+def test_e2m1_table_closed_form():
+    """The 16 OCP FP4 E2M1 values: magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6 for codes 0-7, the
+    same negated for codes 8-15 (code 8 is -0)."""
+    mags = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]
+    want = mags + [-m for m in mags]
+    assert oracle.E2M1_TABLE.tolist() == want
+    assert np.signbit(oracle.E2M1_TABLE[8])
+
+
+def test_e8m0_table_matches_torch_for_all_256_codes():
+    codes = torch.arange(256, dtype=torch.uint8)
+    ref = codes.view(torch.float8_e8m0fnu).to(torch.float64).numpy()
+    got = oracle.E8M0_TABLE
+    assert np.isnan(got[255]) and np.isnan(ref[255])
+    assert np.array_equal(got[:255], ref[:255])
+    assert got[127] == 1.0 and got[0] == 2.0 ** -127
+
+
+def test_mxfp4_nibble_order_and_block_scales():
+    """Byte j holds element 2j in its low nibble; each run of 32 elements of a row has its own
+    scale."""
+    packed = np.zeros((2, 32), dtype=np.uint8)        # 2 rows x 64 elements
+    packed[0, 0] = 0x21                               # elements 0, 1 = codes 1, 2 = 0.5, 1.0
+    packed[0, 16] = 0xF7                              # elements 32, 33 = 6.0, -6.0
+    packed[1, 31] = 0x9C                              # elements 62, 63 = -2.0, -0.5
+    scales = np.array([[127, 130], [126, 120]], dtype=np.uint8)
+    d = oracle.mxfp4_to_f64(packed, scales)
+    assert d.shape == (2, 64)
+    assert (d[0, 0], d[0, 1]) == (0.5, 1.0)
+    assert (d[0, 32], d[0, 33]) == (6.0 * 8, -6.0 * 8)
+    assert (d[1, 62], d[1, 63]) == (-2.0 * 2.0 ** -7, -0.5 * 2.0 ** -7)
+    assert np.count_nonzero(d) == 6
+
+
+def test_mxfp4_decode_matches_torch_based_decode():
+    import workloads
+    w = torch.randn(64, 256, generator=torch.Generator().manual_seed(4)) * 0.05
+    packed, sc = workloads.quantize_mxfp4(w)
+    got = oracle.decode_weight(packed.numpy(), oracle.DT_MXFP4, sc.numpy())
+    want = decode_bank_torch(packed, 3, sc).numpy()
+    assert np.array_equal(got, want)
+
+
 def test_bf16_decode_matches_torch():
     g = torch.Generator().manual_seed(5)
     x = torch.randn(4096, generator=g) * torch.exp(torch.randn(4096, generator=g) * 20)
@@ -251,7 +294,8 @@ def _with_residency(lay, mask):
 
 
 @pytest.mark.parametrize("w_dtype,gating,shared", [(0, 0, False), (1, 0, False), (1, 1, False),
-                                                   (2, 1, True), (2, 0, False)])
+                                                   (2, 1, True), (2, 0, False), (3, 1, False),
+                                                   (3, 0, True)])
 def test_partial_output_matches_dense_masked_evaluation(w_dtype, gating, shared):
     lay = _full_pool_layer(3 + w_dtype, w_dtype, gating, shared)
     g = torch.Generator().manual_seed(9)
@@ -265,7 +309,7 @@ def test_partial_output_matches_dense_masked_evaluation(w_dtype, gating, shared)
         np.testing.assert_allclose(out, ref.astype(np.float32), rtol=2e-6, atol=1e-7)
 
 
-@pytest.mark.parametrize("w_dtype,shared", [(1, False), (2, True)])
+@pytest.mark.parametrize("w_dtype,shared", [(1, False), (2, True), (3, False)])
 def test_zero_residency_and_additivity(w_dtype, shared):
     lay = _full_pool_layer(21, w_dtype, 1, shared, E=8, k=4, T=10)
     E = lay.n_experts

@@ -44,6 +44,8 @@ GATE_SIGMOID = 1   # sigmoid per expert, keep top-k, renormalise over the k
 DT_F32 = 0
 DT_BF16 = 1
 DT_FP8 = 2         # fp8 e4m3fn codes with one float32 scale per 128x128 block
+DT_MXFP4 = 3       # OCP MXFP4: E2M1 code pairs (even element in the low nibble), one E8M0 scale
+                   # per 32 consecutive elements of a row
 
 FP8_MAX = 448.0
 
@@ -85,6 +87,13 @@ CONFIGS = {
     # DeepSeek-V3-shaped prefill chunk whose hot set shifts every 1024 tokens.
     "dsv3_prefill": LayerConfig("dsv3_prefill", 7168, 2048, 256, 8, GATE_SIGMOID, DT_FP8, DT_BF16,
                                 (8192,), 4, 0.40, 1.2, True, shift_every=1024),
+    # DeepSeek-V4-Flash-shaped layer with MXFP4 routed experts: 256 routed experts, top-6 (the
+    # paper's figures); H = 4096, I = 2048 make one expert 13.4 MB, the size its 140 GB pool of
+    # 43 x 256 experts implies.  No shared expert (the paper names routed experts only).
+    "dsv4flash_decode": LayerConfig("dsv4flash_decode", 4096, 2048, 256, 6, GATE_SIGMOID, DT_MXFP4,
+                                    DT_BF16, (1, 16, 64), 5, 0.25, 1.2, False),
+    "dsv4flash_prefill": LayerConfig("dsv4flash_prefill", 4096, 2048, 256, 6, GATE_SIGMOID, DT_MXFP4,
+                                     DT_BF16, (8192,), 6, 0.40, 1.2, False, shift_every=1024),
 }
 
 
@@ -103,10 +112,11 @@ class Layer:
     logits: torch.Tensor      # [T][E] float32
     slot_table: torch.Tensor  # [E] int32
     x: torch.Tensor           # [T][H] bfloat16 or float32
-    w13: torch.Tensor         # [n_slots][2I][H] float32 / bfloat16 / uint8 (fp8 codes)
-    w2: torch.Tensor          # [n_slots][H][I]
-    s13: Optional[torch.Tensor]  # [n_slots][2I/128][H/128] float32 (fp8 only)
-    s2: Optional[torch.Tensor]   # [n_slots][H/128][I/128] float32 (fp8 only)
+    w13: torch.Tensor         # [n_slots][2I][H] float32 / bfloat16 / uint8 (fp8 codes);
+                              # MXFP4: [n_slots][2I][H/2] uint8 code pairs
+    w2: torch.Tensor          # [n_slots][H][I] (MXFP4: [n_slots][H][I/2])
+    s13: Optional[torch.Tensor]  # fp8: [n_slots][2I/128][H/128] float32; MXFP4: [n_slots][2I][H/32] uint8
+    s2: Optional[torch.Tensor]   # fp8: [n_slots][H/128][I/128] float32; MXFP4: [n_slots][H][I/32] uint8
 
     @property
     def tokens(self) -> int:
@@ -143,13 +153,69 @@ def quantize_fp8_blocks(w: torch.Tensor):
     return codes, scale
 
 
+def quantize_mxfp4(w: torch.Tensor):
+    """Input preparation only: float32 ``[R][C]`` -> (E2M1 code pairs [R][C/2] uint8, E8M0 scales
+    [R][C/32] uint8), following the OCP MX recipe: per 32-element block the shared exponent is
+    floor(log2(amax)) - 2 (2 = the largest E2M1 exponent), and each element is rounded to the
+    nearest E2M1 value, ties to even, saturating at +-6; an all-zero block takes scale 1."""
+    r, c = w.shape
+    blk = w.view(r, c // 32, 32)
+    amax = blk.abs().amax(dim=2)
+    e = torch.where(amax > 0, torch.floor(torch.log2(torch.where(amax > 0, amax, torch.ones_like(amax)))) - 2,
+                    torch.zeros_like(amax))
+    code_s = (e + 127).clamp_(0, 254)
+    scale = torch.pow(2.0, code_s - 127)
+    q = blk / scale[:, :, None]
+    a = q.abs()
+    idx = ((a > 0.25).to(torch.uint8) + (a >= 0.75) + (a > 1.25) + (a >= 1.75) + (a > 2.5) + (a >= 3.5)
+           + (a > 5)).to(torch.uint8)
+    codes = (idx | (torch.signbit(q).to(torch.uint8) << 3)).view(r, c)
+    packed = (codes[:, 0::2] | (codes[:, 1::2] << 4)).contiguous()
+    return packed, code_s.to(torch.uint8)
+
+
 def _weights(g, rows, cols, w_dtype, device):
     w = torch.randn(rows, cols, generator=g, dtype=torch.float32, device=device).mul_(0.02)
     if w_dtype == DT_F32:
         return w, None
     if w_dtype == DT_BF16:
         return w.to(torch.bfloat16), None
+    if w_dtype == DT_MXFP4:
+        return quantize_mxfp4(w)
     return quantize_fp8_blocks(w)
+
+
+def alloc_banks(n_slots: int, hidden: int, inter: int, w_dtype: int, device="cpu"):
+    """Zeroed (w13, w2, s13, s2) banks of n_slots rows in the bank layout of w_dtype."""
+    H, I = hidden, inter
+    if w_dtype == DT_MXFP4:
+        u8 = dict(dtype=torch.uint8, device=device)
+        return (torch.zeros(n_slots, 2 * I, H // 2, **u8), torch.zeros(n_slots, H, I // 2, **u8),
+                torch.zeros(n_slots, 2 * I, H // 32, **u8), torch.zeros(n_slots, H, I // 32, **u8))
+    wdt = {DT_F32: torch.float32, DT_BF16: torch.bfloat16, DT_FP8: torch.uint8}[w_dtype]
+    w13 = torch.zeros(n_slots, 2 * I, H, dtype=wdt, device=device)
+    w2 = torch.zeros(n_slots, H, I, dtype=wdt, device=device)
+    if w_dtype != DT_FP8:
+        return w13, w2, None, None
+    return (w13, w2, torch.ones(n_slots, 2 * I // 128, H // 128, device=device),
+            torch.ones(n_slots, H // 128, I // 128, device=device))
+
+
+def put_expert(banks, slot: int, inter: int, w_dtype: int, w1, a1, w3, a3, wd, ad):
+    """Store one expert's quantised projections (from _weights) in bank row ``slot``."""
+    w13, w2, s13, s2 = banks
+    I = inter
+    w13[slot, :I] = w1
+    w13[slot, I:] = w3
+    w2[slot] = wd
+    if w_dtype == DT_FP8:
+        s13[slot, : I // 128] = a1
+        s13[slot, I // 128:] = a3
+        s2[slot] = ad
+    elif w_dtype == DT_MXFP4:
+        s13[slot, :I] = a1
+        s13[slot, I:] = a3
+        s2[slot] = ad
 
 
 def make_layer_from(cfg: LayerConfig, tokens: int, layer: int = 0, device="cpu",
@@ -202,13 +268,8 @@ def make_layer_from(cfg: LayerConfig, tokens: int, layer: int = 0, device="cpu",
         x = x.to(torch.bfloat16)
 
     # 6. weights, one bank row per slot
-    wdt = {DT_F32: torch.float32, DT_BF16: torch.bfloat16, DT_FP8: torch.uint8}[cfg.w_dtype]
-    w13 = torch.empty(n_slots, 2 * I, H, dtype=wdt, device=device)
-    w2 = torch.empty(n_slots, H, I, dtype=wdt, device=device)
-    s13 = s2 = None
-    if cfg.w_dtype == DT_FP8:
-        s13 = torch.empty(n_slots, 2 * I // 128, H // 128, dtype=torch.float32, device=device)
-        s2 = torch.empty(n_slots, H // 128, I // 128, dtype=torch.float32, device=device)
+    banks = alloc_banks(n_slots, H, I, cfg.w_dtype, device)
+    w13, w2, s13, s2 = banks
     order = [(e, int(slot_table[e])) for e in resident]
     if cfg.shared_expert:
         order.append((-1, shared_slot))
@@ -216,13 +277,7 @@ def make_layer_from(cfg: LayerConfig, tokens: int, layer: int = 0, device="cpu",
         w1, a1 = _weights(g, I, H, cfg.w_dtype, device)
         w3, a3 = _weights(g, I, H, cfg.w_dtype, device)
         wd, ad = _weights(g, H, I, cfg.w_dtype, device)
-        w13[slot, :I] = w1
-        w13[slot, I:] = w3
-        w2[slot] = wd
-        if cfg.w_dtype == DT_FP8:
-            s13[slot, : I // 128] = a1
-            s13[slot, I // 128:] = a3
-            s2[slot] = ad
+        put_expert(banks, slot, I, cfg.w_dtype, w1, a1, w3, a3, wd, ad)
     return Layer(H, I, E, cfg.top_k, cfg.gating, cfg.w_dtype, cfg.x_dtype, n_slots, shared_slot,
                  logits, slot_table, x, w13, w2, s13, s2)
 
@@ -291,24 +346,13 @@ def random_layer(seed: int, *, hidden: int, inter: int, n_experts: int, top_k: i
     x = torch.randn(tokens, hidden, generator=g)
     if x_dtype == DT_BF16:
         x = x.to(torch.bfloat16)
-    wdt = {DT_F32: torch.float32, DT_BF16: torch.bfloat16, DT_FP8: torch.uint8}[w_dtype]
-    w13 = torch.zeros(n_slots, 2 * inter, hidden, dtype=wdt)
-    w2 = torch.zeros(n_slots, hidden, inter, dtype=wdt)
-    s13 = s2 = None
-    if w_dtype == DT_FP8:
-        s13 = torch.ones(n_slots, 2 * inter // 128, hidden // 128)
-        s2 = torch.ones(n_slots, hidden // 128, inter // 128)
+    banks = alloc_banks(n_slots, hidden, inter, w_dtype)
+    w13, w2, s13, s2 = banks
     for slot in range(n_slots):   # every pool slot gets weights, also the empty ones
         w1, a1 = _weights(g, inter, hidden, w_dtype, "cpu")
         w3, a3 = _weights(g, inter, hidden, w_dtype, "cpu")
         wd, ad = _weights(g, hidden, inter, w_dtype, "cpu")
-        w13[slot, :inter] = w1
-        w13[slot, inter:] = w3
-        w2[slot] = wd
-        if w_dtype == DT_FP8:
-            s13[slot, : inter // 128] = a1
-            s13[slot, inter // 128:] = a3
-            s2[slot] = ad
+        put_expert(banks, slot, inter, w_dtype, w1, a1, w3, a3, wd, ad)
     lay = Layer(hidden, inter, E, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot,
                 logits.float(), slot_table, x, w13, w2, s13, s2)
     return lay.to(device)
