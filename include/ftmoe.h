@@ -51,7 +51,10 @@ enum { FT_GATE_SOFTMAX_TOPK_RENORM = 0, FT_GATE_SIGMOID_TOPK_RENORM = 1 };
 enum {
     FT_DT_F32 = 0,              /* IEEE float32 */
     FT_DT_BF16 = 1,             /* bfloat16 */
-    FT_DT_FP8E4M3FN_B128 = 2    /* OCP fp8 e4m3fn codes, one float32 scale per 128x128 block */
+    FT_DT_FP8E4M3FN_B128 = 2,   /* OCP fp8 e4m3fn codes, one float32 scale per 128x128 block */
+    FT_DT_MXFP4 = 3             /* OCP MXFP4: fp4 e2m1 codes, two per byte (element 2j in the low
+                                   nibble of byte j), one e8m0 scale byte (2^(s-127)) per 32
+                                   consecutive elements of a row */
 };
 
 #define FT_SLOT_MISS (-1)
@@ -66,8 +69,10 @@ enum {
  *   hidden (H), inter (I): multiples of 128, 128 <= H, I <= 65536.
  *   n_experts (E): 1..1024 routed experts.   top_k (k): 1..min(E, 64).
  *   gating: FT_GATE_*.
- *   w_dtype: FT_DT_F32 with x_dtype FT_DT_F32, or FT_DT_BF16 / FT_DT_FP8E4M3FN_B128 with
- *            x_dtype FT_DT_BF16.  Activations stay bf16 and products accumulate in float32.
+ *   w_dtype: FT_DT_F32 with x_dtype FT_DT_F32, or FT_DT_BF16 / FT_DT_FP8E4M3FN_B128 /
+ *            FT_DT_MXFP4 with x_dtype FT_DT_BF16.  Activations stay bf16 and products accumulate
+ *            in float32.  MXFP4 weights times their scale are exact in bf16, so both paths
+ *            widen them exactly.
  *            fp8 weights: with T < 256 tokens each code is widened exactly and the block scale
  *            multiplies the float32 partial sum of its 128-wide K block; with T >= 256 (matrix
  *            core path) each code times its block scale is rounded to bf16 once (relative
@@ -89,14 +94,18 @@ typedef struct {
  * row-major:
  *   w13 [n_slots][2I][H]  rows 0..I-1 = gate projection W1, rows I..2I-1 = up projection W3
  *   w2  [n_slots][H][I]   down projection
- *   s13 [n_slots][2I/128][H/128], s2 [n_slots][H/128][I/128]  float32 block scales (fp8 only,
- *       NULL otherwise): weight (r, c) = code(r, c) * scale(r/128, c/128).
+ *   s13 [n_slots][2I/128][H/128], s2 [n_slots][H/128][I/128]  float32 block scales (fp8,
+ *       NULL for f32 and bf16): weight (r, c) = code(r, c) * scale(r/128, c/128).
+ * MXFP4 packs two codes per byte along each row and keeps byte scales per 32 elements:
+ *   w13 [n_slots][2I][H/2], w2 [n_slots][H][I/2]  uint8 code pairs
+ *   s13 [n_slots][2I][H/32], s2 [n_slots][H][I/32]  uint8 e8m0 scales:
+ *       weight (r, c) = e2m1(code(r, c)) * 2^(s(r, c/32) - 127)
  */
 typedef struct {
     const void *w13;
     const void *w2;
-    const float *s13;
-    const float *s2;
+    const void *s13;   /* float32 (fp8) or uint8 (MXFP4) scales; NULL for f32 and bf16 */
+    const void *s2;
 } ft_banks_t;
 
 /*

@@ -36,7 +36,7 @@ LIB_PATH = os.path.join(HERE, "libftmoe.so")
 
 FT_OK, FT_ERR_NULL, FT_ERR_SHAPE, FT_ERR_DTYPE, FT_ERR_CAPACITY, FT_ERR_HIP = range(6)
 FT_GATE_SOFTMAX_TOPK_RENORM, FT_GATE_SIGMOID_TOPK_RENORM = 0, 1
-FT_DT_F32, FT_DT_BF16, FT_DT_FP8E4M3FN_B128 = 0, 1, 2
+FT_DT_F32, FT_DT_BF16, FT_DT_FP8E4M3FN_B128, FT_DT_MXFP4 = 0, 1, 2, 3
 FT_SLOT_MISS = -1
 FT_DEV_SLOT_RANGE, FT_DEV_SLOT_DUP, FT_DEV_SLOT_SHARED = 1, 2, 4
 

@@ -26,7 +26,8 @@ ft_status_t dtype_status(const ft_moe_desc_t *d) {
     if (d->gating != FT_GATE_SOFTMAX_TOPK_RENORM && d->gating != FT_GATE_SIGMOID_TOPK_RENORM)
         return FT_ERR_DTYPE;
     if (d->w_dtype == FT_DT_F32 && d->x_dtype == FT_DT_F32) return FT_OK;
-    if ((d->w_dtype == FT_DT_BF16 || d->w_dtype == FT_DT_FP8E4M3FN_B128) && d->x_dtype == FT_DT_BF16)
+    if ((d->w_dtype == FT_DT_BF16 || d->w_dtype == FT_DT_FP8E4M3FN_B128 || d->w_dtype == FT_DT_MXFP4) &&
+        d->x_dtype == FT_DT_BF16)
         return FT_OK;
     return FT_ERR_DTYPE;
 }
@@ -103,8 +104,7 @@ ft_status_t check_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, co
     if (T == 0) return FT_OK;
     if (!x || !out_partial) return FT_ERR_NULL;
     if (desc->n_slots > 0 && (!banks->w13 || !banks->w2)) return FT_ERR_NULL;
-    if (desc->w_dtype == FT_DT_FP8E4M3FN_B128 && desc->n_slots > 0 && (!banks->s13 || !banks->s2))
-        return FT_ERR_NULL;
+    if (has_scales(desc->w_dtype) && desc->n_slots > 0 && (!banks->s13 || !banks->s2)) return FT_ERR_NULL;
     const uintptr_t al = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(out_partial) |
                          reinterpret_cast<uintptr_t>(banks->w13) | reinterpret_cast<uintptr_t>(banks->w2);
     if (al % 16) return FT_ERR_SHAPE;
@@ -256,8 +256,7 @@ ft_status_t ft_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_poo
     if (T == 0) return FT_OK;
     if (!x || !topk_ids || !topk_w || !out || (n_list > 0 && !experts)) return FT_ERR_NULL;
     if (n_list > 0 && (!host_pool->w13 || !host_pool->w2)) return FT_ERR_NULL;
-    if (desc->w_dtype == FT_DT_FP8E4M3FN_B128 && n_list > 0 && (!host_pool->s13 || !host_pool->s2))
-        return FT_ERR_NULL;
+    if (has_scales(desc->w_dtype) && n_list > 0 && (!host_pool->s13 || !host_pool->s2)) return FT_ERR_NULL;
     std::vector<char> seen(desc->n_experts, 0);
     for (int i = 0; i < n_list; ++i) {
         const int e = experts[i];
@@ -297,16 +296,14 @@ ft_status_t ft_cache_fill(const ft_moe_desc_t *desc, const ft_banks_t *host_pool
     if (ft_status_t st = dtype_status(desc); st != FT_OK) return st;
     if (max_fill < 1 || max_fill > kPlanMaxFill) return FT_ERR_SHAPE;
     if (!plan->counts || !plan->fill_expert || !plan->fill_slot) return FT_ERR_NULL;
-    const bool fp8 = desc->w_dtype == FT_DT_FP8E4M3FN_B128;
-    const void *hp[4] = {host_pool->w13, host_pool->w2, fp8 ? host_pool->s13 : nullptr,
-                         fp8 ? host_pool->s2 : nullptr};
+    const bool sc = has_scales(desc->w_dtype);
+    const void *hp[4] = {host_pool->w13, host_pool->w2, sc ? host_pool->s13 : nullptr,
+                         sc ? host_pool->s2 : nullptr};
     void *dp[4] = {const_cast<void *>(dev_banks->w13), const_cast<void *>(dev_banks->w2),
-                   fp8 ? const_cast<float *>(dev_banks->s13) : nullptr,
-                   fp8 ? const_cast<float *>(dev_banks->s2) : nullptr};
-    const size_t H = desc->hidden, I = desc->inter;
-    const size_t wb = desc->w_dtype == FT_DT_F32 ? 4 : (desc->w_dtype == FT_DT_BF16 ? 2 : 1);
-    const size_t rows[4] = {2 * I * H * wb, H * I * wb, fp8 ? (2 * I / 128) * (H / 128) * 4 : 0,
-                            fp8 ? (H / 128) * (I / 128) * 4 : 0};
+                   sc ? const_cast<void *>(dev_banks->s13) : nullptr,
+                   sc ? const_cast<void *>(dev_banks->s2) : nullptr};
+    const ExpertBytes eb = expert_bytes(desc->w_dtype, desc->hidden, desc->inter);
+    const size_t rows[4] = {eb.w13, eb.w2, eb.s13, eb.s2};
     FillArgs a{};
     a.E = desc->n_experts;
     a.n_slots = desc->n_slots;

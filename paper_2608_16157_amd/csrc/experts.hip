@@ -29,6 +29,9 @@ namespace ftmoe {
 #ifndef FT_GEMV_NB_FP8
 #define FT_GEMV_NB_FP8 4
 #endif
+#ifndef FT_GEMV_NB_FP4
+#define FT_GEMV_NB_FP4 4
+#endif
 #ifndef FT_GEMV_MT_MAX
 #define FT_GEMV_MT_MAX 2
 #endif
@@ -40,6 +43,9 @@ namespace ftmoe {
 #endif
 #ifndef FT_GEMV_D_FP8
 #define FT_GEMV_D_FP8 1
+#endif
+#ifndef FT_GEMV_D_FP4
+#define FT_GEMV_D_FP4 1
 #endif
 #ifndef FT_GEMV_LDS
 #define FT_GEMV_LDS 1
@@ -54,10 +60,15 @@ constexpr int kGemvWaves = kGemvThreads / kWave;
 enum { EPI_GATEUP = 0, EPI_DOWN = 1 };
 
 template <int WT> struct WTr;
-// kLoads: 16-byte weight loads per lane per 128-wide K block; kBatch: K blocks in flight ahead
-template <> struct WTr<FT_DT_F32> { static constexpr int kLoads = 8, kElem = 4, kBatch = FT_GEMV_D_F32; };
-template <> struct WTr<FT_DT_BF16> { static constexpr int kLoads = 4, kElem = 2, kBatch = FT_GEMV_D_BF16; };
-template <> struct WTr<FT_DT_FP8E4M3FN_B128> { static constexpr int kLoads = 2, kElem = 1, kBatch = FT_GEMV_D_FP8; };
+// kLoads: 16-byte weight loads per lane per 128-wide K block; kBlock: bytes of one row's
+// 128-wide K block; kBatch: K blocks in flight ahead
+template <> struct WTr<FT_DT_F32> { static constexpr int kLoads = 8, kBlock = 512, kBatch = FT_GEMV_D_F32; };
+template <> struct WTr<FT_DT_BF16> { static constexpr int kLoads = 4, kBlock = 256, kBatch = FT_GEMV_D_BF16; };
+template <> struct WTr<FT_DT_FP8E4M3FN_B128> { static constexpr int kLoads = 2, kBlock = 128, kBatch = FT_GEMV_D_FP8; };
+template <> struct WTr<FT_DT_MXFP4> { static constexpr int kLoads = 1, kBlock = 64, kBatch = FT_GEMV_D_FP4; };
+template <int WT> constexpr int gemv_nb() {
+    return WT == FT_DT_FP8E4M3FN_B128 ? FT_GEMV_NB_FP8 : (WT == FT_DT_MXFP4 ? FT_GEMV_NB_FP4 : FT_GEMV_NB);
+}
 
 __device__ __forceinline__ u32x4_t ld16(const void *p) {
     return *reinterpret_cast<const u32x4_t *>(p);
@@ -73,27 +84,27 @@ typedef __attribute__((address_space(3))) void gemv_lds_t;
 // instruction (a 16x16x32 MFMA operand read straight from global memory would take only 64 bytes
 // of each of 16 rows per instruction), then reads the MFMA operands from there.  Within a row
 // the 16-byte chunks are XOR-swizzled by the row so that the operand reads of 16 rows hit 16
-// distinct bank groups: row bytes KB = 128 (fp8), 256 (bf16) or 512 (f32).
+// distinct bank groups: row bytes KB = 64 (MXFP4), 128 (fp8), 256 (bf16) or 512 (f32).
 __device__ __forceinline__ void gemv_dma16(const void *g, uint8_t *lds) {
     __builtin_amdgcn_global_load_lds(g, (gemv_lds_t *)(lds), 16, 0, 0);
 }
 
 template <int KB>
 __device__ __forceinline__ int wswz(int row, int chunk) {
-    if constexpr (KB == 128) return chunk ^ ((row >> 1) & 7);
+    if constexpr (KB == 64) return chunk ^ ((row >> 2) & 3);
+    else if constexpr (KB == 128) return chunk ^ ((row >> 1) & 7);
     else return chunk ^ (row & 15);
 }
 
-// Element offset (within a 128-wide K block) of a lane's 16-byte weight load number c.
-template <int WT> __device__ __forceinline__ int wofs(int c, int q) {
-    if constexpr (WT == FT_DT_F32) return c * 16 + q * 4;
-    else if constexpr (WT == FT_DT_BF16) return c * 32 + q * 8;
-    else return c * 64 + q * 16;
-}
+// Byte offset (within a row's 128-wide K block) of a lane's 16-byte weight load number c: the
+// K values it holds are c * 16 + q * 4 (f32, 4 values), c * 32 + q * 8 (bf16, 8), c * 64 + q * 16
+// (fp8, 16) and q * 32 (MXFP4, 32), i.e. chunk 4 c + q of the row's block.
+template <int WT> __device__ __forceinline__ int wbyte(int c, int q) { return (4 * c + q) * 16; }
 
 // Activation loads of one 128-wide K block for one 16-row M tile, 16 bytes each, at the K
 // offsets the lane's weight operand uses (f32: 8 x 4 floats at c*16 + q*4; bf16: 4 x 8 at
-// c*32 + q*8; fp8 weights widened to bf16: 4 x 8 at (c/2)*64 + q*16 + (c%2)*8).  `a_row` points
+// c*32 + q*8; fp8 weights widened to bf16: 4 x 8 at (c/2)*64 + q*16 + (c%2)*8; MXFP4 widened to
+// bf16: 4 x 8 at q*32 + c*8).  `a_row` points
 // at this lane's activation row offset to the K block; padding rows point at a real row and
 // their results are never stored, so the loads need no branch.
 template <int WT> struct ALd { static constexpr int n = WT == FT_DT_F32 ? 8 : 4; };
@@ -105,6 +116,7 @@ __device__ __forceinline__ void aload(u32x4_t (&dst)[ALd<WT>::n], const uint8_t 
         int ofs;
         if constexpr (WT == FT_DT_F32) ofs = (c * 16 + q * 4) * 4;
         else if constexpr (WT == FT_DT_BF16) ofs = (c * 32 + q * 8) * 2;
+        else if constexpr (WT == FT_DT_MXFP4) ofs = (q * 32 + c * 8) * 2;
         else ofs = ((c >> 1) * 64 + q * 16 + (c & 1) * 8) * 2;
         dst[c] = ld16(a_row + ofs);
     }
@@ -136,7 +148,7 @@ template <int WT, int EPI, int NB>
 __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int tiles) {
     constexpr int D = WTr<WT>::kBatch, NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
     constexpr int COLS = NB * 16;
-    constexpr int KB = 128 * WTr<WT>::kElem;                  // bytes of one row's K block
+    constexpr int KB = WTr<WT>::kBlock;                        // bytes of one row's K block
     constexpr int STAGE = FT_GEMV_LDS ? D * NB * 16 * KB : 0; // per wave
     constexpr int RED = kGemvWaves * 16 * (COLS + 1) * 4;
     // the per-wave staging areas and the cross-wave reduction are disjoint: a wave writes its
@@ -162,18 +174,24 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
     const int nkb = K / 128;
     // weight row of this lane's N column in block b: a gate/up block pairs 8 gate rows with the
     // 8 matching up rows, so SiLU(gate) * up of one h column stays inside the block
+    const size_t row_bytes = static_cast<size_t>(nkb) * KB;
     const uint8_t *wbase[NB];
-    const float *sbase[NB];
+    const float *sbase[NB];      // fp8: the row's 128 x 128 block scales
+    const uint32_t *xbase[NB];   // MXFP4: the row's e8m0 scales, one 32-bit word per K block
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
         const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
         const int wrow = EPI == EPI_GATEUP ? (n < 8 ? col0 + n : I + col0 + n - 8) : col0 + n;
         wbase[b] = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.w13 : a.w2) +
-                   (static_cast<size_t>(slot) * nrows + wrow) * static_cast<size_t>(K) * WTr<WT>::kElem;
+                   (static_cast<size_t>(slot) * nrows + wrow) * row_bytes;
         sbase[b] = nullptr;
+        xbase[b] = nullptr;
         if constexpr (WT == FT_DT_FP8E4M3FN_B128)
-            sbase[b] = (EPI == EPI_GATEUP ? a.s13 : a.s2) +
+            sbase[b] = static_cast<const float *>(EPI == EPI_GATEUP ? a.s13 : a.s2) +
                        (static_cast<size_t>(slot) * (nrows / 128) + wrow / 128) * nkb;
+        if constexpr (WT == FT_DT_MXFP4)
+            xbase[b] = static_cast<const uint32_t *>(EPI == EPI_GATEUP ? a.s13 : a.s2) +
+                       (static_cast<size_t>(slot) * nrows + wrow) * nkb;
     }
     // global_load_lds sources: instruction c of block b covers rows [c * RPI, c * RPI + RPI) of
     // the block's 16, LPR lanes per row; lane i fills LDS chunk i % LPR of its row, so it fetches
@@ -190,8 +208,7 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                 const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
                 const int wr = EPI == EPI_GATEUP ? (j < 8 ? col0 + j : I + col0 + j - 8) : col0 + j;
                 dsrc[b][c] = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.w13 : a.w2) +
-                             (static_cast<size_t>(slot) * nrows + wr) * static_cast<size_t>(K) * WTr<WT>::kElem +
-                             wswz<KB>(j, lane % LPR) * 16;
+                             (static_cast<size_t>(slot) * nrows + wr) * row_bytes + wswz<KB>(j, lane % LPR) * 16;
             }
     }
     uint8_t *wst = s_lds + wave * STAGE;
@@ -222,6 +239,7 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
             u32x4_t av[D][MT][NA];
             u32x4_t wv[D][NB][NL];
             float sv[D][NB];
+            uint32_t xv[D][NB];
 #pragma unroll
             for (int d = 0; d < D; ++d) {
                 const int kb = min(kbb + d, kb1 - 1);
@@ -236,11 +254,12 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                             gemv_dma16(dsrc[b][c] + static_cast<size_t>(kb) * KB,
                                        wst + ((d * NB + b) * 16 * KB + c * 1024));
                         } else {
-                            const uint8_t *p = wbase[b] + static_cast<size_t>(kb * 128 + wofs<WT>(c, q)) * WTr<WT>::kElem;
+                            const uint8_t *p = wbase[b] + static_cast<size_t>(kb) * KB + wbyte<WT>(c, q);
                             wv[d][b][c] = FT_GEMV_NT_LOADS ? ld16_stream(p) : ld16(p);
                         }
                     }
                     if constexpr (WT == FT_DT_FP8E4M3FN_B128) sv[d][b] = sbase[b][kb];
+                    if constexpr (WT == FT_DT_MXFP4) xv[d][b] = xbase[b][kb];
                 }
             }
             if constexpr (FT_GEMV_LDS) {
@@ -270,11 +289,17 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                         wc[2] = fp8x8_to_bf16x8(wv[d][b][1][0], wv[d][b][1][1]);
                         wc[3] = fp8x8_to_bf16x8(wv[d][b][1][2], wv[d][b][1][3]);
                     }
+                    if constexpr (WT == FT_DT_MXFP4) {
+                        // the lane's 32 codes share the scale of its 32-value run q
+                        const float xs = e8m0_to_f32((xv[d][b] >> (8 * q)) & 0xFF);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) wc[i] = fp4x8_scaled_to_bf16x8(wv[d][b][0][i], xs);
+                    }
                     const float sc = keep * (WT == FT_DT_FP8E4M3FN_B128 ? sv[d][b] : 1.f);
 #pragma unroll
                     for (int mt = 0; mt < MT; ++mt) {
                         floatx4_t part{0.f, 0.f, 0.f, 0.f};
-                        if constexpr (WT == FT_DT_FP8E4M3FN_B128) mfma_kblock<WT>(av[d][mt], wc, part);
+                        if constexpr (WT == FT_DT_FP8E4M3FN_B128 || WT == FT_DT_MXFP4) mfma_kblock<WT>(av[d][mt], wc, part);
                         else mfma_kblock<WT>(av[d][mt], wv[d][b], part);
 #pragma unroll
                         for (int i = 0; i < 4; ++i) acc[mt][b][i] += sc * part[i];
@@ -355,7 +380,7 @@ __global__ __launch_bounds__(256) void zero_out(float *out, size_t n4) {
 
 template <int WT, int EPI>
 static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
-    constexpr int NB = WT == FT_DT_FP8E4M3FN_B128 ? FT_GEMV_NB_FP8 : FT_GEMV_NB;
+    constexpr int NB = gemv_nb<WT>();
     const int tiles = EPI == EPI_GATEUP ? a.I / (8 * NB) : a.H / (16 * NB);
     hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
                        s, a, tiles);
@@ -389,6 +414,8 @@ hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof) 
         case FT_DT_BF16:
             if (gemm_path(a)) return launch_gemm(a, s, prof);
             return launch_stream_path<FT_DT_BF16>(a, s, prof);
+        case FT_DT_MXFP4:
+            return launch_stream_path<FT_DT_MXFP4>(a, s, prof);
         default:
             if (gemm_path(a)) return launch_gemm(a, s, prof);
             return launch_stream_path<FT_DT_FP8E4M3FN_B128>(a, s, prof);

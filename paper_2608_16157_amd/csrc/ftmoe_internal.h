@@ -69,8 +69,8 @@ struct RouteArgs {
 struct ExpertArgs {
     const void *w13;
     const void *w2;
-    const float *s13;
-    const float *s2;
+    const void *s13;   // float32 block scales (fp8) or uint8 e8m0 scales (MXFP4)
+    const void *s2;
     const void *x;
     float *out;
     int T, H, I, k, w_dtype, n_slots, shared;
@@ -157,6 +157,20 @@ struct FillArgs {
 hipError_t launch_cache_fill(const FillArgs &a, int max_fill, hipStream_t s);
 hipError_t launch_add_partial(float *out, const float *other, size_t n, hipStream_t s);
 
+// Bytes of one expert in each bank (w13, w2, s13, s2) for a weight dtype; H, I multiples of 128.
+struct ExpertBytes {
+    size_t w13, w2, s13, s2;
+};
+inline ExpertBytes expert_bytes(int w_dtype, size_t H, size_t I) {
+    switch (w_dtype) {
+        case FT_DT_F32: return {2 * I * H * 4, H * I * 4, 0, 0};
+        case FT_DT_BF16: return {2 * I * H * 2, H * I * 2, 0, 0};
+        case FT_DT_FP8E4M3FN_B128: return {2 * I * H, H * I, (2 * I / 128) * (H / 128) * 4, (H / 128) * (I / 128) * 4};
+        default: return {I * H, H * I / 2, 2 * I * (H / 32), H * (I / 32)};   // MXFP4
+    }
+}
+inline bool has_scales(int w_dtype) { return w_dtype == FT_DT_FP8E4M3FN_B128 || w_dtype == FT_DT_MXFP4; }
+
 // Every host-checkable condition of ft_moe_forward (FT_OK when the call would be enqueued).
 ft_status_t check_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
                           const int32_t *slot_table, const void *x, int32_t T, const float *out_partial,
@@ -165,12 +179,12 @@ ft_status_t check_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, co
 // CPU branch of a layer step (host_experts.cpp).
 struct CpuBank {
     const void *w;       // one expert's matrix, row-major
-    const float *s;      // its fp8 block scales, or null
+    const void *s;       // its fp8 block scales (float32) or MXFP4 scales (uint8), or null
 };
 struct CpuExpertArgs {
     int E, H, I, k, T, w_dtype, x_dtype, n_list, n_threads;
     const void *w13, *w2;            // host expert pool, [E][2I][H] and [E][H][I]
-    const float *s13, *s2;           // fp8 block scales per expert, or null
+    const void *s13, *s2;            // fp8 / MXFP4 scales per expert, or null
     const void *x;                   // [T][H]
     const int32_t *topk_ids;         // [T][k]
     const float *topk_w;             // [T][k]

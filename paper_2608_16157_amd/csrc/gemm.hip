@@ -254,7 +254,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
     // block for down), one per 128-wide K block, staged in LDS before the pipeline starts: a
     // vector load inside the loop would make the compiler drain the DMA stages
     if constexpr (kFp8) {
-        const float *s = EPI == GEMM_GATEUP ? a.s13 : a.s2;
+        const float *s = static_cast<const float *>(EPI == GEMM_GATEUP ? a.s13 : a.s2);
         for (int idx = t; idx < kWavesN * 2 * nkb; idx += kGemmThreads) {
             const int w = idx / (2 * nkb), which = (idx / nkb) & 1, kb = idx % nkb;
             int r;

@@ -12,8 +12,8 @@
 //   down   : items of 32 output columns: out[t][c] += gate * (W2[c] . h), experts in list order,
 //            so every output element is summed in a fixed order (the result does not depend on
 //            the thread count or timing).
-// Weights are decoded exactly (bf16 by widening, fp8 e4m3fn from the format definition times
-// the block scale) and every product accumulates in float32.  All code in this file is
+// Weights are decoded exactly (bf16 by widening, fp8 e4m3fn and MXFP4 e2m1 from the format
+// definitions times their scales) and every product accumulates in float32.  All code in this file is
 // compiled for AVX2 + FMA; the entry point checks the CPU supports them before calling in.
 #include <atomic>
 #include <cmath>
@@ -48,6 +48,27 @@ struct Fp8Table {
     }
 };
 
+// e2m1: 1 sign bit, 2 exponent bits (bias 1), 1 mantissa bit; exponent field 0 encodes m/2.
+float e2m1_to_float(uint8_t code) {
+    const int e = (code >> 1) & 3, m = code & 1;
+    const float v = e == 0 ? 0.5f * m : std::ldexp(1.0f + 0.5f * m, e - 1);
+    return code & 8 ? -v : v;
+}
+
+// Both codes of every byte decoded at once: entry b = (element of the low nibble, of the high).
+struct Fp4PairTable {
+    float v[256][2];
+    Fp4PairTable() {
+        for (int b = 0; b < 256; ++b) {
+            v[b][0] = e2m1_to_float(static_cast<uint8_t>(b & 15));
+            v[b][1] = e2m1_to_float(static_cast<uint8_t>(b >> 4));
+        }
+    }
+};
+
+// e8m0 scale: 2^(s - 127), 255 is NaN.
+float e8m0_to_float(uint8_t s) { return s == 255 ? NAN : std::ldexp(1.0f, static_cast<int>(s) - 127); }
+
 float bf16_to_float(uint16_t b) {
     const uint32_t u = static_cast<uint32_t>(b) << 16;
     float f;
@@ -62,10 +83,21 @@ void decode_row(const CpuBank &bank, int w_dtype, int nrows, int K, int r, float
     } else if (w_dtype == FT_DT_BF16) {
         const uint16_t *src = static_cast<const uint16_t *>(bank.w) + static_cast<size_t>(r) * K;
         for (int c = 0; c < K; ++c) dst[c] = bf16_to_float(src[c]);
+    } else if (w_dtype == FT_DT_MXFP4) {
+        static const Fp4PairTable pairs;
+        const uint8_t *src = static_cast<const uint8_t *>(bank.w) + static_cast<size_t>(r) * (K / 2);
+        const uint8_t *sc = static_cast<const uint8_t *>(bank.s) + static_cast<size_t>(r) * (K / 32);
+        for (int cb = 0; cb < K / 32; ++cb) {
+            const float s = e8m0_to_float(sc[cb]);
+            for (int j = cb * 16; j < cb * 16 + 16; ++j) {
+                dst[2 * j] = pairs.v[src[j]][0] * s;
+                dst[2 * j + 1] = pairs.v[src[j]][1] * s;
+            }
+        }
     } else {
         static const Fp8Table table;
         const uint8_t *src = static_cast<const uint8_t *>(bank.w) + static_cast<size_t>(r) * K;
-        const float *sc = bank.s + static_cast<size_t>(r / 128) * (K / 128);
+        const float *sc = static_cast<const float *>(bank.s) + static_cast<size_t>(r / 128) * (K / 128);
         for (int cb = 0; cb < K / 128; ++cb) {
             const float s = sc[cb];
             for (int c = cb * 128; c < cb * 128 + 128; ++c) dst[c] = table.v[src[c]] * s;
@@ -102,8 +134,7 @@ void run_items(int n_items, int n_threads, F &&fn) {
 
 void cpu_experts(const CpuExpertArgs &a) {
     const int H = a.H, I = a.I, k = a.k, T = a.T;
-    const size_t w13_rows = 2 * static_cast<size_t>(I), w2_rows = H;
-    const size_t wb = a.w_dtype == FT_DT_F32 ? 4 : (a.w_dtype == FT_DT_BF16 ? 2 : 1);
+    const ExpertBytes eb = expert_bytes(a.w_dtype, H, I);
     // tokens and gates of every listed expert, in token order
     std::vector<std::vector<int>> toks(a.n_list);
     std::vector<std::vector<float>> gates(a.n_list);
@@ -126,14 +157,14 @@ void cpu_experts(const CpuExpertArgs &a) {
 
     auto bank13 = [&](int e) {
         CpuBank b;
-        b.w = static_cast<const uint8_t *>(a.w13) + static_cast<size_t>(e) * w13_rows * H * wb;
-        b.s = a.s13 ? a.s13 + static_cast<size_t>(e) * (w13_rows / 128) * (H / 128) : nullptr;
+        b.w = static_cast<const uint8_t *>(a.w13) + static_cast<size_t>(e) * eb.w13;
+        b.s = a.s13 ? static_cast<const uint8_t *>(a.s13) + static_cast<size_t>(e) * eb.s13 : nullptr;
         return b;
     };
     auto bank2 = [&](int e) {
         CpuBank b;
-        b.w = static_cast<const uint8_t *>(a.w2) + static_cast<size_t>(e) * w2_rows * I * wb;
-        b.s = a.s2 ? a.s2 + static_cast<size_t>(e) * (w2_rows / 128) * (I / 128) : nullptr;
+        b.w = static_cast<const uint8_t *>(a.w2) + static_cast<size_t>(e) * eb.w2;
+        b.s = a.s2 ? static_cast<const uint8_t *>(a.s2) + static_cast<size_t>(e) * eb.s2 : nullptr;
         return b;
     };
 

@@ -48,14 +48,12 @@ extern "C" ft_status_t ft_prefill_layers(const ft_moe_desc_t *desc, int32_t n_la
     if (overlap && (!copy_stream || copy_stream == stream)) return FT_ERR_SHAPE;
     if (ft_moe_workspace_bytes(desc, 1) == 0) return FT_ERR_SHAPE;
     if (n_layers == 0 || T == 0) return FT_OK;
-    const bool fp8 = desc->w_dtype == FT_DT_FP8E4M3FN_B128;
-    const size_t H = desc->hidden, I = desc->inter, S = desc->n_slots > 0 ? desc->n_slots : 0;
-    const size_t wb = desc->w_dtype == FT_DT_F32 ? 4 : (desc->w_dtype == FT_DT_BF16 ? 2 : 1);
+    const size_t S = desc->n_slots > 0 ? desc->n_slots : 0;
     // bytes of one complete bank (all n_slots rows) of each tensor
-    const size_t bank[4] = {S * 2 * I * H * wb, S * H * I * wb, fp8 ? S * (2 * I / 128) * (H / 128) * 4 : 0,
-                            fp8 ? S * (H / 128) * (I / 128) * 4 : 0};
+    const ftmoe::ExpertBytes eb = ftmoe::expert_bytes(desc->w_dtype, desc->hidden, desc->inter);
+    const size_t bank[4] = {S * eb.w13, S * eb.w2, S * eb.s13, S * eb.s2};
     auto ptrs = [](const ft_banks_t &b, int i) -> const void * {
-        return i == 0 ? b.w13 : i == 1 ? b.w2 : i == 2 ? static_cast<const void *>(b.s13) : b.s2;
+        return i == 0 ? b.w13 : i == 1 ? b.w2 : i == 2 ? b.s13 : b.s2;
     };
     for (int i = 0; i < 4; ++i) {
         if (!bank[i]) continue;

@@ -12,7 +12,7 @@ import paper_2608_16157_amd as ftm
 import workloads
 from tests._util import to_np_bits
 
-TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2}
+TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2, workloads.DT_MXFP4: 1e-2}
 
 
 def _pool_case(seed, wdt, gating, E, k, T, H, I):
@@ -32,6 +32,8 @@ CASES = [
     (2, workloads.DT_BF16, 0, 12, 3, 1, 384, 256, 0),
     (3, workloads.DT_FP8, 1, 10, 4, 6, 256, 384, 4),
     (4, workloads.DT_FP8, 0, 6, 6, 3, 128, 128, 2),
+    (5, workloads.DT_MXFP4, 1, 10, 3, 4, 256, 384, 3),
+    (6, workloads.DT_MXFP4, 0, 6, 6, 2, 128, 128, 0),
 ]
 
 

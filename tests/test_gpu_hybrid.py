@@ -17,7 +17,7 @@ from tests._util import to_np_bits
 
 pytestmark = pytest.mark.gpu
 
-TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2}
+TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2, workloads.DT_MXFP4: 1e-2}
 
 
 def _say(msg):
@@ -31,11 +31,11 @@ class Setup:
         lay = workloads.random_layer(seed, hidden=H, inter=I, n_experts=E, top_k=k, tokens=T,
                                      gating=gating, w_dtype=wdt, n_resident=E, shared=shared)
         st = lay.slot_table.long()
-        fp8 = wdt == workloads.DT_FP8
+        scaled = lay.s13 is not None
         self.pool = {"w13": lay.w13[st].contiguous().pin_memory(),
                      "w2": lay.w2[st].contiguous().pin_memory(),
-                     "s13": lay.s13[st].contiguous().pin_memory() if fp8 else None,
-                     "s2": lay.s2[st].contiguous().pin_memory() if fp8 else None}
+                     "s13": lay.s13[st].contiguous().pin_memory() if scaled else None,
+                     "s2": lay.s2[st].contiguous().pin_memory() if scaled else None}
         self.E, self.R, self.k, self.T, self.H, self.I, self.K = E, R, k, T, H, I, K
         self.wdt, self.shared = wdt, shared
         n_slots = R + (1 if shared else 0)
@@ -104,6 +104,7 @@ CASES = [
     (1, workloads.DT_FP8, 1, 20, 6, 4, 2, 256, 384, True, 3, (52.7, 77.3)),
     (2, workloads.DT_F32, 0, 8, 3, 2, 4, 128, 128, False, 2, (6.0, 5.0)),
     (3, workloads.DT_BF16, 1, 24, 8, 6, 5, 384, 256, True, 8, (25.1, 63.2)),
+    (4, workloads.DT_MXFP4, 1, 20, 6, 4, 3, 256, 384, False, 4, (55.5, 44.9)),
 ]
 
 

@@ -1,8 +1,10 @@
 """GPU parity: the HIP path through the C ABI against the CPU oracle, on the same seeded inputs.
 
 Lists, ids, slots, offsets and counts must be bit-exact; gates within 2e-6; layer outputs
-within the max-relative-error bound (row-RMS floor) of 1e-3 for fp32 weights, 1e-2 for bf16
-and 3e-2 for fp8 weights, and rows the oracle makes exactly zero must be exactly zero.
+within the max-relative-error bound (row-RMS floor) of 1e-3 for fp32 weights, 1e-2 for bf16,
+3e-2 for fp8 and 1e-2 for MXFP4 weights (every MXFP4 weight times its scale is exact in bf16, so
+that path has the bf16 path's arithmetic), and rows the oracle makes exactly zero must be exactly
+zero.
 """
 import numpy as np
 import pytest
@@ -15,7 +17,7 @@ from tests._util import oracle_inputs
 
 pytestmark = pytest.mark.gpu
 
-TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2}
+TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2, workloads.DT_MXFP4: 1e-2}
 
 
 def _say(*a):
@@ -73,7 +75,8 @@ def check_output(out, ref, w_dtype, rows=None):
 
 ROUTE_CASES = [("tiny", 16), ("qwen3_decode", 1), ("qwen3_decode", 8), ("qwen3_decode", 32),
                ("dsv3_decode", 1), ("dsv3_decode", 16), ("dsv3_decode", 64),
-               ("qwen3_prefill", 4096), ("dsv3_prefill", 8192), ("qwen3_decode", 300)]
+               ("qwen3_prefill", 4096), ("dsv3_prefill", 8192), ("qwen3_decode", 300),
+               ("dsv4flash_decode", 64)]
 
 
 def _route_only_layer(name, T):
@@ -134,7 +137,8 @@ def test_invalid_slot_tables_flagged_and_treated_as_misses(T):
 # ------------------------------------------------------------------ whole layer
 
 @pytest.mark.parametrize("name,T", [("tiny", 16), ("qwen3_decode", 1), ("qwen3_decode", 8),
-                                    ("qwen3_decode", 32), ("dsv3_decode", 1), ("dsv3_decode", 16)])
+                                    ("qwen3_decode", 32), ("dsv3_decode", 1), ("dsv3_decode", 16),
+                                    ("dsv4flash_decode", 1), ("dsv4flash_decode", 16)])
 def test_forward_configs_full(name, T):
     _say(f"forward {name} T={T}")
     lay = workloads.make_layer(name, T, device="cuda")
@@ -146,7 +150,9 @@ def test_forward_configs_full(name, T):
 
 @pytest.mark.parametrize("name,T,rows", [("dsv3_decode", 64, [0, 13, 63]),
                                          ("qwen3_prefill", 4096, list(range(0, 4096, 97)) + [4095]),
-                                         ("dsv3_prefill", 8192, [0, 1023, 1024, 3000, 8191])])
+                                         ("dsv3_prefill", 8192, [0, 1023, 1024, 3000, 8191]),
+                                         ("dsv4flash_decode", 64, [0, 31, 63]),
+                                         ("dsv4flash_prefill", 8192, [0, 1023, 1024, 5000, 8191])])
 def test_forward_configs_sampled(name, T, rows):
     _say(f"forward {name} T={T} sampled rows {rows}")
     lay = workloads.make_layer(name, T, device="cuda")
@@ -175,6 +181,12 @@ RANDOM_FWD = [
     (13, workloads.DT_BF16, 0, 16, 4, 700, 11, False, 512, 256, 1.0),
     (14, workloads.DT_FP8, 1, 32, 8, 520, 13, True, 512, 384, 2.0),
     (15, workloads.DT_BF16, 1, 8, 8, 260, 8, True, 768, 128, 0.0),
+    # MXFP4 weights: streaming and many-token shapes, ragged groups, shared expert, no residency
+    (16, workloads.DT_MXFP4, 1, 16, 4, 37, 10, True, 256, 384, 0.0),
+    (17, workloads.DT_MXFP4, 0, 8, 2, 5, 8, False, 128, 128, 0.0),
+    (18, workloads.DT_MXFP4, 0, 24, 6, 300, 14, True, 384, 256, 1.2),
+    (19, workloads.DT_MXFP4, 1, 12, 3, 70, 0, True, 256, 256, 0.0),
+    (20, workloads.DT_MXFP4, 0, 32, 8, 520, 13, False, 512, 384, 2.0),
 ]
 
 

@@ -16,7 +16,7 @@ from tests._util import to_np_bits
 
 pytestmark = pytest.mark.gpu
 
-TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2}
+TOL = {workloads.DT_F32: 1e-3, workloads.DT_BF16: 1e-2, workloads.DT_FP8: 3e-2, workloads.DT_MXFP4: 1e-2}
 BANKS = ("w13", "w2", "s13", "s2")
 
 
@@ -89,6 +89,8 @@ CASES = [
     (2, workloads.DT_F32, 0, 8, 2, 20, 128, 128, False, 2),
     (3, workloads.DT_FP8, 1, 20, 4, 260, 384, 256, True, 3),       # MFMA path, fp8, shared
     (4, workloads.DT_BF16, 0, 8, 2, 17, 128, 256, False, 1),       # a single layer
+    (5, workloads.DT_MXFP4, 1, 12, 3, 30, 256, 384, False, 3),     # MXFP4, GEMV path
+    (6, workloads.DT_MXFP4, 0, 16, 4, 280, 256, 256, False, 2),    # MXFP4, many tokens
 ]
 
 
