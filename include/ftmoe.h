@@ -96,10 +96,11 @@ typedef struct {
  *   w2  [n_slots][H][I]   down projection
  *   s13 [n_slots][2I/128][H/128], s2 [n_slots][H/128][I/128]  float32 block scales (fp8,
  *       NULL for f32 and bf16): weight (r, c) = code(r, c) * scale(r/128, c/128).
- * MXFP4 packs two codes per byte along each row and keeps byte scales per 32 elements:
+ * MXFP4 packs two codes per byte along each row and keeps byte scales per 32 elements of a row,
+ * stored run-major so that the scales of one 32-wide K run of consecutive rows are contiguous:
  *   w13 [n_slots][2I][H/2], w2 [n_slots][H][I/2]  uint8 code pairs
- *   s13 [n_slots][2I][H/32], s2 [n_slots][H][I/32]  uint8 e8m0 scales:
- *       weight (r, c) = e2m1(code(r, c)) * 2^(s(r, c/32) - 127)
+ *   s13 [n_slots][H/32][2I], s2 [n_slots][I/32][H]  uint8 e8m0 scales:
+ *       weight (r, c) = e2m1(code(r, c)) * 2^(s(c/32, r) - 127)
  */
 typedef struct {
     const void *w13;
@@ -172,7 +173,8 @@ ft_status_t ft_route_only(const ft_moe_desc_t *desc, const float *logits, const 
  *               expert) gets exact zeros.  The gate-weighted expert outputs are summed with
  *               float32 atomic adds, so the order of that sum (and the last bits) may differ
  *               between calls; the routing outputs are bit-reproducible.
- *   x, out_partial, banks->w13 and banks->w2 must be 16-byte aligned (FT_ERR_SHAPE otherwise).
+ *   x, out_partial, banks->w13 and banks->w2 (and for MXFP4 banks->s13 and banks->s2) must be
+ *   16-byte aligned (FT_ERR_SHAPE otherwise).
  */
 ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
                            const int32_t *slot_table, const void *x, int32_t T,

@@ -106,14 +106,15 @@ E8M0_TABLE = np.array([e8m0_value(c) for c in range(256)], dtype=np.float64)
 def mxfp4_to_f64(packed: np.ndarray, scales: np.ndarray) -> np.ndarray:
     """Dequantise an MXFP4 matrix: packed [R][C/2] bytes holding E2M1 codes, element 2j in the
     low nibble of byte j and element 2j+1 in the high nibble, with one E8M0 scale per 32
-    consecutive elements of a row (scales [R][C/32])."""
+    consecutive elements of a row, stored run-major: scales [C/32][R], element (r, c) scaled by
+    scales[c // 32][r]."""
     b = np.ascontiguousarray(packed).view(np.uint8)
     r, half = b.shape
     codes = np.empty((r, 2 * half), dtype=np.uint8)
     codes[:, 0::2] = b & 0xF
     codes[:, 1::2] = b >> 4
     v = E2M1_TABLE[codes]
-    s = np.repeat(E8M0_TABLE[np.ascontiguousarray(scales).view(np.uint8)], 32, axis=1)
+    s = np.repeat(E8M0_TABLE[np.ascontiguousarray(scales).view(np.uint8)].T, 32, axis=1)
     assert s.shape == v.shape
     return v * s
 
@@ -261,7 +262,7 @@ def moe_partial(desc: dict, banks: dict, logits, slot_table, x, tokens=None):
     desc   : hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot
     banks  : w13 [n_slots][2I][H], w2 [n_slots][H][I] (float32 arrays, bf16 bit patterns as
              uint16, fp8 codes as uint8, or MXFP4 code pairs as uint8 [..][K/2]) and for fp8 s13, s2
-             float32 block scales, for MXFP4 uint8 E8M0 scales [..][K/32]
+             float32 block scales, for MXFP4 uint8 E8M0 scales [..][K/32][rows]
     logits : [T][E] float32; slot_table : [E] int32; x : [T][H] (float32 or bf16 bits as uint16)
     tokens : optional list of token indices; only those rows are evaluated (others stay 0)
 

@@ -105,6 +105,9 @@ ft_status_t check_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, co
     if (!x || !out_partial) return FT_ERR_NULL;
     if (desc->n_slots > 0 && (!banks->w13 || !banks->w2)) return FT_ERR_NULL;
     if (has_scales(desc->w_dtype) && desc->n_slots > 0 && (!banks->s13 || !banks->s2)) return FT_ERR_NULL;
+    if (desc->w_dtype == FT_DT_MXFP4 &&
+        (reinterpret_cast<uintptr_t>(banks->s13) | reinterpret_cast<uintptr_t>(banks->s2)) % 16)
+        return FT_ERR_SHAPE;
     const uintptr_t al = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(out_partial) |
                          reinterpret_cast<uintptr_t>(banks->w13) | reinterpret_cast<uintptr_t>(banks->w2);
     if (al % 16) return FT_ERR_SHAPE;

@@ -177,7 +177,7 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
     const size_t row_bytes = static_cast<size_t>(nkb) * KB;
     const uint8_t *wbase[NB];
     const float *sbase[NB];      // fp8: the row's 128 x 128 block scales
-    const uint32_t *xbase[NB];   // MXFP4: the row's e8m0 scales, one 32-bit word per K block
+    const uint8_t *xbase[NB];    // MXFP4: this lane's e8m0 scale of the row in K block 0
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
         const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
@@ -189,9 +189,9 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
         if constexpr (WT == FT_DT_FP8E4M3FN_B128)
             sbase[b] = static_cast<const float *>(EPI == EPI_GATEUP ? a.s13 : a.s2) +
                        (static_cast<size_t>(slot) * (nrows / 128) + wrow / 128) * nkb;
-        if constexpr (WT == FT_DT_MXFP4)
-            xbase[b] = static_cast<const uint32_t *>(EPI == EPI_GATEUP ? a.s13 : a.s2) +
-                       (static_cast<size_t>(slot) * nrows + wrow) * nkb;
+        if constexpr (WT == FT_DT_MXFP4)   // run-major scales: run 4 kb + q of row wrow
+            xbase[b] = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.s13 : a.s2) +
+                       (static_cast<size_t>(slot) * (K / 32) + q) * nrows + wrow;
     }
     // global_load_lds sources: instruction c of block b covers rows [c * RPI, c * RPI + RPI) of
     // the block's 16, LPR lanes per row; lane i fills LDS chunk i % LPR of its row, so it fetches
@@ -259,7 +259,7 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                         }
                     }
                     if constexpr (WT == FT_DT_FP8E4M3FN_B128) sv[d][b] = sbase[b][kb];
-                    if constexpr (WT == FT_DT_MXFP4) xv[d][b] = xbase[b][kb];
+                    if constexpr (WT == FT_DT_MXFP4) xv[d][b] = xbase[b][static_cast<size_t>(kb) * 4 * nrows];
                 }
             }
             if constexpr (FT_GEMV_LDS) {
@@ -291,7 +291,7 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                     }
                     if constexpr (WT == FT_DT_MXFP4) {
                         // the lane's 32 codes share the scale of its 32-value run q
-                        const float xs = e8m0_to_f32((xv[d][b] >> (8 * q)) & 0xFF);
+                        const float xs = e8m0_to_f32(xv[d][b]);
 #pragma unroll
                         for (int i = 0; i < 4; ++i) wc[i] = fp4x8_scaled_to_bf16x8(wv[d][b][0][i], xs);
                     }
@@ -415,6 +415,7 @@ hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof) 
             if (gemm_path(a)) return launch_gemm(a, s, prof);
             return launch_stream_path<FT_DT_BF16>(a, s, prof);
         case FT_DT_MXFP4:
+            if (gemm_path(a)) return launch_gemm(a, s, prof);
             return launch_stream_path<FT_DT_MXFP4>(a, s, prof);
         default:
             if (gemm_path(a)) return launch_gemm(a, s, prof);

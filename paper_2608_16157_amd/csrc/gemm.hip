@@ -74,10 +74,15 @@ enum { GEMM_GATEUP = 0, GEMM_DOWN = 1 };
 #endif
 template <int WT> struct GTr;
 template <> struct GTr<FT_DT_BF16> {
-    static constexpr int BK = FT_GEMM_BF16_BK, NS = FT_GEMM_BF16_NS, kWb = 2;
+    static constexpr int BK = FT_GEMM_BF16_BK, NS = FT_GEMM_BF16_NS, BRB = 2 * BK;
 };
 template <> struct GTr<FT_DT_FP8E4M3FN_B128> {
-    static constexpr int BK = FT_GEMM_FP8_BK, NS = FT_GEMM_FP8_NS, kWb = 1;
+    static constexpr int BK = FT_GEMM_FP8_BK, NS = FT_GEMM_FP8_NS, BRB = BK;
+};
+// MXFP4: 64 K values (32 code bytes) per weight row and stage, so that one lane's 16-byte chunk
+// of a row is a whole 32-value scale run
+template <> struct GTr<FT_DT_MXFP4> {
+    static constexpr int BK = 64, NS = 3, BRB = BK / 2;
 };
 
 template <int V> using ic = std::integral_constant<int, V>;
@@ -135,16 +140,24 @@ __device__ __forceinline__ void dma16(const void *g, uint8_t *lds_block) {
     __builtin_amdgcn_global_load_lds(g, (lds_void_t *)(lds_block), 16, 0, 0);
 }
 
+// 4 bytes per lane: lane i writes LDS bytes [4 i, 4 i + 4) of the 256-byte block
+__device__ __forceinline__ void dma4(const void *g, uint8_t *lds_block) {
+    __builtin_amdgcn_global_load_lds(g, (lds_void_t *)(lds_block), 4, 0, 0);
+}
+
 template <int WT, int EPI>
 __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, int ntn) {
     constexpr bool kFp8 = WT == FT_DT_FP8E4M3FN_B128;
+    constexpr bool kFp4 = WT == FT_DT_MXFP4;
     constexpr int BK = GTr<WT>::BK, NS = GTr<WT>::NS;
     constexpr int ARB = BK * 2;                      // A row bytes per stage (bf16)
-    constexpr int BRB = BK * GTr<WT>::kWb;           // B row bytes per stage
+    constexpr int BRB = GTr<WT>::BRB;                // B row bytes per stage
     constexpr int ASTAGE = kBM * ARB, BSTAGE = kBN * BRB;
     constexpr int A_INSTR = ASTAGE / 1024 / kGemmWaves;   // 1 KB DMA instructions per wave
     constexpr int B_INSTR = BSTAGE / 1024 / kGemmWaves;
-    constexpr int PER_STAGE = A_INSTR + B_INSTR;
+    // MXFP4: one more DMA per wave and stage brings a quarter of the stage's e8m0 scales
+    constexpr int PER_STAGE = A_INSTR + B_INSTR + (kFp4 ? 1 : 0);
+    constexpr int XSTAGE = kFp4 ? 1024 : 16;         // LDS per scale stage: 4 waves x 256 bytes
     static_assert(A_INSTR >= 1 && B_INSTR >= 1, "stage too small");
     static_assert(NS >= 2 && NS <= 4, "ring depth");
     static_assert((NS - 1) * PER_STAGE < 64, "vmcnt range");
@@ -156,6 +169,9 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
     __shared__ __attribute__((aligned(1024))) uint8_t sB0[BSTAGE], sB1[BSTAGE];
     __shared__ __attribute__((aligned(1024))) uint8_t sB2[NS > 2 ? BSTAGE : 16];
     __shared__ __attribute__((aligned(1024))) uint8_t sB3[NS > 3 ? BSTAGE : 16];
+    __shared__ __attribute__((aligned(512))) uint8_t sX0[XSTAGE], sX1[XSTAGE];
+    __shared__ __attribute__((aligned(512))) uint8_t sX2[kFp4 && NS > 2 ? XSTAGE : 16];
+    __shared__ __attribute__((aligned(512))) uint8_t sX3[kFp4 && NS > 3 ? XSTAGE : 16];
     constexpr int kMaxKb = 64;                       // K <= 8192
     __shared__ float s_scale[kWavesN][2][kMaxKb];
     __shared__ int32_t s_tok[kBM];
@@ -173,6 +189,13 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
         else if constexpr (S == 1) return sB1;
         else if constexpr (S == 2) return sB2;
         else return sB3;
+    };
+    auto stX = [&](auto s) -> uint8_t * {
+        constexpr int S = decltype(s)::value;
+        if constexpr (S == 0) return sX0;
+        else if constexpr (S == 1) return sX1;
+        else if constexpr (S == 2) return sX2;
+        else return sX3;
     };
 
     const int t = threadIdx.x;
@@ -235,20 +258,44 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
             wrow = nt * kBN + row;
         }
         bsrc[ii] = static_cast<const uint8_t *>(EPI == GEMM_GATEUP ? a.w13 : a.w2) +
-                   (static_cast<size_t>(slot) * nrows + wrow) * K * GTr<WT>::kWb +
+                   (static_cast<size_t>(slot) * nrows + wrow) * static_cast<size_t>(K / BK) * BRB +
                    (swz<BRB>(row, lane % B_CHUNKS) << 4);
     }
-    auto issue = [&](int kt, uint8_t *dA, uint8_t *dB) {
+    const int wm = wave / kWavesN, wn = wave % kWavesN;
+    const int fn = lane & 31, fq = lane >> 5;
+    // MXFP4 scales (run-major in memory: the scales of one 32-wide K run of consecutive weight
+    // rows are contiguous).  A stage covers runs 2 kt and 2 kt + 1 of the tile's 256 weight rows,
+    // which are 4 segments of 128 contiguous bytes (gate/up: the 128 gate rows and the 128 up
+    // rows of the tile; down: two halves of its 256 rows).  Wave w = 2 run + half moves segment
+    // (run, half) with one 4-byte-per-lane DMA into bytes [256 w, 256 w + 128) of the stage;
+    // lanes 32..63 fetch the same segment again into the next 128 bytes, so the instruction has
+    // every lane active and stays in bounds.
+    const uint8_t *xsrc = nullptr;
+    int xcol[kNJ] = {};
+    if constexpr (kFp4) {
+        const int xr = wave >> 1, xh = wave & 1;
+        const int row0 = EPI == GEMM_GATEUP ? (xh ? I : 0) + nt * (kBN / 2) : nt * kBN + xh * (kBN / 2);
+        xsrc = static_cast<const uint8_t *>(EPI == GEMM_GATEUP ? a.s13 : a.s2) +
+               (static_cast<size_t>(slot) * (K / 32) + xr) * nrows + row0 + 4 * (lane & 31);
+        // this lane's scale byte for column tile j, run fq: segment (fq, half) at 256 (2 fq + half)
+#pragma unroll
+        for (int j = 0; j < kNJ; ++j) {
+            const int half = EPI == GEMM_GATEUP ? j : (wn * kWaveCols + j * 32) / (kBN / 2);
+            const int r = EPI == GEMM_GATEUP ? wn * (kWaveCols / 2) + fn : (wn * kWaveCols + j * 32 + fn) % (kBN / 2);
+            xcol[j] = 256 * (2 * fq + half) + r;
+        }
+    }
+    auto issue = [&](int kt, uint8_t *dA, uint8_t *dB, auto ws) {
 #pragma unroll
         for (int ii = 0; ii < A_INSTR; ++ii)
             dma16(asrc[ii] + static_cast<size_t>(kt) * ARB, dA + (wave * A_INSTR + ii) * 1024);
 #pragma unroll
         for (int ii = 0; ii < B_INSTR; ++ii)
             dma16(bsrc[ii] + static_cast<size_t>(kt) * BRB, dB + (wave * B_INSTR + ii) * 1024);
+        if constexpr (kFp4) {
+            dma4(xsrc + static_cast<size_t>(kt) * (BK / 32) * nrows, stX(ws) + wave * 256);
+        }
     };
-
-    const int wm = wave / kWavesN, wn = wave % kWavesN;
-    const int fn = lane & 31, fq = lane >> 5;
     const int nkb = K / 128;
     // fp8 block scales of each wave's columns (gate half and up half of a gate/up tile; one
     // block for down), one per 128-wide K block, staged in LDS before the pipeline starts: a
@@ -297,7 +344,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
         wait_vmcnt<(NS - 2) * PER_STAGE>();
         wait_lgkmcnt0();
         stage_barrier();
-        issue(min(kt + NS - 1, nk - 1), stA(ws), stB(ws));
+        issue(min(kt + NS - 1, nk - 1), stA(ws), stB(ws), ws);
         if (kt < nk) {
             const uint8_t *A = stA(rs);
             const uint8_t *B = stB(rs);
@@ -313,11 +360,15 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
             // sub-step ks takes K [16 ks + 8 kg, +8), i.e. 16-byte chunk 2 ks + kg of both rows.
             // fp8 weights: a lane reads one 16-byte chunk of its weight row, 16 K values, for
             // two sub-steps, so sub-step ks = 2 p + s takes K [32 p + 16 kg + 8 s, +8): weight
-            // chunk 2 p + kg (bytes 8 s ..), activation chunk 4 p + 2 kg + s.
+            // chunk 2 p + kg (bytes 8 s ..), activation chunk 4 p + 2 kg + s.  MXFP4 weights: a
+            // lane reads weight chunk kg, 32 K values under one scale, for all four sub-steps, so
+            // sub-step ks takes K [32 kg + 8 ks, +8): word ks of the chunk, activation chunk
+            // 4 kg + ks.
             u32x4_t b16[kNJ];
+            float xs[kNJ];
 #pragma unroll
             for (int ks = 0; ks < KS; ++ks) {
-                const int ca = kFp8 ? 4 * (ks / 2) + 2 * fq + (ks % 2) : 2 * ks + fq;
+                const int ca = kFp8 ? 4 * (ks / 2) + 2 * fq + (ks % 2) : (kFp4 ? 4 * fq + ks : 2 * ks + fq);
                 u32x4_t af[kMI], bf[kNJ];
 #pragma unroll
                 for (int i = 0; i < ML; ++i) {
@@ -327,7 +378,13 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
 #pragma unroll
                 for (int j = 0; j < kNJ; ++j) {
                     const int rb = wn * kWaveCols + j * 32 + fn;
-                    if constexpr (!kFp8) {
+                    if constexpr (kFp4) {
+                        if (ks == 0) {
+                            b16[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, fq) << 4));
+                            xs[j] = e8m0_to_f32(stX(rs)[xcol[j]]);
+                        }
+                        bf[j] = fp4x8_scaled_to_bf16x8(b16[j][ks], xs[j]);
+                    } else if constexpr (!kFp8) {
                         bf[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, ca) << 4));
                     } else {
                         if (ks % 2 == 0)
@@ -352,7 +409,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
     // barrier publishes the staged scale / token / gate tables
     wait_vmcnt<0>();
     __syncthreads();
-    static_for<0, NS - 1>([&](auto s) { issue(min(decltype(s)::value, nk - 1), stA(s), stB(s)); });
+    static_for<0, NS - 1>([&](auto s) { issue(min(decltype(s)::value, nk - 1), stA(s), stB(s), s); });
     auto mainloop = [&](auto ml) {
         for (int kt = 0; kt < nk; kt += NS) {
             // stage kt + S sits in slot S; its step refills slot (S + NS - 1) mod NS
@@ -427,6 +484,7 @@ static hipError_t launch_gemm_wt(const ExpertArgs &a, hipStream_t s, const Prof 
 
 hipError_t launch_gemm(const ExpertArgs &a, hipStream_t s, const Prof &prof) {
     if (a.w_dtype == FT_DT_BF16) return launch_gemm_wt<FT_DT_BF16>(a, s, prof);
+    if (a.w_dtype == FT_DT_MXFP4) return launch_gemm_wt<FT_DT_MXFP4>(a, s, prof);
     return launch_gemm_wt<FT_DT_FP8E4M3FN_B128>(a, s, prof);
 }
 

@@ -86,9 +86,10 @@ void decode_row(const CpuBank &bank, int w_dtype, int nrows, int K, int r, float
     } else if (w_dtype == FT_DT_MXFP4) {
         static const Fp4PairTable pairs;
         const uint8_t *src = static_cast<const uint8_t *>(bank.w) + static_cast<size_t>(r) * (K / 2);
-        const uint8_t *sc = static_cast<const uint8_t *>(bank.s) + static_cast<size_t>(r) * (K / 32);
+        // scales are run-major: run cb of row r at [cb][r]
+        const uint8_t *sc = static_cast<const uint8_t *>(bank.s) + r;
         for (int cb = 0; cb < K / 32; ++cb) {
-            const float s = e8m0_to_float(sc[cb]);
+            const float s = e8m0_to_float(sc[static_cast<size_t>(cb) * nrows]);
             for (int j = cb * 16; j < cb * 16 + 16; ++j) {
                 dst[2 * j] = pairs.v[src[j]][0] * s;
                 dst[2 * j + 1] = pairs.v[src[j]][1] * s;
@@ -103,7 +104,6 @@ void decode_row(const CpuBank &bank, int w_dtype, int nrows, int K, int r, float
             for (int c = cb * 128; c < cb * 128 + 128; ++c) dst[c] = table.v[src[c]] * s;
         }
     }
-    (void)nrows;
 }
 
 // Dot product of two float vectors (n a multiple of 128) with 8 independent partial sums.

@@ -35,7 +35,7 @@ def decode_bank_torch(bank: torch.Tensor, w_dtype: int, scales=None) -> torch.Te
         sign = torch.where(codes >= 8, -1.0, 1.0).double()
         e, m = (codes >> 1) & 3, (codes & 1).double()
         mag = torch.where(e == 0, m * 0.5, (1.0 + m * 0.5) * torch.pow(2.0, (e - 1).double()))
-        s = scales.contiguous().view(torch.float8_e8m0fnu).to(torch.float64).repeat_interleave(32, 1)
+        s = scales.t().contiguous().view(torch.float8_e8m0fnu).to(torch.float64).repeat_interleave(32, 1)
         return sign * mag * s
     v = bank.view(torch.float8_e4m3fn).to(torch.float64)
     s = scales.double().repeat_interleave(128, 0).repeat_interleave(128, 1)

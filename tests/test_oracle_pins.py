@@ -48,12 +48,12 @@ def test_e8m0_table_matches_torch_for_all_256_codes():
 
 def test_mxfp4_nibble_order_and_block_scales():
     """Byte j holds element 2j in its low nibble; each run of 32 elements of a row has its own
-    scale."""
+    scale, stored run-major (scales[run][row])."""
     packed = np.zeros((2, 32), dtype=np.uint8)        # 2 rows x 64 elements
     packed[0, 0] = 0x21                               # elements 0, 1 = codes 1, 2 = 0.5, 1.0
     packed[0, 16] = 0xF7                              # elements 32, 33 = 6.0, -6.0
     packed[1, 31] = 0x9C                              # elements 62, 63 = -2.0, -0.5
-    scales = np.array([[127, 130], [126, 120]], dtype=np.uint8)
+    scales = np.array([[127, 126], [130, 120]], dtype=np.uint8)   # [run][row]
     d = oracle.mxfp4_to_f64(packed, scales)
     assert d.shape == (2, 64)
     assert (d[0, 0], d[0, 1]) == (0.5, 1.0)

@@ -115,8 +115,8 @@ class Layer:
     w13: torch.Tensor         # [n_slots][2I][H] float32 / bfloat16 / uint8 (fp8 codes);
                               # MXFP4: [n_slots][2I][H/2] uint8 code pairs
     w2: torch.Tensor          # [n_slots][H][I] (MXFP4: [n_slots][H][I/2])
-    s13: Optional[torch.Tensor]  # fp8: [n_slots][2I/128][H/128] float32; MXFP4: [n_slots][2I][H/32] uint8
-    s2: Optional[torch.Tensor]   # fp8: [n_slots][H/128][I/128] float32; MXFP4: [n_slots][H][I/32] uint8
+    s13: Optional[torch.Tensor]  # fp8: [n_slots][2I/128][H/128] float32; MXFP4: [n_slots][H/32][2I] uint8
+    s2: Optional[torch.Tensor]   # fp8: [n_slots][H/128][I/128] float32; MXFP4: [n_slots][I/32][H] uint8
 
     @property
     def tokens(self) -> int:
@@ -155,7 +155,7 @@ def quantize_fp8_blocks(w: torch.Tensor):
 
 def quantize_mxfp4(w: torch.Tensor):
     """Input preparation only: float32 ``[R][C]`` -> (E2M1 code pairs [R][C/2] uint8, E8M0 scales
-    [R][C/32] uint8), following the OCP MX recipe: per 32-element block the shared exponent is
+    [C/32][R] uint8, run-major), following the OCP MX recipe: per 32-element block the shared exponent is
     floor(log2(amax)) - 2 (2 = the largest E2M1 exponent), and each element is rounded to the
     nearest E2M1 value, ties to even, saturating at +-6; an all-zero block takes scale 1."""
     r, c = w.shape
@@ -171,7 +171,7 @@ def quantize_mxfp4(w: torch.Tensor):
            + (a > 5)).to(torch.uint8)
     codes = (idx | (torch.signbit(q).to(torch.uint8) << 3)).view(r, c)
     packed = (codes[:, 0::2] | (codes[:, 1::2] << 4)).contiguous()
-    return packed, code_s.to(torch.uint8)
+    return packed, code_s.to(torch.uint8).t().contiguous()
 
 
 def _weights(g, rows, cols, w_dtype, device):
@@ -191,7 +191,7 @@ def alloc_banks(n_slots: int, hidden: int, inter: int, w_dtype: int, device="cpu
     if w_dtype == DT_MXFP4:
         u8 = dict(dtype=torch.uint8, device=device)
         return (torch.zeros(n_slots, 2 * I, H // 2, **u8), torch.zeros(n_slots, H, I // 2, **u8),
-                torch.zeros(n_slots, 2 * I, H // 32, **u8), torch.zeros(n_slots, H, I // 32, **u8))
+                torch.zeros(n_slots, H // 32, 2 * I, **u8), torch.zeros(n_slots, I // 32, H, **u8))
     wdt = {DT_F32: torch.float32, DT_BF16: torch.bfloat16, DT_FP8: torch.uint8}[w_dtype]
     w13 = torch.zeros(n_slots, 2 * I, H, dtype=wdt, device=device)
     w2 = torch.zeros(n_slots, H, I, dtype=wdt, device=device)
@@ -213,8 +213,8 @@ def put_expert(banks, slot: int, inter: int, w_dtype: int, w1, a1, w3, a3, wd, a
         s13[slot, I // 128:] = a3
         s2[slot] = ad
     elif w_dtype == DT_MXFP4:
-        s13[slot, :I] = a1
-        s13[slot, I:] = a3
+        s13[slot, :, :I] = a1
+        s13[slot, :, I:] = a3
         s2[slot] = ad
 
 
