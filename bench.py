@@ -54,8 +54,11 @@ class HipEvents:
 
 
 def expert_bytes(lay):
-    """Bytes of one complete expert (W1, W3, W2 and block scales) and of its W13 part."""
+    """Bytes of one complete expert (W1, W3, W2 and their scales) and of its W13 part."""
     H, I = lay.hidden, lay.inter
+    if lay.w_dtype == 3:       # MXFP4: half a byte per weight, one scale byte per 32
+        w13 = I * H + 2 * I * H // 32
+        return w13 + H * I // 2 + H * I // 32, w13
     wb = {0: 4, 1: 2, 2: 1}[lay.w_dtype]
     s13 = (2 * I // 128) * (H // 128) * 4 if lay.w_dtype == 2 else 0
     s2 = (H // 128) * (I // 128) * 4 if lay.w_dtype == 2 else 0
@@ -163,27 +166,16 @@ def ingest_traffic(key, kernel_match, fetch_csv, write_csv, cal_fetch_csv, cal_w
 def _pool_tensors(cfg, E, device):
     """Random expert weights of one layer shape, E experts, in the bank layout."""
     import torch
-    H, I = cfg.hidden, cfg.inter
+    import workloads
     g = torch.Generator(device=device)
     g.manual_seed(12345)
-    out = {}
-    if cfg.w_dtype == 2:
-        import workloads
-        w13 = torch.empty(E, 2 * I, H, dtype=torch.uint8, device=device)
-        w2 = torch.empty(E, H, I, dtype=torch.uint8, device=device)
-        s13 = torch.empty(E, 2 * I // 128, H // 128, dtype=torch.float32, device=device)
-        s2 = torch.empty(E, H // 128, I // 128, dtype=torch.float32, device=device)
-        for e in range(E):
-            w13[e], s13[e] = workloads.quantize_fp8_blocks(
-                torch.randn(2 * I, H, generator=g, device=device) * 0.02)
-            w2[e], s2[e] = workloads.quantize_fp8_blocks(torch.randn(H, I, generator=g, device=device) * 0.02)
-        out.update(w13=w13, w2=w2, s13=s13, s2=s2)
-    else:
-        dt = torch.bfloat16 if cfg.w_dtype == 1 else torch.float32
-        out["w13"] = (torch.randn(E, 2 * I, H, generator=g, device=device) * 0.02).to(dt)
-        out["w2"] = (torch.randn(E, H, I, generator=g, device=device) * 0.02).to(dt)
-        out["s13"] = out["s2"] = None
-    return out
+    banks = workloads.alloc_banks(E, cfg.hidden, cfg.inter, cfg.w_dtype, device)
+    for e in range(E):
+        w1, a1 = workloads._weights(g, cfg.inter, cfg.hidden, cfg.w_dtype, device)
+        w3, a3 = workloads._weights(g, cfg.inter, cfg.hidden, cfg.w_dtype, device)
+        wd, ad = workloads._weights(g, cfg.hidden, cfg.inter, cfg.w_dtype, device)
+        workloads.put_expert(banks, e, cfg.inter, cfg.w_dtype, w1, a1, w3, a3, wd, ad)
+    return dict(zip(("w13", "w2", "s13", "s2"), banks))
 
 
 def measure_bandwidths(cfg_name, n_fill, reps):
@@ -591,7 +583,8 @@ def main():
     key = f"{args.config}:T{T}"
     traffic = measured_traffic(key)
     if mfma_path:
-        # fp8 weights are widened to bf16 in registers, so every contraction runs on bf16 MFMA
+        # fp8 and MXFP4 weights are widened to bf16 in registers, so every contraction runs on
+        # bf16 MFMA
         achieved = gu_flops / (gu_ms / 1e3) / 1e12
         roof = {"kernel": "grouped gate/up GEMM + SiLU-mul (grouped_gemm<gate/up>)", "bound": "mfma",
                 "achieved": round(achieved, 1), "peak": MFMA_PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
@@ -604,7 +597,7 @@ def main():
                 "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
                 "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
-    dtype = {0: "f32", 1: "bf16", 2: "fp8e4m3->bf16"}[cfg.w_dtype]
+    dtype = {0: "f32", 1: "bf16", 2: "fp8e4m3->bf16", 3: "mxfp4->bf16"}[cfg.w_dtype]
     res = {
         "metric": METRIC,
         "value": round(tokens_per_s, 1),
