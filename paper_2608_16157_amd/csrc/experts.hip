@@ -20,17 +20,26 @@
 
 namespace ftmoe {
 
-// Tuning constants (measured on MI355X; see the design notes for the sweep).
-// weight rows per work item = 16 * NB; fp8 weights take wider items (their activation loads,
-// bf16, are twice the weight bytes per element, so one activation load should feed more rows)
+// Tuning constants, chosen by sweeping them on MI355X.
+// weight rows per work item = 16 * NB; fp8 and MXFP4 weights may take wider items (their bf16
+// activation loads are 2 or 4 times the weight bytes per element, so one activation load should
+// feed more rows once there are enough groups to fill the chip)
 #ifndef FT_GEMV_NB
 #define FT_GEMV_NB 2
 #endif
+// fp8 and MXFP4 take items of 2 or 4 blocks: the narrow ones spread few-token calls (few groups)
+// over more workgroups; the fp8 down projection always takes the narrow ones
 #ifndef FT_GEMV_NB_FP8
 #define FT_GEMV_NB_FP8 4
 #endif
 #ifndef FT_GEMV_NB_FP4
 #define FT_GEMV_NB_FP4 4
+#endif
+#ifndef FT_GEMV_FP8_NARROW_PAIRS
+#define FT_GEMV_FP8_NARROW_PAIRS 128   // T * k up to which fp8 gate/up items are narrow
+#endif
+#ifndef FT_GEMV_FP4_NARROW_PAIRS
+#define FT_GEMV_FP4_NARROW_PAIRS 12    // same for MXFP4, both projections
 #endif
 #ifndef FT_GEMV_MT_MAX
 #define FT_GEMV_MT_MAX 2
@@ -66,9 +75,6 @@ template <> struct WTr<FT_DT_F32> { static constexpr int kLoads = 8, kBlock = 51
 template <> struct WTr<FT_DT_BF16> { static constexpr int kLoads = 4, kBlock = 256, kBatch = FT_GEMV_D_BF16; };
 template <> struct WTr<FT_DT_FP8E4M3FN_B128> { static constexpr int kLoads = 2, kBlock = 128, kBatch = FT_GEMV_D_FP8; };
 template <> struct WTr<FT_DT_MXFP4> { static constexpr int kLoads = 1, kBlock = 64, kBatch = FT_GEMV_D_FP4; };
-template <int WT> constexpr int gemv_nb() {
-    return WT == FT_DT_FP8E4M3FN_B128 ? FT_GEMV_NB_FP8 : (WT == FT_DT_MXFP4 ? FT_GEMV_NB_FP4 : FT_GEMV_NB);
-}
 
 __device__ __forceinline__ u32x4_t ld16(const void *p) {
     return *reinterpret_cast<const u32x4_t *>(p);
@@ -380,10 +386,23 @@ __global__ __launch_bounds__(256) void zero_out(float *out, size_t n4) {
 
 template <int WT, int EPI>
 static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
-    constexpr int NB = gemv_nb<WT>();
-    const int tiles = EPI == EPI_GATEUP ? a.I / (8 * NB) : a.H / (16 * NB);
-    hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
-                       s, a, tiles);
+    auto go = [&](auto nb) {
+        constexpr int NB = decltype(nb)::value;
+        const int tiles = EPI == EPI_GATEUP ? a.I / (8 * NB) : a.H / (16 * NB);
+        hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
+                           s, a, tiles);
+    };
+    const int pairs = a.T * a.k;
+    if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
+        if constexpr (EPI == EPI_DOWN) go(std::integral_constant<int, 2>{});
+        else if (pairs <= FT_GEMV_FP8_NARROW_PAIRS) go(std::integral_constant<int, 2>{});
+        else go(std::integral_constant<int, FT_GEMV_NB_FP8>{});
+    } else if constexpr (WT == FT_DT_MXFP4) {
+        if (pairs <= FT_GEMV_FP4_NARROW_PAIRS) go(std::integral_constant<int, 2>{});
+        else go(std::integral_constant<int, FT_GEMV_NB_FP4>{});
+    } else {
+        go(std::integral_constant<int, FT_GEMV_NB>{});
+    }
 }
 
 template <int WT>
