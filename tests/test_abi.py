@@ -213,3 +213,22 @@ def _prefill_call(desc, n_layers=2, T=4, overlap=1, copy_stream=FAKE + 8, stream
 def test_prefill_layers_rejects_before_enqueue(kw, want):
     assert _prefill_call(_desc(), **kw) == want
     assert _prefill_call(_desc(hidden=100), **kw) in (ftm.FT_ERR_SHAPE, ftm.FT_ERR_NULL, want)
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    """Without the built library every call raises; nothing falls back to another path."""
+    import subprocess
+    import sys
+    code = ("import paper_2608_16157_amd as ftm\n"
+            "try:\n"
+            "    ftm.ft_moe_workspace_bytes({'hidden': 256, 'inter': 512, 'n_experts': 8, 'top_k': 2,"
+            " 'gating': 0, 'w_dtype': 0, 'x_dtype': 0, 'n_slots': 4, 'shared_slot': -1}, 4)\n"
+            "except RuntimeError as e:\n"
+            "    print('raised:', e)\n"
+            "    raise SystemExit(0)\n"
+            "raise SystemExit(1)\n")
+    env = dict(os.environ, FTMOE_LIBRARY=str(tmp_path / "absent.so"))
+    r = subprocess.run([sys.executable, "-c", code], cwd=ROOT, env=env, capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "not built" in r.stdout
