@@ -350,10 +350,11 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     for (int i = tid; i < nch * E; i += kFusedThreads) s_wh[i] = 0;
     for (int i = tid; i < ncnt; i += kFusedThreads) s_cnt[i] = 0;
     if (tid == 0) *s_status = 0;
-    if (tid < E) s_raw[tid] = raw;
+    // (the slot-table entry is stored in phase B, so this barrier does not wait for its load)
     lds_barrier();
 
     // ---- B
+    if (tid < E) s_raw[tid] = raw;
     slot_count(raw, E, a.n_slots, s_cnt);
     auto put = [&](int t, int id, float w) {
         if (t < T && lane < k) {
@@ -445,14 +446,30 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     if (wave != 0) {
         chunk_prefix();
     } else {
-        // lane l owns experts [l*epl, l*epl + epl)
+        // lane l owns experts [l*epl, l*epl + epl), epl = NPL; up to 8 per lane, their totals
+        // and slots stay in registers for the second pass (more would not fit the 128 registers
+        // of a 1024-thread workgroup; those are read again from LDS)
+        constexpr int kMaxEpl = NPL;
+        constexpr bool kCache = NPL <= 8;
         const int epl = (E + kWave - 1) / kWave;
         const int e0 = min(E, lane * epl), e1 = min(E, e0 + epl);
-        uint32_t h = 0, m = 0, g = 0, mx = 0, mtl = 0;
-        for (int e = e0; e < e1; ++e) {
+        int tots[kCache ? kMaxEpl : 1], slots[kCache ? kMaxEpl : 1];
+        auto total_of = [&](int e) {
             int tot = 0;
             for (int c = 0; c < nch; ++c) tot += s_wh[c * E + e];
-            const bool hit = s_eff[e] >= 0;
+            return tot;
+        };
+        uint32_t h = 0, m = 0, g = 0, mx = 0, mtl = 0;
+#pragma unroll
+        for (int i = 0; i < kMaxEpl; ++i) {
+            const int e = e0 + i;
+            const int tot = e < e1 ? total_of(e) : 0;
+            const int slot = e < e1 ? s_eff[e] : -1;
+            if constexpr (kCache) {
+                tots[i] = tot;
+                slots[i] = slot;
+            }
+            const bool hit = slot >= 0;
             h += hit ? tot : 0;
             m += hit ? 0 : tot;
             g += (hit && tot > 0) ? 1 : 0;
@@ -463,10 +480,18 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
         const uint32_t gi = wave_incl_scan_u32(g), xi = wave_incl_scan_u32(mx);
         const uint32_t ti = wave_incl_scan_u32(mtl);
         uint32_t hrun = hi - h, mrun = mi - m, grun = gi - g, trun = ti - mtl;
-        for (int e = e0; e < e1; ++e) {
-            int tot = 0;
-            for (int c = 0; c < nch; ++c) tot += s_wh[c * E + e];
-            const int slot = s_eff[e];
+#pragma unroll
+        for (int i = 0; i < kMaxEpl; ++i) {
+            const int e = e0 + i;
+            if (e >= e1) continue;
+            int tot, slot;
+            if constexpr (kCache) {
+                tot = tots[i];
+                slot = slots[i];
+            } else {
+                tot = total_of(e);
+                slot = s_eff[e];
+            }
             const bool hit = slot >= 0;
             s_hoff[e] = hrun;
             s_moff[e] = mrun;
@@ -478,7 +503,7 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
                 a.wv.grp_len[grun] = tot;
                 a.wv.grp_mt_off[grun] = trun;
                 const int nmt = (tot + kGemmBM - 1) / kGemmBM;
-                for (int i = 0; i < nmt; ++i) a.wv.mt_group[trun + i] = grun;
+                for (int u = 0; u < nmt; ++u) a.wv.mt_group[trun + u] = grun;
             }
             hrun += hit ? tot : 0;
             mrun += hit ? 0 : tot;
