@@ -45,7 +45,11 @@ namespace ftmoe {
 constexpr int kGemmThreads = 256;
 constexpr int kGemmWaves = kGemmThreads / kWave;
 constexpr int kWavesM = 1, kWavesN = 4;
-constexpr int kWaveRows = 128, kWaveCols = 64;          // per-wave output tile
+#ifndef FT_GEMM_OCC
+#define FT_GEMM_OCC 2
+#endif
+constexpr int kGemmOcc = FT_GEMM_OCC;                   // workgroups per CU
+constexpr int kWaveRows = kGemmBM, kWaveCols = 64;      // per-wave output tile
 constexpr int kMI = kWaveRows / 32, kNJ = kWaveCols / 32; // 32 x 32 MFMA tiles per wave
 constexpr int kBM = kGemmBM;                            // token rows per tile
 constexpr int kBN = kGemmBN;                            // weight rows per tile
@@ -146,7 +150,7 @@ __device__ __forceinline__ void dma4(const void *g, uint8_t *lds_block) {
 }
 
 template <int WT, int EPI>
-__global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, int ntn) {
+__global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArgs a, int ntn) {
     constexpr bool kFp8 = WT == FT_DT_FP8E4M3FN_B128;
     constexpr bool kFp4 = WT == FT_DT_MXFP4;
     constexpr int BK = GTr<WT>::BK, NS = GTr<WT>::NS;
@@ -160,7 +164,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
     constexpr int XSTAGE = kFp4 ? 1024 : 16;         // LDS per scale stage: 4 waves x 256 bytes
     static_assert(A_INSTR >= 1 && B_INSTR >= 1, "stage too small");
     static_assert(NS >= 2 && NS <= 4, "ring depth");
-    static_assert((NS - 1) * PER_STAGE < 64, "vmcnt range");
+    static_assert(NS * PER_STAGE < 64, "vmcnt range");
     static_assert(!kFp8 || 128 % BK == 0, "an fp8 K stage lies in one scale block");
     // one array per stage (see the header comment); unused ones shrink to 16 bytes
     __shared__ __attribute__((aligned(1024))) uint8_t sA0[ASTAGE], sA1[ASTAGE];
@@ -332,99 +336,161 @@ __global__ __launch_bounds__(kGemmThreads, 2) void grouped_gemm(ExpertArgs a, in
         for (int j = 0; j < kNJ; ++j) acc[i][j] = floatx16_t{};
 
     const int nk = K / BK;
-    // One pipeline step: multiply K stage kt from slot RS while the DMA of stage kt + NS - 1
-    // fills slot WS.  Stage kt has landed once this wave allows only stages kt+1 .. kt+NS-2 to be
-    // outstanding and the barrier has passed (every wave's share landed, and every wave is done
-    // reading stage kt-1, whose slot WS is); past the end the DMA re-reads the last stage into
-    // that free slot, which keeps the counts constant.
-    // ML: the 32-row MFMA sub-tiles of the M tile that hold at least one real row; the others
-    // hold padding only, so their operand reads and MFMAs are skipped
-    auto step = [&](int kt, auto rs, auto ws, auto ml) {
-        constexpr int ML = decltype(ml)::value;
-        wait_vmcnt<(NS - 2) * PER_STAGE>();
-        wait_lgkmcnt0();
-        stage_barrier();
-        issue(min(kt + NS - 1, nk - 1), stA(ws), stB(ws), ws);
-        if (kt < nk) {
-            const uint8_t *A = stA(rs);
-            const uint8_t *B = stB(rs);
-            constexpr int KS = BK / 16;
-            float sc[2] = {1.f, 1.f};
-            if constexpr (kFp8) {
-                const int kb = (kt * BK) / 128;
-                sc[0] = s_scale[wn][0][kb];
-                sc[1] = s_scale[wn][1][kb];
-            }
-            // 32x32x16 MFMA operands: lane (r = lane % 32, kg = lane / 32) holds 8 K values of
-            // row r for each operand; which 8 is free as long as A and B agree.  bf16 weights:
-            // sub-step ks takes K [16 ks + 8 kg, +8), i.e. 16-byte chunk 2 ks + kg of both rows.
-            // fp8 weights: a lane reads one 16-byte chunk of its weight row, 16 K values, for
-            // two sub-steps, so sub-step ks = 2 p + s takes K [32 p + 16 kg + 8 s, +8): weight
-            // chunk 2 p + kg (bytes 8 s ..), activation chunk 4 p + 2 kg + s.  MXFP4 weights: a
-            // lane reads weight chunk kg, 32 K values under one scale, for all four sub-steps, so
-            // sub-step ks takes K [32 kg + 8 ks, +8): word ks of the chunk, activation chunk
-            // 4 kg + ks.
-            u32x4_t b16[kNJ];
-            float xs[kNJ];
+    constexpr int KS = BK / 16;   // MFMA sub-steps per K stage
+    // Operands of one 32x32x16 MFMA sub-step.  The lane (r = lane % 32, kg = lane / 32) holds 8 K
+    // values of row r for each operand; which 8 is free as long as A and B agree.  bf16 weights:
+    // sub-step ks takes K [16 ks + 8 kg, +8), i.e. 16-byte chunk 2 ks + kg of both rows.  fp8
+    // weights: a lane reads one 16-byte chunk of its weight row, 16 K values, for two sub-steps,
+    // so sub-step ks = 2 p + s takes K [32 p + 16 kg + 8 s, +8): weight chunk 2 p + kg (bytes
+    // 8 s ..), activation chunk 4 p + 2 kg + s.  MXFP4 weights: a lane reads weight chunk kg, 32
+    // K values under one scale, for all four sub-steps, so sub-step ks takes K [32 kg + 8 ks, +8):
+    // word ks of the chunk, activation chunk 4 kg + ks.  Weight chunks and scales are carried
+    // over from the sub-step that read them.
+    struct Frag {
+        u32x4_t a[kMI];
+        u32x4_t b[kNJ];
+        float xs[kNJ];   // MXFP4 scale of each column tile
+        float sc[2];     // fp8 block scale of the gate (or down) and the up columns
+    };
+    auto load_frag = [&](auto rs, auto ks, auto ml, Frag &f, const Frag &prev, int kt) {
+        constexpr int KSI = decltype(ks)::value, ML = decltype(ml)::value;
+        const uint8_t *A = stA(rs);
+        const uint8_t *B = stB(rs);
+        const int ca = kFp8 ? 4 * (KSI / 2) + 2 * fq + (KSI % 2) : (kFp4 ? 4 * fq + KSI : 2 * KSI + fq);
 #pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-                const int ca = kFp8 ? 4 * (ks / 2) + 2 * fq + (ks % 2) : (kFp4 ? 4 * fq + ks : 2 * ks + fq);
-                u32x4_t af[kMI], bf[kNJ];
+        for (int i = 0; i < ML; ++i) {
+            const int ra = wm * kWaveRows + i * 32 + fn;
+            f.a[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, ca) << 4));
+        }
 #pragma unroll
-                for (int i = 0; i < ML; ++i) {
-                    const int ra = wm * kWaveRows + i * 32 + fn;
-                    af[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, ca) << 4));
+        for (int j = 0; j < kNJ; ++j) {
+            const int rb = wn * kWaveCols + j * 32 + fn;
+            if constexpr (kFp4) {
+                if constexpr (KSI == 0) {
+                    f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, fq) << 4));
+                    f.xs[j] = e8m0_to_f32(stX(rs)[xcol[j]]);
+                } else {
+                    f.b[j] = prev.b[j];
+                    f.xs[j] = prev.xs[j];
                 }
-#pragma unroll
-                for (int j = 0; j < kNJ; ++j) {
-                    const int rb = wn * kWaveCols + j * 32 + fn;
-                    if constexpr (kFp4) {
-                        if (ks == 0) {
-                            b16[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, fq) << 4));
-                            xs[j] = e8m0_to_f32(stX(rs)[xcol[j]]);
-                        }
-                        bf[j] = fp4x8_scaled_to_bf16x8(b16[j][ks], xs[j]);
-                    } else if constexpr (!kFp8) {
-                        bf[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, ca) << 4));
-                    } else {
-                        if (ks % 2 == 0)
-                            b16[j] = *reinterpret_cast<const u32x4_t *>(
-                                B + rb * BRB + (swz<BRB>(rb, 2 * (ks / 2) + fq) << 4));
-                        const float s = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? sc[1] : sc[0];
-                        bf[j] = ks % 2 == 0 ? fp8x8_scaled_to_bf16x8(b16[j][0], b16[j][1], s)
-                                            : fp8x8_scaled_to_bf16x8(b16[j][2], b16[j][3], s);
-                    }
-                }
-#pragma unroll
-                for (int i = 0; i < ML; ++i)
-#pragma unroll
-                    for (int j = 0; j < kNJ; ++j)
-                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                            as_bf16x8(af[i]), as_bf16x8(bf[j]), acc[i][j], 0, 0, 0);
+            } else if constexpr (kFp8) {
+                if constexpr (KSI % 2 == 0)
+                    f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, 2 * (KSI / 2) + fq) << 4));
+                else
+                    f.b[j] = prev.b[j];
+            } else {
+                f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, ca) << 4));
             }
         }
+        if constexpr (kFp8) {
+            if constexpr (KSI == 0) {
+                const int kb = (kt * BK) / 128;
+                f.sc[0] = s_scale[wn][0][kb];
+                f.sc[1] = s_scale[wn][1][kb];
+            } else {
+                f.sc[0] = prev.sc[0];
+                f.sc[1] = prev.sc[1];
+            }
+        }
+    };
+    auto mma = [&](const Frag &f, auto ks, auto ml) {
+        constexpr int KSI = decltype(ks)::value, ML = decltype(ml)::value;
+        u32x4_t bf[kNJ];
+#pragma unroll
+        for (int j = 0; j < kNJ; ++j) {
+            if constexpr (kFp4) {
+                bf[j] = fp4x8_scaled_to_bf16x8(f.b[j][KSI], f.xs[j]);
+            } else if constexpr (kFp8) {
+                const float s = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.sc[1] : f.sc[0];
+                bf[j] = KSI % 2 == 0 ? fp8x8_scaled_to_bf16x8(f.b[j][0], f.b[j][1], s)
+                                     : fp8x8_scaled_to_bf16x8(f.b[j][2], f.b[j][3], s);
+            } else {
+                bf[j] = f.b[j];
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < ML; ++i)
+#pragma unroll
+            for (int j = 0; j < kNJ; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(f.a[i]), as_bf16x8(bf[j]), acc[i][j], 0,
+                                                                     0, 0);
+    };
+
+    // Software pipeline.  The ring holds NS stages; the DMA of stage kt + NS goes into the slot of
+    // stage kt once every wave has read all of stage kt.  Each sub-step's operands are read from
+    // LDS while the previous sub-step's MFMAs run, and the hand-off sits in the last sub-step of
+    // a stage: wait for this wave's share of stage kt + 1 (stages kt + 2 .. kt + NS - 1 may stay
+    // outstanding) and for its LDS reads of stage kt, barrier, refill the slot of stage kt, read
+    // the first operands of stage kt + 1, then run the last MFMAs of stage kt.  Past the end the
+    // DMA re-reads the last stage, which keeps the counts constant.
+    // ML: the 32-row MFMA sub-tiles of the M tile that hold at least one real row; the others
+    // hold padding only, so their operand reads and MFMAs are skipped.
+    // Order of one sub-step's instructions: its MFMAs with the next sub-step's operand reads
+    // (sub-step ks2 of the same or the next stage) threaded between them, one read after each
+    // MFMA, so the reads have the remaining MFMAs' time to land.
+    auto interleave = [&](auto ks2, auto ml) {
+        constexpr int K2 = decltype(ks2)::value, ML = decltype(ml)::value;
+        constexpr bool kReadsB = kFp4 ? K2 == 0 : (kFp8 ? K2 % 2 == 0 : true);
+        constexpr int kReads = ML + (kReadsB ? kNJ : 0) + (kFp4 && K2 == 0 ? kNJ : 0) + (kFp8 && K2 == 0 ? 2 : 0);
+        constexpr int kMfma = ML * kNJ;
+        constexpr int kPairs = kReads < kMfma ? kReads : kMfma;
+        static_for<0, kPairs>([&](auto) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+        });
+        if constexpr (kMfma > kPairs) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kPairs, 0);
+        if constexpr (kReads > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kPairs, 0);
+    };
+    auto mainloop = [&](auto ml) {
+        Frag cur, nxt;
+        // stage kt, in ring slot S (= kt mod NS)
+        auto stage = [&](auto s, int kt) {
+            constexpr int S = decltype(s)::value;
+            static_for<0, KS>([&](auto ks) {
+                constexpr int KSI = decltype(ks)::value;
+                if constexpr (KSI + 1 == KS) {
+                    wait_vmcnt<(NS - 2) * PER_STAGE>();
+                    wait_lgkmcnt0();
+                    stage_barrier();
+                    issue(min(kt + NS, nk - 1), stA(s), stB(s), s);
+                }
+                __builtin_amdgcn_sched_barrier(0);
+                mma(cur, ks, ml);
+                if constexpr (KSI + 1 < KS)
+                    load_frag(s, ic<KSI + 1>{}, ml, nxt, cur, kt);
+                else
+                    load_frag(ic<(S + 1) % NS>{}, ic<0>{}, ml, nxt, cur, min(kt + 1, nk - 1));
+                interleave(ic<(KSI + 1) % KS>{}, ml);
+                __builtin_amdgcn_sched_barrier(0);
+                cur = nxt;
+            });
+        };
+        wait_vmcnt<(NS - 1) * PER_STAGE>();
+        wait_lgkmcnt0();
+        stage_barrier();
+        load_frag(ic<0>{}, ic<0>{}, ml, cur, cur, 0);
+        // whole turns of the ring without branches (a branch around a stage would make the
+        // compiler lose track of which slot each DMA writes, and drain them all), then the rest
+        int kt0 = 0;
+        for (; kt0 + NS <= nk; kt0 += NS)
+            static_for<0, NS>([&](auto s) { stage(s, kt0 + decltype(s)::value); });
+        static_for<0, NS - 1>([&](auto s) {
+            if (kt0 + decltype(s)::value < nk) stage(s, kt0 + decltype(s)::value);
+        });
     };
 
     // outstanding stores of the zeroing loop must not count against the DMA waits below; the
     // barrier publishes the staged scale / token / gate tables
     wait_vmcnt<0>();
     __syncthreads();
-    static_for<0, NS - 1>([&](auto s) { issue(min(decltype(s)::value, nk - 1), stA(s), stB(s), s); });
-    auto mainloop = [&](auto ml) {
-        for (int kt = 0; kt < nk; kt += NS) {
-            // stage kt + S sits in slot S; its step refills slot (S + NS - 1) mod NS
-            static_for<0, NS>([&](auto s) {
-                constexpr int S = decltype(s)::value;
-                step(kt + S, s, ic<(S + NS - 1) % NS>{}, ml);
-            });
-        }
-    };
-    static_assert(kMI == 4, "one main loop per live sub-tile count");
-    const int mlive = __builtin_amdgcn_readfirstlane(min(kMI, (min(len - m0, kBM) + 31) / 32));
-    if (mlive >= 4) mainloop(ic<4>{});
-    else if (mlive == 3) mainloop(ic<3>{});
-    else if (mlive == 2) mainloop(ic<2>{});
-    else mainloop(ic<1>{});
+    static_for<0, NS>([&](auto s) { issue(min(decltype(s)::value, nk - 1), stA(s), stB(s), s); });
+    // one main loop per live sub-tile count (in steps of MLQ sub-tiles for tall tiles)
+    constexpr int MLQ = kMI > 4 ? 2 : 1;
+    const int mlive = __builtin_amdgcn_readfirstlane(min(kMI, (min(len - m0, kBM) + 32 * MLQ - 1) / (32 * MLQ) * MLQ));
+    static_for<1, kMI / MLQ + 1>([&](auto q) {
+        constexpr int ML = decltype(q)::value * MLQ;
+        if (mlive == ML) mainloop(ic<ML>{});
+    });
     wait_vmcnt<0>();   // the redundant tail stages
 
     // ---- epilogue: element e of a 32 x 32 tile in lane (fn, fq) is row 8 (e / 4) + 4 fq + e % 4,
