@@ -297,7 +297,7 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                     }
                     if constexpr (WT == FT_DT_MXFP4) {
                         // the lane's 32 codes share the scale of its 32-value run q
-                        const float xs = e8m0_to_f32(xv[d][b]);
+                        const float xs = fp4_scale_operand(xv[d][b]);
 #pragma unroll
                         for (int i = 0; i < 4; ++i) wc[i] = fp4x8_scaled_to_bf16x8(wv[d][b][0][i], xs);
                     }

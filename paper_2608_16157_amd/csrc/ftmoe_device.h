@@ -55,14 +55,18 @@ __device__ __forceinline__ u32x4_t fp8x8_scaled_to_bf16x8(uint32_t w0, uint32_t 
                    pk(__builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w1), true))};
 }
 
-// e8m0 scale byte -> float32 2^(e - 127): e = 0 is the subnormal 2^-127, e = 255 is NaN
-__device__ __forceinline__ float e8m0_to_f32(uint32_t e) {
-    const uint32_t bits = e == 0 ? 0x00400000u : (e == 255 ? 0x7FC00000u : e << 23);
-    return __builtin_bit_cast(float, bits);
+// Scale operand of the scaled fp4 conversion for an e8m0 scale byte e (2^(e - 127); e = 0 the
+// subnormal 2^-127, e = 255 NaN).  The conversion reads only the exponent field of its float
+// operand, as an e8m0 exponent, so the byte shifted into that field is the whole decode: measured
+// bit-identical to passing the decoded float (2^-127 as a subnormal, NaN for 255) for every byte
+// and every code pair, without the compares and selects the decode costs.
+__device__ __forceinline__ float fp4_scale_operand(uint32_t e) {
+    return __builtin_bit_cast(float, e << 23);
 }
 
 // 8 fp4 e2m1 codes (one 32-bit word, element 0 in the low nibble) times a power-of-two scale ->
-// 8 bf16 (exact: an e2m1 value has two significant bits), element order preserved
+// 8 bf16 (exact: an e2m1 value has two significant bits), element order preserved; s comes from
+// fp4_scale_operand
 __device__ __forceinline__ u32x4_t fp4x8_scaled_to_bf16x8(uint32_t w, float s) {
     auto pk = [](bf16x2_vec_t v) { return __builtin_bit_cast(uint32_t, v); };
     return u32x4_t{pk(__builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(w, s, 0)),

@@ -6,15 +6,20 @@
 //   gate/up: h[rows of g] = silu(X_g W1^T) * (X_g W3^T)       tile = BM rows x BN/2 h columns
 //   down   : out[tok] += gate * (h_g W2^T)                    tile = BM rows x BN out columns
 //
-// Work decomposition.  One workgroup of 4 waves per (group, BM-row M tile, BN-row N tile); each
-// wave computes all 128 rows of the tile for its own 64 columns, as 4 x 2 MFMA 32x32x16 tiles
-// (the bf16 MFMA shape with the highest measured throughput on gfx950), so every weight element
-// is read from LDS (and, for fp8, widened) by exactly one wave.  Two workgroups share a CU, so one
-// multiplies while the other waits at a stage barrier or runs its prologue or epilogue.  The tile
-// is as wide as two workgroups per CU allow because the kernel is bound by how fast L2 feeds the
-// CUs (global -> LDS traffic tops out near 25 bytes per clock per CU): a 128 x 256 tile moves 768
-// bytes per K step for 65536 flops, a third less per flop than 128 x 128, while the 128-row M
-// tile keeps the padding of the small expert groups in check.
+// Work decomposition.  One workgroup per (group, BM-row M tile, BN-row N tile).  Each wave
+// computes 128 rows of the tile for its own 64 columns, as 4 x 2 MFMA 32x32x16 tiles (the bf16
+// MFMA shape with the highest measured throughput on gfx950), so every weight element is read
+// from LDS (and, for fp8 or MXFP4, widened) by exactly one wave.  The default tile is 128 x 256
+// with 4 waves and two workgroups per CU, so one multiplies while the other waits at a stage
+// barrier or runs its prologue or epilogue.  A build with FT_GEMM_BM = 256 uses 256 x 256 tiles
+// of 8 waves, one workgroup per CU: a third fewer bytes per flop, measured faster on dense
+// shapes but slower on routed prefill batches, whose expert groups of about 256 rows leave
+// nearly empty tail tiles that still stream a whole weight tile.
+// The kernel is bound by how fast global memory fills LDS (measured: 17 TB/s for L2-resident
+// 64-byte row pieces, 7-11 TB/s once the data comes from the Infinity Cache or HBM), so the tile
+// is as large as LDS and the occupancy allow: a 128 x 256 tile moves 768 bytes per K step for
+// 65536 flops, a third less per flop than 128 x 128, while the 128-row M tile keeps the padding
+// of the small expert groups in check.
 // Tiles are enumerated per group, in bands of up to kBandM M tiles, each band N-tile-major with
 // the M tile fastest, through the per-M-tile group map the router writes, so the tiles that
 // share a weight tile and those that share activation rows run at the same time; the block ->
@@ -22,13 +27,16 @@
 // to share its L2.
 //
 // Data movement.  A (activation rows, gathered through row_tok for gate/up) and B (weight rows,
-// kept in their storage format, bf16 or fp8) go straight from global memory into LDS with
-// global_load_lds (16 bytes per lane), through a ring of NS stages of BK K-values, NS - 1 stages
-// in flight while one is multiplied.  Every LDS row keeps its 16-byte chunks XOR-swizzled by the
-// row index, so MFMA operand reads of consecutive rows hit distinct banks.  The stage hand-off is
-// an explicit vmcnt wait plus s_barrier (a __syncthreads would drain every stage in flight).  The
-// ring is unrolled and every stage buffer is an array of its own, so the compiler can tell the
-// stage being read from the stages still being written and adds no wait of its own.
+// kept in their storage format) go straight from global memory into LDS with global_load_lds
+// (16 bytes per lane), through a ring of NS stages of BK K-values.  Every LDS row keeps its
+// 16-byte chunks XOR-swizzled by the row index, so MFMA operand reads of consecutive rows hit
+// distinct banks.  The main loop is software-pipelined: each MFMA sub-step's operands are read
+// from LDS while the previous sub-step's MFMAs run, and the stage hand-off (an explicit vmcnt
+// wait plus s_barrier; a __syncthreads would drain every stage in flight) sits in the last
+// sub-step of a stage, so the first reads of the next stage overlap its last MFMAs.  The ring is
+// unrolled, every stage buffer is an array of its own and whole turns of the ring run without
+// branches, so the compiler can tell the stage being read from the stages still being written
+// and adds no wait of its own.
 //
 // fp8 weights carry one float32 scale per 128 x 128 block.  A wave's 64 columns lie in at most
 // two scale blocks (the gate and the up half of a gate/up tile, one block for down), so each fp8
@@ -42,18 +50,21 @@
 
 namespace ftmoe {
 
-constexpr int kGemmThreads = 256;
-constexpr int kGemmWaves = kGemmThreads / kWave;
-constexpr int kWavesM = 1, kWavesN = 4;
+#ifndef FT_GEMM_WAVE_ROWS
+#define FT_GEMM_WAVE_ROWS 128
+#endif
+constexpr int kWaveRows = FT_GEMM_WAVE_ROWS, kWaveCols = 64;   // per-wave output tile
+constexpr int kWavesM = kGemmBM / kWaveRows, kWavesN = 4;
+constexpr int kGemmWaves = kWavesM * kWavesN;
+constexpr int kGemmThreads = kGemmWaves * kWave;
 #ifndef FT_GEMM_OCC
 #define FT_GEMM_OCC 2
 #endif
 constexpr int kGemmOcc = FT_GEMM_OCC;                   // workgroups per CU
-constexpr int kWaveRows = kGemmBM, kWaveCols = 64;      // per-wave output tile
 constexpr int kMI = kWaveRows / 32, kNJ = kWaveCols / 32; // 32 x 32 MFMA tiles per wave
 constexpr int kBM = kGemmBM;                            // token rows per tile
 constexpr int kBN = kGemmBN;                            // weight rows per tile
-static_assert(kWavesM * kWavesN == kGemmWaves, "4 waves");
+static_assert(kGemmWaves == 4 || kGemmWaves == 8, "4 or 8 waves");
 static_assert(kBM == kWavesM * kWaveRows && kBN == kWavesN * kWaveCols, "tile = waves x wave tile");
 #ifndef FT_GEMM_BAND
 #define FT_GEMM_BAND 8
@@ -270,14 +281,15 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     // MXFP4 scales (run-major in memory: the scales of one 32-wide K run of consecutive weight
     // rows are contiguous).  A stage covers runs 2 kt and 2 kt + 1 of the tile's 256 weight rows,
     // which are 4 segments of 128 contiguous bytes (gate/up: the 128 gate rows and the 128 up
-    // rows of the tile; down: two halves of its 256 rows).  Wave w = 2 run + half moves segment
-    // (run, half) with one 4-byte-per-lane DMA into bytes [256 w, 256 w + 128) of the stage;
-    // lanes 32..63 fetch the same segment again into the next 128 bytes, so the instruction has
-    // every lane active and stays in bounds.
+    // rows of the tile; down: two halves of its 256 rows).  Wave w = 2 run + half (mod 4) moves
+    // segment (run, half) with one 4-byte-per-lane DMA into bytes [256 w, 256 w + 128) of the
+    // stage; lanes 32..63 fetch the same segment again into the next 128 bytes, so the instruction
+    // has every lane active and stays in bounds.  With 8 waves, waves w and w + 4 write the same
+    // bytes, which keeps every wave's DMA count per stage equal.
     const uint8_t *xsrc = nullptr;
     int xcol[kNJ] = {};
     if constexpr (kFp4) {
-        const int xr = wave >> 1, xh = wave & 1;
+        const int xr = (wave >> 1) & 1, xh = wave & 1;
         const int row0 = EPI == GEMM_GATEUP ? (xh ? I : 0) + nt * (kBN / 2) : nt * kBN + xh * (kBN / 2);
         xsrc = static_cast<const uint8_t *>(EPI == GEMM_GATEUP ? a.s13 : a.s2) +
                (static_cast<size_t>(slot) * (K / 32) + xr) * nrows + row0 + 4 * (lane & 31);
@@ -297,7 +309,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         for (int ii = 0; ii < B_INSTR; ++ii)
             dma16(bsrc[ii] + static_cast<size_t>(kt) * BRB, dB + (wave * B_INSTR + ii) * 1024);
         if constexpr (kFp4) {
-            dma4(xsrc + static_cast<size_t>(kt) * (BK / 32) * nrows, stX(ws) + wave * 256);
+            dma4(xsrc + static_cast<size_t>(kt) * (BK / 32) * nrows, stX(ws) + (wave & 3) * 256);
         }
     };
     const int nkb = K / 128;
@@ -349,7 +361,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     struct Frag {
         u32x4_t a[kMI];
         u32x4_t b[kNJ];
-        float xs[kNJ];   // MXFP4 scale of each column tile
+        uint32_t xb[kNJ];   // MXFP4 e8m0 scale byte of each column tile
         float sc[2];     // fp8 block scale of the gate (or down) and the up columns
     };
     auto load_frag = [&](auto rs, auto ks, auto ml, Frag &f, const Frag &prev, int kt) {
@@ -368,10 +380,10 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
             if constexpr (kFp4) {
                 if constexpr (KSI == 0) {
                     f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, fq) << 4));
-                    f.xs[j] = e8m0_to_f32(stX(rs)[xcol[j]]);
+                    f.xb[j] = stX(rs)[xcol[j]];
                 } else {
                     f.b[j] = prev.b[j];
-                    f.xs[j] = prev.xs[j];
+                    f.xb[j] = prev.xb[j];
                 }
             } else if constexpr (kFp8) {
                 if constexpr (KSI % 2 == 0)
@@ -399,7 +411,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
 #pragma unroll
         for (int j = 0; j < kNJ; ++j) {
             if constexpr (kFp4) {
-                bf[j] = fp4x8_scaled_to_bf16x8(f.b[j][KSI], f.xs[j]);
+                bf[j] = fp4x8_scaled_to_bf16x8(f.b[j][KSI], fp4_scale_operand(f.xb[j]));
             } else if constexpr (kFp8) {
                 const float s = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.sc[1] : f.sc[0];
                 bf[j] = KSI % 2 == 0 ? fp8x8_scaled_to_bf16x8(f.b[j][0], f.b[j][1], s)
@@ -427,7 +439,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     // hold padding only, so their operand reads and MFMAs are skipped.
     // Order of one sub-step's instructions: its MFMAs with the next sub-step's operand reads
     // (sub-step ks2 of the same or the next stage) threaded between them, one read after each
-    // MFMA, so the reads have the remaining MFMAs' time to land.
+    // MFMA.  Measured 2-4 % faster than issuing all the reads first behind an explicit wait.
     auto interleave = [&](auto ks2, auto ml) {
         constexpr int K2 = decltype(ks2)::value, ML = decltype(ml)::value;
         constexpr bool kReadsB = kFp4 ? K2 == 0 : (kFp8 ? K2 % 2 == 0 : true);
@@ -486,8 +498,10 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     static_for<0, NS>([&](auto s) { issue(min(decltype(s)::value, nk - 1), stA(s), stB(s), s); });
     // one main loop per live sub-tile count (in steps of MLQ sub-tiles for tall tiles)
     constexpr int MLQ = kMI > 4 ? 2 : 1;
-    const int mlive = __builtin_amdgcn_readfirstlane(min(kMI, (min(len - m0, kBM) + 32 * MLQ - 1) / (32 * MLQ) * MLQ));
-    static_for<1, kMI / MLQ + 1>([&](auto q) {
+    const int wrows = min(max(len - m0 - wm * kWaveRows, 0), kWaveRows);   // real rows of this wave
+    const int mlive = __builtin_amdgcn_readfirstlane((wrows + 32 * MLQ - 1) / (32 * MLQ) * MLQ);
+    // (a wave of a tall tile may hold no real rows; it still moves its share of the stages)
+    static_for<(kWavesM > 1 ? 0 : 1), kMI / MLQ + 1>([&](auto q) {
         constexpr int ML = decltype(q)::value * MLQ;
         if (mlive == ML) mainloop(ic<ML>{});
     });
