@@ -56,6 +56,14 @@ namespace ftmoe {
 #ifndef FT_GEMV_D_FP4
 #define FT_GEMV_D_FP4 1
 #endif
+// fp8 and MXFP4 batch depth of the one-M-tile kernels (few tokens): their smaller register and
+// LDS footprint leaves room for two K blocks in flight per batch
+#ifndef FT_GEMV_D1_FP8
+#define FT_GEMV_D1_FP8 2
+#endif
+#ifndef FT_GEMV_D1_FP4
+#define FT_GEMV_D1_FP4 2
+#endif
 #ifndef FT_GEMV_LDS
 #define FT_GEMV_LDS 1
 #endif
@@ -70,11 +78,19 @@ enum { EPI_GATEUP = 0, EPI_DOWN = 1 };
 
 template <int WT> struct WTr;
 // kLoads: 16-byte weight loads per lane per 128-wide K block; kBlock: bytes of one row's
-// 128-wide K block; kBatch: K blocks in flight ahead
-template <> struct WTr<FT_DT_F32> { static constexpr int kLoads = 8, kBlock = 512, kBatch = FT_GEMV_D_F32; };
-template <> struct WTr<FT_DT_BF16> { static constexpr int kLoads = 4, kBlock = 256, kBatch = FT_GEMV_D_BF16; };
-template <> struct WTr<FT_DT_FP8E4M3FN_B128> { static constexpr int kLoads = 2, kBlock = 128, kBatch = FT_GEMV_D_FP8; };
-template <> struct WTr<FT_DT_MXFP4> { static constexpr int kLoads = 1, kBlock = 64, kBatch = FT_GEMV_D_FP4; };
+// 128-wide K block; kBatch: K blocks in flight ahead (kBatch1 in the one-M-tile kernels)
+template <> struct WTr<FT_DT_F32> {
+    static constexpr int kLoads = 8, kBlock = 512, kBatch = FT_GEMV_D_F32, kBatch1 = FT_GEMV_D_F32;
+};
+template <> struct WTr<FT_DT_BF16> {
+    static constexpr int kLoads = 4, kBlock = 256, kBatch = FT_GEMV_D_BF16, kBatch1 = FT_GEMV_D_BF16;
+};
+template <> struct WTr<FT_DT_FP8E4M3FN_B128> {
+    static constexpr int kLoads = 2, kBlock = 128, kBatch = FT_GEMV_D_FP8, kBatch1 = FT_GEMV_D1_FP8;
+};
+template <> struct WTr<FT_DT_MXFP4> {
+    static constexpr int kLoads = 1, kBlock = 64, kBatch = FT_GEMV_D_FP4, kBatch1 = FT_GEMV_D1_FP4;
+};
 
 __device__ __forceinline__ u32x4_t ld16(const void *p) {
     return *reinterpret_cast<const u32x4_t *>(p);
@@ -148,19 +164,23 @@ __device__ __forceinline__ void mfma_kblock(const u32x4_t (&av)[ALd<WT>::n], con
 }
 
 // One work item = (group, NB x 16 weight rows).  The 4 waves of the workgroup split the item's
-// K blocks into contiguous quarters and meet in LDS; rows of the group are taken 16 at a time
-// (one MFMA M tile per pass).  Each activation load feeds the NB weight blocks of the item.
-template <int WT, int EPI, int NB>
+// K blocks into contiguous quarters and meet in LDS; rows of the group are taken 16 at a time,
+// up to MTX M tiles per pass (MTX = 1 when no group can hold more than 16 rows, which keeps the
+// register count, and so the occupancy, of few-token calls down).  Each activation load feeds
+// the NB weight blocks of the item.
+template <int WT, int EPI, int NB, int MTX>
 __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int tiles) {
-    constexpr int D = WTr<WT>::kBatch, NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
+    constexpr int D = MTX == 1 ? WTr<WT>::kBatch1 : WTr<WT>::kBatch, NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
     constexpr int COLS = NB * 16;
     constexpr int KB = WTr<WT>::kBlock;                        // bytes of one row's K block
     constexpr int STAGE = FT_GEMV_LDS ? D * NB * 16 * KB : 0; // per wave
-    constexpr int RED = kGemvWaves * 16 * (COLS + 1) * 4;
-    // the per-wave staging areas and the cross-wave reduction are disjoint: a wave writes its
-    // partial sums as soon as its own K range is done, while other waves may still be streaming
-    __shared__ __attribute__((aligned(1024))) uint8_t s_lds[kGemvWaves * STAGE + RED];
-    auto s_red = reinterpret_cast<float (*)[16][COLS + 1]>(s_lds + kGemvWaves * STAGE);
+    constexpr int REDW = 16 * (COLS + 1) * 4;                  // one wave's partial sums
+    constexpr int PW = ((STAGE > REDW ? STAGE : REDW) + 255) / 256 * 256;
+    // A wave writes its partial sums into its own staging area once its own K range is done (its
+    // staged rows have all been read into registers by then); the area stays private to the wave
+    // until the barrier, while other waves may still be streaming into theirs.
+    __shared__ __attribute__((aligned(1024))) uint8_t s_lds[kGemvWaves * PW];
+    auto s_red = [&](int w) { return reinterpret_cast<float (*)[COLS + 1]>(s_lds + w * PW); };
     if constexpr (EPI == EPI_GATEUP) {
         // zero the output that the down projection accumulates into
         const size_t n4 = static_cast<size_t>(a.T) * a.H / 4;
@@ -217,13 +237,13 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                              (static_cast<size_t>(slot) * nrows + wr) * row_bytes + wswz<KB>(j, lane % LPR) * 16;
             }
     }
-    uint8_t *wst = s_lds + wave * STAGE;
+    uint8_t *wst = s_lds + wave * PW;
     const size_t a_elem = (WT == FT_DT_F32) ? 4 : 2;
     const int per = (nkb + kGemvWaves - 1) / kGemvWaves;
     const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
 
     // One pass over the K blocks for MT 16-row M tiles starting at row r0 (MT chosen per pass).
-    auto pass = [&](auto mt_const, int r0, floatx4_t (&acc)[FT_GEMV_MT_MAX][NB]) {
+    auto pass = [&](auto mt_const, int r0, floatx4_t (&acc)[MTX][NB]) {
         constexpr int MT = decltype(mt_const)::value;
         const uint8_t *arow[MT];
 #pragma unroll
@@ -315,15 +335,19 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
         }
     };
 
-    for (int r0 = 0; r0 < len; r0 += 16 * FT_GEMV_MT_MAX) {
-        floatx4_t acc[FT_GEMV_MT_MAX][NB];
+    for (int r0 = 0; r0 < len; r0 += 16 * MTX) {
+        floatx4_t acc[MTX][NB];
 #pragma unroll
-        for (int mt = 0; mt < FT_GEMV_MT_MAX; ++mt)
+        for (int mt = 0; mt < MTX; ++mt)
 #pragma unroll
             for (int b = 0; b < NB; ++b) acc[mt][b] = floatx4_t{0.f, 0.f, 0.f, 0.f};
-        const int nmt = min(FT_GEMV_MT_MAX, (len - r0 + 15) / 16);
-        if (FT_GEMV_MT_MAX > 1 && nmt > 1) pass(std::integral_constant<int, FT_GEMV_MT_MAX>{}, r0, acc);
-        else pass(std::integral_constant<int, 1>{}, r0, acc);
+        const int nmt = min(MTX, (len - r0 + 15) / 16);
+        if constexpr (MTX > 1) {
+            if (nmt > 1) pass(std::integral_constant<int, MTX>{}, r0, acc);
+            else pass(std::integral_constant<int, 1>{}, r0, acc);
+        } else {
+            pass(std::integral_constant<int, 1>{}, r0, acc);
+        }
 
         // lane (n, q) holds rows 4q + i of column n of every block; the 4 K quarters meet in LDS
         for (int mt = 0; mt < nmt; ++mt) {
@@ -334,9 +358,9 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                 for (int i = 0; i < 4; ++i) {
                     float v = acc[0][b][i];
 #pragma unroll
-                    for (int j = 1; j < FT_GEMV_MT_MAX; ++j)
+                    for (int j = 1; j < MTX; ++j)
                         if (j == mt) v = acc[j][b][i];
-                    s_red[wave][4 * q + i][b * 16 + n] = v;
+                    s_red(wave)[4 * q + i][b * 16 + n] = v;
                 }
             __syncthreads();
             if constexpr (EPI == EPI_GATEUP) {
@@ -348,8 +372,8 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                         float gs = 0.f, us = 0.f;
 #pragma unroll
                         for (int w = 0; w < kGemvWaves; ++w) {
-                            gs += s_red[w][m][b * 16 + c];
-                            us += s_red[w][m][b * 16 + c + 8];
+                            gs += s_red(w)[m][b * 16 + c];
+                            us += s_red(w)[m][b * 16 + c + 8];
                         }
                         const float hv = silu_f32(gs) * us;
                         const size_t o = static_cast<size_t>(beg + r) * I + (tile * NB + b) * 8 + c;
@@ -365,7 +389,7 @@ __global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int t
                     if (r < len) {
                         float sum = 0.f;
 #pragma unroll
-                        for (int w = 0; w < kGemvWaves; ++w) sum += s_red[w][m][c];
+                        for (int w = 0; w < kGemvWaves; ++w) sum += s_red(w)[m][c];
                         const int tok = a.wv.row_tok[beg + r];
                         unsafeAtomicAdd(a.out + static_cast<size_t>(tok) * H + tile * COLS + c,
                                         a.wv.row_gate[beg + r] * sum);
@@ -389,8 +413,13 @@ static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
     auto go = [&](auto nb) {
         constexpr int NB = decltype(nb)::value;
         const int tiles = EPI == EPI_GATEUP ? a.I / (8 * NB) : a.H / (16 * NB);
-        hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
-                           s, a, tiles);
+        // a group holds at most T rows (plus nothing: the shared expert's group holds exactly T)
+        if (a.T <= 16)
+            hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB, 1>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
+                               s, a, tiles);
+        else
+            hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB, FT_GEMV_MT_MAX>), dim3(a.max_groups * tiles),
+                               dim3(kGemvThreads), 0, s, a, tiles);
     };
     const int pairs = a.T * a.k;
     if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
