@@ -168,9 +168,17 @@ __device__ __forceinline__ void mfma_kblock(const u32x4_t (&av)[ALd<WT>::n], con
 // up to MTX M tiles per pass (MTX = 1 when no group can hold more than 16 rows, which keeps the
 // register count, and so the occupancy, of few-token calls down).  Each activation load feeds
 // the NB weight blocks of the item.
+// Workgroups per CU the bf16 kernels are held to (128 registers a lane, no spills): one more
+// than the register count the compiler picks by itself allows.  The fp8 and MXFP4 kernels would
+// spill under the same bound and keep the compiler's choice.
+template <int WT> constexpr int gemv_min_blocks() { return WT == FT_DT_BF16 ? 4 : 1; }
+
 template <int WT, int EPI, int NB, int MTX>
-__global__ __launch_bounds__(kGemvThreads) void grouped_gemv(ExpertArgs a, int tiles) {
-    constexpr int D = MTX == 1 ? WTr<WT>::kBatch1 : WTr<WT>::kBatch, NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
+__global__ __launch_bounds__(kGemvThreads, gemv_min_blocks<WT>()) void grouped_gemv(ExpertArgs a, int tiles) {
+    // the deeper batch of the one-M-tile kernels is used where the registers allow it (not by
+    // the wide fp8 items)
+    constexpr int D = (MTX == 1 && (WT != FT_DT_FP8E4M3FN_B128 || NB == 2)) ? WTr<WT>::kBatch1 : WTr<WT>::kBatch;
+    constexpr int NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
     constexpr int COLS = NB * 16;
     constexpr int KB = WTr<WT>::kBlock;                        // bytes of one row's K block
     constexpr int STAGE = FT_GEMV_LDS ? D * NB * 16 * KB : 0; // per wave
