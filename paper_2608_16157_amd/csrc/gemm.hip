@@ -73,8 +73,9 @@ constexpr int kBandM = FT_GEMM_BAND;  // M tiles that run together on each weigh
 
 enum { GEMM_GATEUP = 0, GEMM_DOWN = 1 };
 
-// Per weight format: K values per stage and ring depth (two workgroups of either fit one CU's
-// LDS), bytes per weight element.
+// Per weight format: K values per stage (BK), ring slots (NS: two workgroups of the default tile
+// fit one CU's LDS; after the hand-off in a stage's last sub-step up to NS - 1 later stages are
+// in flight) and weight row bytes per stage (BRB).
 #ifndef FT_GEMM_BF16_BK
 #define FT_GEMM_BF16_BK 32
 #endif
