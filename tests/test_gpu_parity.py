@@ -193,6 +193,7 @@ RANDOM_FWD = [
     (22, workloads.DT_FP8, 0, 16, 4, 20, 10, False, 256, 384, 0.0),    # fp8, two tiles, narrow
     (23, workloads.DT_MXFP4, 1, 16, 4, 16, 12, True, 256, 256, 0.0),   # MXFP4, one tile, wide
     (24, workloads.DT_BF16, 0, 16, 4, 16, 16, True, 384, 256, 0.0),    # bf16, T = 16 exactly
+    (25, workloads.DT_FP8, 1, 8, 4, 60, 8, True, 256, 256, 0.0),       # fp8 wide gate/up, 4 M tiles a pass
 ]
 
 
