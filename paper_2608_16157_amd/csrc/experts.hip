@@ -64,12 +64,6 @@ namespace ftmoe {
 #ifndef FT_GEMV_D1_FP4
 #define FT_GEMV_D1_FP4 2
 #endif
-#ifndef FT_GEMV_LDS
-#define FT_GEMV_LDS 1
-#endif
-#ifndef FT_GEMV_NT_LOADS
-#define FT_GEMV_NT_LOADS 0
-#endif
 
 constexpr int kGemvThreads = 256;
 constexpr int kGemvWaves = kGemvThreads / kWave;
@@ -95,18 +89,17 @@ template <> struct WTr<FT_DT_MXFP4> {
 __device__ __forceinline__ u32x4_t ld16(const void *p) {
     return *reinterpret_cast<const u32x4_t *>(p);
 }
-__device__ __forceinline__ u32x4_t ld16_stream(const void *p) {
-    return __builtin_nontemporal_load(reinterpret_cast<const u32x4_t *>(p));
-}
 
 typedef __attribute__((address_space(3))) void gemv_lds_t;
 
-// Weight staging through LDS (FT_GEMV_LDS): a wave copies its own K block of the item's weight
+// Weight staging through LDS: a wave copies its own K block of the item's weight
 // rows into its own LDS region with global_load_lds, 16 bytes per lane and whole rows per
 // instruction (a 16x16x32 MFMA operand read straight from global memory would take only 64 bytes
 // of each of 16 rows per instruction), then reads the MFMA operands from there.  Within a row
 // the 16-byte chunks are XOR-swizzled by the row so that the operand reads of 16 rows hit 16
-// distinct bank groups: row bytes KB = 64 (MXFP4), 128 (fp8), 256 (bf16) or 512 (f32).
+// distinct bank groups: row bytes KB = 64 (MXFP4), 128 (fp8), 256 (bf16) or 512 (f32).  (Loading
+// the operands into registers straight from global memory, with or without non-temporal hints,
+// was measured slower.)
 __device__ __forceinline__ void gemv_dma16(const void *g, uint8_t *lds) {
     __builtin_amdgcn_global_load_lds(g, (gemv_lds_t *)(lds), 16, 0, 0);
 }
@@ -118,10 +111,6 @@ __device__ __forceinline__ int wswz(int row, int chunk) {
     else return chunk ^ (row & 15);
 }
 
-// Byte offset (within a row's 128-wide K block) of a lane's 16-byte weight load number c: the
-// K values it holds are c * 16 + q * 4 (f32, 4 values), c * 32 + q * 8 (bf16, 8), c * 64 + q * 16
-// (fp8, 16) and q * 32 (MXFP4, 32), i.e. chunk 4 c + q of the row's block.
-template <int WT> __device__ __forceinline__ int wbyte(int c, int q) { return (4 * c + q) * 16; }
 
 // Activation loads of one 128-wide K block for one 16-row M tile, 16 bytes each, at the K
 // offsets the lane's weight operand uses (f32: 8 x 4 floats at c*16 + q*4; bf16: 4 x 8 at
@@ -181,7 +170,7 @@ __global__ __launch_bounds__(kGemvThreads, gemv_min_blocks<WT>()) void grouped_g
     constexpr int NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
     constexpr int COLS = NB * 16;
     constexpr int KB = WTr<WT>::kBlock;                        // bytes of one row's K block
-    constexpr int STAGE = FT_GEMV_LDS ? D * NB * 16 * KB : 0; // per wave
+    constexpr int STAGE = D * NB * 16 * KB;                   // per wave
     constexpr int REDW = 16 * (COLS + 1) * 4;                  // one wave's partial sums
     constexpr int PW = ((STAGE > REDW ? STAGE : REDW) + 255) / 256 * 256;
     // A wave writes its partial sums into its own staging area once its own K range is done (its
@@ -209,15 +198,12 @@ __global__ __launch_bounds__(kGemvThreads, gemv_min_blocks<WT>()) void grouped_g
     // weight row of this lane's N column in block b: a gate/up block pairs 8 gate rows with the
     // 8 matching up rows, so SiLU(gate) * up of one h column stays inside the block
     const size_t row_bytes = static_cast<size_t>(nkb) * KB;
-    const uint8_t *wbase[NB];
     const float *sbase[NB];      // fp8: the row's 128 x 128 block scales
     const uint8_t *xbase[NB];    // MXFP4: this lane's e8m0 scale of the row in K block 0
 #pragma unroll
     for (int b = 0; b < NB; ++b) {
         const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
         const int wrow = EPI == EPI_GATEUP ? (n < 8 ? col0 + n : I + col0 + n - 8) : col0 + n;
-        wbase[b] = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.w13 : a.w2) +
-                   (static_cast<size_t>(slot) * nrows + wrow) * row_bytes;
         sbase[b] = nullptr;
         xbase[b] = nullptr;
         if constexpr (WT == FT_DT_FP8E4M3FN_B128)
@@ -231,20 +217,18 @@ __global__ __launch_bounds__(kGemvThreads, gemv_min_blocks<WT>()) void grouped_g
     // the block's 16, LPR lanes per row; lane i fills LDS chunk i % LPR of its row, so it fetches
     // the chunk the swizzle puts there
     constexpr int LPR = KB / 16, RPI = 64 / LPR;
-    static_assert(!FT_GEMV_LDS || RPI * NL == 16, "one block is NL whole-row instructions");
+    static_assert(RPI * NL == 16, "one block is NL whole-row instructions");
     const uint8_t *dsrc[NB][NL];
-    if constexpr (FT_GEMV_LDS) {
 #pragma unroll
-        for (int b = 0; b < NB; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
-            for (int c = 0; c < NL; ++c) {
-                const int j = c * RPI + lane / LPR;
-                const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
-                const int wr = EPI == EPI_GATEUP ? (j < 8 ? col0 + j : I + col0 + j - 8) : col0 + j;
-                dsrc[b][c] = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.w13 : a.w2) +
-                             (static_cast<size_t>(slot) * nrows + wr) * row_bytes + wswz<KB>(j, lane % LPR) * 16;
-            }
-    }
+        for (int c = 0; c < NL; ++c) {
+            const int j = c * RPI + lane / LPR;
+            const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
+            const int wr = EPI == EPI_GATEUP ? (j < 8 ? col0 + j : I + col0 + j - 8) : col0 + j;
+            dsrc[b][c] = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.w13 : a.w2) +
+                         (static_cast<size_t>(slot) * nrows + wr) * row_bytes + wswz<KB>(j, lane % LPR) * 16;
+        }
     uint8_t *wst = s_lds + wave * PW;
     const size_t a_elem = (WT == FT_DT_F32) ? 4 : 2;
     const int per = (nkb + kGemvWaves - 1) / kGemvWaves;
@@ -283,20 +267,13 @@ __global__ __launch_bounds__(kGemvThreads, gemv_min_blocks<WT>()) void grouped_g
 #pragma unroll
                 for (int b = 0; b < NB; ++b) {
 #pragma unroll
-                    for (int c = 0; c < NL; ++c) {
-                        if constexpr (FT_GEMV_LDS) {
-                            gemv_dma16(dsrc[b][c] + static_cast<size_t>(kb) * KB,
-                                       wst + ((d * NB + b) * 16 * KB + c * 1024));
-                        } else {
-                            const uint8_t *p = wbase[b] + static_cast<size_t>(kb) * KB + wbyte<WT>(c, q);
-                            wv[d][b][c] = FT_GEMV_NT_LOADS ? ld16_stream(p) : ld16(p);
-                        }
-                    }
+                    for (int c = 0; c < NL; ++c)
+                        gemv_dma16(dsrc[b][c] + static_cast<size_t>(kb) * KB, wst + ((d * NB + b) * 16 * KB + c * 1024));
                     if constexpr (WT == FT_DT_FP8E4M3FN_B128) sv[d][b] = sbase[b][kb];
                     if constexpr (WT == FT_DT_MXFP4) xv[d][b] = xbase[b][static_cast<size_t>(kb) * 4 * nrows];
                 }
             }
-            if constexpr (FT_GEMV_LDS) {
+            {
                 // this wave's staged rows have landed (its own DMA: no barrier needed); lane
                 // (n, q)'s operand chunk c is chunk 4 c + q of row n
                 __builtin_amdgcn_s_waitcnt(0x0 | (0x7 << 4) | (0xF << 8) | (0x0 << 14));   // vmcnt(0)
