@@ -617,10 +617,19 @@ __global__ __launch_bounds__(1024) void route_scan(RouteArgs a, int nblk) {
     const int per = (nblk + parts - 1) / parts;
     const int b0 = min(nblk, part * per), b1 = min(nblk, b0 + per);
     const bool active = part < parts;
+    // each thread's column range is read kScanBatch entries at a time, all in flight together
+    // (one workgroup does the whole scan, so its memory latency is the scan's cost)
+    constexpr int kScanBatch = 32;
     if (active) {
         int sum = 0;
-#pragma unroll 8
-        for (int b = b0; b < b1; ++b) sum += a.wv.blk_hist[static_cast<size_t>(b) * E + e];
+        for (int b = b0; b < b1; b += kScanBatch) {
+            int buf[kScanBatch];
+            // clamped, unconditional loads; entries past the range count 0
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i) buf[i] = a.wv.blk_hist[static_cast<size_t>(min(b + i, b1 - 1)) * E + e];
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i) sum += b + i < b1 ? buf[i] : 0;
+        }
         s_part[part * E + e] = sum;
     }
     __syncthreads();
@@ -639,19 +648,21 @@ __global__ __launch_bounds__(1024) void route_scan(RouteArgs a, int nblk) {
     __syncthreads();
     if (active) {
         int run = s_part[part * E + e] + (s_eff[e] >= 0 ? s_hoff[e] : s_moff[e]);
-        int buf[8];
-        for (int b = b0; b < b1; b += 8) {
-            const int n = min(8, b1 - b);
+        for (int b = b0; b < b1; b += kScanBatch) {
+            // all loads of the batch, then the running offsets, then all stores (a store between
+            // two loads would make each wait cover the store too)
+            int buf[kScanBatch];
 #pragma unroll
-            for (int i = 0; i < 8; ++i)
-                buf[i] = i < n ? a.wv.blk_hist[static_cast<size_t>(b + i) * E + e] : 0;
+            for (int i = 0; i < kScanBatch; ++i) buf[i] = a.wv.blk_hist[static_cast<size_t>(min(b + i, b1 - 1)) * E + e];
+            int off[kScanBatch];
 #pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                if (i < n) {
-                    a.wv.blk_hist[static_cast<size_t>(b + i) * E + e] = run;
-                    run += buf[i];
-                }
+            for (int i = 0; i < kScanBatch; ++i) {
+                off[i] = run;
+                run += b + i < b1 ? buf[i] : 0;
             }
+#pragma unroll
+            for (int i = 0; i < kScanBatch; ++i)
+                if (b + i < b1) a.wv.blk_hist[static_cast<size_t>(b + i) * E + e] = off[i];
         }
     }
 }
