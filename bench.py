@@ -490,8 +490,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures one MI355X: the MoE layer over a GPU expert cache runs on a single "
-              "GPU (no sharding or collectives in this build); run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one MI355X: this library runs the MoE layer over a GPU expert cache "
+              "on a single GPU (no sharding or collectives); run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import torch
