@@ -287,6 +287,54 @@ def hybrid_decode(cfg_name, T, steps, warmup, n_slots, b_pcie, b_host, max_fill)
         "cpu_experts_per_step": round(cpus / steps, 2)}), flush=True)
 
 
+def cache_plan_timing(cfg_name, T, steps, warmup, n_slots, b_pcie, b_host, max_fill):
+    """Device-side cache control alone (ft_route_only then ft_cache_plan, row f1) over decode
+    steps whose cache state evolves: HIP events on the library's stream around each call.  The
+    host issues one step at a time, so these intervals include the launch gaps; the kernels'
+    own durations come from a kernel trace of the same run."""
+    import torch
+    import paper_2608_16157_amd as ftm
+    import workloads
+    cfg = workloads.CONFIGS[cfg_name]
+    E = cfg.n_experts
+    desc = dict(hidden=cfg.hidden, inter=cfg.inter, n_experts=E, top_k=cfg.top_k, gating=cfg.gating,
+                w_dtype=cfg.w_dtype, x_dtype=cfg.x_dtype, n_slots=n_slots, shared_slot=-1)
+    table = torch.full((E,), -1, dtype=torch.int32, device="cuda")
+    state = ftm.CacheState(torch.full((n_slots,), -1, dtype=torch.int32, device="cuda"),
+                           torch.zeros(n_slots, dtype=torch.int32, device="cuda"))
+    route = ftm.RouteBuffers(T, cfg.top_k, E)
+    plan = ftm.FillPlanBuffers(max_fill, E)
+    ws = ftm.alloc_workspace(desc, T)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(78)
+    rank = torch.randperm(E, generator=g, device="cuda").float() + 1
+    bias = -cfg.zipf_s * torch.log(rank)
+    n = warmup + steps
+    logits = [torch.randn(T, E, generator=g, device="cuda") + bias[None, :] for _ in range(n)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
+    counts = []
+    for i in range(n):
+        e0, e1, e2 = evs[i]
+        e0.record()
+        ftm.ft_route_only(desc, logits[i], table, T, route, ws)
+        e1.record()
+        ftm.ft_cache_plan(desc, route, T, table, state, b_pcie, b_host, max_fill, i + 1, plan)
+        e2.record()
+        if i >= warmup:
+            counts.append(plan.counts.clone())
+    torch.cuda.synchronize()
+    r_us = sum(evs[i][0].elapsed_time(evs[i][1]) for i in range(warmup, n)) * 1e3 / steps
+    p_us = sum(evs[i][1].elapsed_time(evs[i][2]) for i in range(warmup, n)) * 1e3 / steps
+    c = torch.stack(counts).float().mean(0).tolist()
+    print(json.dumps({
+        "measurement": "device-side cache control: ft_route_only then ft_cache_plan per decode step",
+        "workload": f"{cfg_name} shapes, T={T}, {n_slots} of {E} experts cacheable, Zipf {cfg.zipf_s} "
+                    f"routing, B_P={b_pcie} B_H={b_host} GB/s, K={max_fill}, {steps} steps",
+        "route_us_with_launch": round(r_us, 2), "cache_plan_us_with_launch": round(p_us, 2),
+        "fills_per_step": round(c[0], 2), "cpu_experts_per_step": round(c[1], 2),
+        "missing_experts_per_step": round(c[2], 2)}), flush=True)
+
+
 def prefill_pipeline(cfg_name, T, n_layers, reps):
     """Full-layer double-buffered prefill (ft_prefill_layers): a T-token chunk through n_layers
     MoE layers whose complete expert sets are loaded from pinned host memory, with the loads
@@ -466,7 +514,9 @@ def main():
                     help="measure B_P (fills over PCIe) and B_H (CPU branch) for --config, then exit")
     ap.add_argument("--hybrid", action="store_true",
                     help="time complete decode steps with fills and the CPU branch, then exit")
-    ap.add_argument("--slots", type=int, default=64, help="cache slots for --hybrid")
+    ap.add_argument("--cache-plan", action="store_true",
+                    help="time device-side cache control (ft_route_only + ft_cache_plan) per decode step")
+    ap.add_argument("--slots", type=int, default=64, help="cache slots for --hybrid / --cache-plan")
     ap.add_argument("--b-pcie", type=float, default=50.0, help="B_P (GB/s) for --hybrid")
     ap.add_argument("--b-host", type=float, default=60.0, help="B_H (GB/s) for --hybrid")
     ap.add_argument("--max-fill", type=int, default=8, help="K for --hybrid")
@@ -510,6 +560,10 @@ def main():
         return
     if args.prefill_pipeline:
         prefill_pipeline(args.config, args.tokens, args.layers, max(1, args.steps))
+        return
+    if args.cache_plan:
+        cache_plan_timing(args.config, args.tokens, args.steps, args.warmup, args.slots, args.b_pcie,
+                          args.b_host, args.max_fill)
         return
     if args.hybrid:
         hybrid_decode(args.config, args.tokens, args.steps, args.warmup, args.slots, args.b_pcie,
