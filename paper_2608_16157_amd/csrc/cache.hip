@@ -6,9 +6,11 @@
 // consumes the first q of them and rewrites routed ids into slot ids, leaving a fixed-shape copy
 // list with a valid count).
 //
-// One workgroup.  Phases, separated by barriers:
+// One workgroup, one thread per expert (E <= 1024).  Phases, separated by barriers:
 //   1  cache state and per-expert demand into LDS (the routing's hit/miss offsets give, per
-//      expert, the pairs that hit and the pairs that missed);
+//      expert, the pairs that hit and the pairs that missed); every per-expert value the later
+//      phases need is loaded here, in one batch, and kept in the thread's registers, so the
+//      kernel waits on global memory once before its last phase;
 //   2  every hit expert marks its slot as used in this step;
 //   3  every evictable slot (not hit, not the shared expert's) gets its rank by
 //      (age, slot id), age 0 for an empty slot and stamp + 1 otherwise; ranks below K are the
@@ -25,6 +27,7 @@
 namespace ftmoe {
 
 constexpr int kPlanThreads = 1024;
+static_assert(kMaxExperts <= kPlanThreads, "one thread per expert");
 
 __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
     extern __shared__ uint64_t plan_lds[];
@@ -39,20 +42,23 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
 
     // ---- 1
     const int status = a.route_counts[3], m = a.route_counts[2];
+    // this thread's expert e = tid: its missed pairs [mo0, mo1), whether it hit, its slot
+    const int e_me = tid;
+    const bool has_e = e_me < E;
+    const int mo0 = has_e ? a.miss_off[e_me] : 0, mo1 = has_e ? a.miss_off[e_me + 1] : 0;
+    const bool hit = has_e && a.hit_off[e_me + 1] > a.hit_off[e_me];
+    const int slot_me = has_e ? a.slot_table[e_me] : -1;
     for (int s = tid; s < S; s += kPlanThreads) {
         s_owner[s] = a.slot_expert[s];
         s_key[s] = s == a.shared_slot ? kNotEvictable
                                       : (s_owner[s] < 0 ? 0ull : static_cast<uint64_t>(a.slot_stamp[s]) + 1ull);
     }
-    for (int e = tid; e < E; e += kPlanThreads) s_dem[e] = a.miss_off[e + 1] - a.miss_off[e];
+    if (has_e) s_dem[e_me] = mo1 - mo0;
     if (tid == 0) s_misc[0] = 0;
     __syncthreads();
 
     // ---- 2
-    if (status == 0) {
-        for (int e = tid; e < E; e += kPlanThreads)
-            if (a.hit_off[e + 1] > a.hit_off[e]) s_key[a.slot_table[e]] = kNotEvictable;
-    }
+    if (status == 0 && hit) s_key[slot_me] = kNotEvictable;
     __syncthreads();
 
     // ---- 3
@@ -99,9 +105,8 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
 
     // ---- 5
     const int q = s_misc[1];
-    for (int e = tid; e < E; e += kPlanThreads) {
-        if (s_dem[e] == 0) continue;
-        const int i = s_rank[e];
+    if (has_e && mo1 > mo0) {
+        const int e = e_me, i = s_rank[e];
         if (i < q) {
             const int v = s_cand[i], old = s_owner[v];
             a.fill_expert[i] = e;
@@ -111,7 +116,7 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
             a.slot_table[e] = v;
             a.slot_expert[v] = e;
             a.slot_stamp[v] = a.step;
-            for (int j = a.miss_off[e]; j < a.miss_off[e + 1]; ++j) a.topk_slot[a.miss_pairs[j]] = v;
+            for (int j = mo0; j < mo1; ++j) a.topk_slot[a.miss_pairs[j]] = v;
         } else {
             // position among the missing experts left to the CPU, in id order
             int pos = 0;
@@ -119,10 +124,7 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
             a.cpu_expert[pos] = e;
         }
     }
-    if (status == 0) {
-        for (int e = tid; e < E; e += kPlanThreads)
-            if (a.hit_off[e + 1] > a.hit_off[e]) a.slot_stamp[a.slot_table[e]] = a.step;   // hits keep their slot
-    }
+    if (status == 0 && hit) a.slot_stamp[slot_me] = a.step;   // hits keep their slot
     for (int i = q + tid; i < K; i += kPlanThreads) {
         a.fill_expert[i] = -1;
         a.fill_slot[i] = -1;
