@@ -108,6 +108,26 @@ def test_route_bit_exact_random(seed, E, k, T, ties):
     check_route(route, oracle.route(desc, logits, st), T, k)
 
 
+# One or two tokens (at most 64 pairs) are routed by a single wave: its edges are 8 experts per
+# lane, k = 64 and two tokens of 32 choices (every lane holds a pair), an expert count that is not
+# a multiple of 64, sigmoid gating, and the shared expert's rows after the hit rows.
+@pytest.mark.parametrize("seed,E,k,T,ties,gating,shared",
+                         [(20, 512, 8, 2, True, workloads.GATE_SOFTMAX, False),
+                          (21, 256, 64, 1, False, workloads.GATE_SOFTMAX, True),
+                          (22, 300, 6, 2, True, workloads.GATE_SIGMOID, True),
+                          (23, 64, 32, 2, False, workloads.GATE_SOFTMAX, False),
+                          (24, 200, 3, 1, True, workloads.GATE_SIGMOID, True),
+                          (25, 8, 2, 2, True, workloads.GATE_SOFTMAX, False)])
+def test_route_bit_exact_single_wave(seed, E, k, T, ties, gating, shared):
+    _say(f"route single-wave seed={seed} E={E} k={k} T={T} shared={shared}")
+    lay = workloads.random_layer(seed, hidden=128, inter=128, n_experts=E, top_k=k, tokens=T,
+                                 gating=gating, tie_logits=ties, shared=shared,
+                                 zipf_s=1.0 if seed % 2 else 0.0, device="cuda")
+    route = run_route(lay)
+    desc, banks, logits, st, x = oracle_inputs(lay)
+    check_route(route, oracle.route(desc, logits, st), T, k)
+
+
 def test_route_deterministic():
     lay = _route_only_layer("dsv3_prefill", 8192)
     a, b = run_route(lay), run_route(lay)
@@ -116,7 +136,7 @@ def test_route_deterministic():
         assert torch.equal(getattr(a, n), getattr(b, n)), n
 
 
-@pytest.mark.parametrize("T", [5, 700])
+@pytest.mark.parametrize("T", [2, 5, 700])
 def test_invalid_slot_tables_flagged_and_treated_as_misses(T):
     lay = workloads.random_layer(11, hidden=128, inter=128, n_experts=16, top_k=4, tokens=T,
                                  n_resident=10, shared=True, device="cuda")
