@@ -404,14 +404,16 @@ static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
         // a group holds at most T rows (the shared expert's group exactly T).  The wide fp8
         // gate/up items take four M tiles per pass above 32 tokens: a group of up to 64 rows
         // then streams its weights once, at no cost in occupancy (their register count allows
-        // two waves per SIMD either way); measured +4 % on that kernel at dsv3 T = 64.
+        // two waves per SIMD either way); measured +4 % on that kernel at dsv3 T = 64.  The wide
+        // MXFP4 gate/up items do so from 64 tokens (their occupancy halves: measured -1 % at
+        // T = 48, +1 % at T = 64, +4 % at T = 128).
         if (a.T <= 16) {
             hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB, 1>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
                                s, a, tiles);
             return;
         }
-        if constexpr (WT == FT_DT_FP8E4M3FN_B128 && EPI == EPI_GATEUP && NB == 4) {
-            if (a.T > 32) {
+        if constexpr ((WT == FT_DT_FP8E4M3FN_B128 || WT == FT_DT_MXFP4) && EPI == EPI_GATEUP && NB == 4) {
+            if (a.T >= (WT == FT_DT_MXFP4 ? 64 : 33)) {
                 hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB, 4>), dim3(a.max_groups * tiles), dim3(kGemvThreads),
                                    0, s, a, tiles);
                 return;

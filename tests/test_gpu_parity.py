@@ -208,12 +208,14 @@ RANDOM_FWD = [
     (19, workloads.DT_MXFP4, 1, 12, 3, 70, 0, True, 256, 256, 0.0),
     (20, workloads.DT_MXFP4, 0, 32, 8, 520, 13, False, 512, 384, 2.0),
     # every streaming-kernel variant the launcher picks: T <= 16 takes the one-M-tile kernels;
-    # fp8 items are wide above 128 pairs, MXFP4 items above 12
+    # fp8 items are wide above 128 pairs, MXFP4 items above 12; the wide gate/up items take four M
+    # tiles a pass above 32 tokens (fp8) or from 64 (MXFP4)
     (21, workloads.DT_FP8, 1, 32, 12, 16, 20, True, 256, 256, 0.0),    # fp8, one tile, wide
     (22, workloads.DT_FP8, 0, 16, 4, 20, 10, False, 256, 384, 0.0),    # fp8, two tiles, narrow
     (23, workloads.DT_MXFP4, 1, 16, 4, 16, 12, True, 256, 256, 0.0),   # MXFP4, one tile, wide
     (24, workloads.DT_BF16, 0, 16, 4, 16, 16, True, 384, 256, 0.0),    # bf16, T = 16 exactly
     (25, workloads.DT_FP8, 1, 8, 4, 60, 8, True, 256, 256, 0.0),       # fp8 wide gate/up, 4 M tiles a pass
+    (26, workloads.DT_MXFP4, 0, 16, 4, 100, 12, True, 256, 256, 0.7),  # MXFP4 wide gate/up, 4 M tiles a pass
 ]
 
 
