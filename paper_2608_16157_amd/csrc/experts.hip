@@ -53,6 +53,13 @@ namespace ftmoe {
 #ifndef FT_GEMV_D_BF16
 #define FT_GEMV_D_BF16 1
 #endif
+// bf16 gate/up batch depth of the kernels with several M tiles a pass (more than 16 tokens): two
+// K blocks a batch halve the workgroups per CU (LDS) and still keep more bytes in flight
+// (measured +2 % on that kernel at Qwen3 T = 32; the down projection and the one-M-tile kernels
+// lost with it)
+#ifndef FT_GEMV_DGU_BF16
+#define FT_GEMV_DGU_BF16 2
+#endif
 #ifndef FT_GEMV_D_FP8
 #define FT_GEMV_D_FP8 1
 #endif
@@ -75,18 +82,23 @@ enum { EPI_GATEUP = 0, EPI_DOWN = 1 };
 
 template <int WT> struct WTr;
 // kLoads: 16-byte weight loads per lane per 128-wide K block; kBlock: bytes of one row's
-// 128-wide K block; kBatch: K blocks in flight ahead (kBatch1 in the one-M-tile kernels)
+// 128-wide K block; kBatch: K blocks in flight ahead (kBatch1 in the one-M-tile kernels, kBatchGU
+// in the gate/up kernels with several M tiles a pass)
 template <> struct WTr<FT_DT_F32> {
-    static constexpr int kLoads = 8, kBlock = 512, kBatch = FT_GEMV_D_F32, kBatch1 = FT_GEMV_D_F32;
+    static constexpr int kLoads = 8, kBlock = 512, kBatch = FT_GEMV_D_F32, kBatch1 = FT_GEMV_D_F32,
+                         kBatchGU = FT_GEMV_D_F32;
 };
 template <> struct WTr<FT_DT_BF16> {
-    static constexpr int kLoads = 4, kBlock = 256, kBatch = FT_GEMV_D_BF16, kBatch1 = FT_GEMV_D_BF16;
+    static constexpr int kLoads = 4, kBlock = 256, kBatch = FT_GEMV_D_BF16, kBatch1 = FT_GEMV_D_BF16,
+                         kBatchGU = FT_GEMV_DGU_BF16;
 };
 template <> struct WTr<FT_DT_FP8E4M3FN_B128> {
-    static constexpr int kLoads = 2, kBlock = 128, kBatch = FT_GEMV_D_FP8, kBatch1 = FT_GEMV_D1_FP8;
+    static constexpr int kLoads = 2, kBlock = 128, kBatch = FT_GEMV_D_FP8, kBatch1 = FT_GEMV_D1_FP8,
+                         kBatchGU = FT_GEMV_D_FP8;
 };
 template <> struct WTr<FT_DT_MXFP4> {
-    static constexpr int kLoads = 1, kBlock = 64, kBatch = FT_GEMV_D_FP4, kBatch1 = FT_GEMV_D1_FP4;
+    static constexpr int kLoads = 1, kBlock = 64, kBatch = FT_GEMV_D_FP4, kBatch1 = FT_GEMV_D1_FP4,
+                         kBatchGU = FT_GEMV_D_FP4;
 };
 
 __device__ __forceinline__ u32x4_t ld16(const void *p) {
@@ -161,15 +173,20 @@ __device__ __forceinline__ void mfma_kblock(const u32x4_t (&av)[ALd<WT>::n], con
 // register count, and so the occupancy, of few-token calls down).  Each activation load feeds
 // the NB weight blocks of the item.
 // Workgroups per CU the bf16 kernels are held to (128 registers a lane, no spills): one more
-// than the register count the compiler picks by itself allows.  The fp8 and MXFP4 kernels would
-// spill under the same bound and keep the compiler's choice.
-template <int WT> constexpr int gemv_min_blocks() { return WT == FT_DT_BF16 ? 4 : 1; }
+// than the register count the compiler picks by itself allows; two for the gate/up kernels whose
+// deeper batches fill that much LDS.  The fp8 and MXFP4 kernels would spill under the same bound
+// and keep the compiler's choice.
+template <int WT, int EPI, int MTX> constexpr int gemv_min_blocks() {
+    return WT != FT_DT_BF16 ? 1 : (EPI == EPI_GATEUP && MTX > 1 && FT_GEMV_DGU_BF16 > 1 ? 2 : 4);
+}
 
 template <int WT, int EPI, int NB, int MTX>
-__global__ __launch_bounds__(kGemvThreads, gemv_min_blocks<WT>()) void grouped_gemv(ExpertArgs a, int tiles) {
+__global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) void grouped_gemv(ExpertArgs a, int tiles) {
     // the deeper batch of the one-M-tile kernels is used where the registers allow it (not by
     // the wide fp8 items)
-    constexpr int D = (MTX == 1 && (WT != FT_DT_FP8E4M3FN_B128 || NB == 2)) ? WTr<WT>::kBatch1 : WTr<WT>::kBatch;
+    constexpr int D = (MTX == 1 && (WT != FT_DT_FP8E4M3FN_B128 || NB == 2))
+                          ? WTr<WT>::kBatch1
+                          : (MTX > 1 && EPI == EPI_GATEUP ? WTr<WT>::kBatchGU : WTr<WT>::kBatch);
     constexpr int NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
     constexpr int COLS = NB * 16;
     constexpr int KB = WTr<WT>::kBlock;                        // bytes of one row's K block
