@@ -2,11 +2,11 @@
  * ftmoe.h -- C ABI of the MoE layer executed against a GPU expert cache (gfx950 / MI355X).
  *
  * What the library computes (FreeToken, Section 3.2 "Decode codesign" and Section 4.1
- * "CUDA-Graph-compatible LRU cache"): at one MoE layer the router and the cache lookup run on
- * the GPU; the routed (token, expert) pairs whose expert is resident in a cache slot form the
- * hit set H and are evaluated on the GPU; the remaining pairs form the miss set M, whose m
- * distinct experts are served elsewhere (CPU execution or a cache fill).  The GPU's partial
- * output and the partial output of the misses add up to the exact layer output.
+ * "CUDA-Graph-compatible LRU cache"): at one MoE layer, gating and the slot-table lookup are
+ * device work.  A routed (token, expert) pair belongs to the hit set H when its expert occupies
+ * a cache slot, and H is evaluated on the GPU; every other pair belongs to the miss set M, and
+ * the m distinct experts of M are left to the host (CPU execution or a cache fill).  Summing the
+ * GPU partial and the partial of the misses gives the layer output exactly.
  *
  * Layer definition used throughout (the paper states it only in words, Section 2):
  *   top-k      S_t = the k experts with the largest float32 logit, ordered by (logit desc,
@@ -150,9 +150,9 @@ typedef struct {
 size_t ft_moe_workspace_bytes(const ft_moe_desc_t *desc, int32_t max_tokens);
 
 /*
- * Router, hit/miss classification and the expert-sorted permutation only (Section 3.2: the
- * router and cache lookup run on the GPU and identify the hits; Section 4.1: routed logical ids
- * are rewritten into slot ids or a CPU-assignment flag).
+ * Router, hit/miss classification and the expert-sorted permutation only (Section 3.2: gating
+ * and the cache lookup are device work that separates hits from misses; Section 4.1: each routed
+ * expert id is replaced by its slot id or by a flag that sends it to the CPU).
  *   logits     [T][E] float32 device
  *   slot_table [E] int32 device: slot of expert e, or -1 if not resident
  *   T >= 0 (T == 0 enqueues nothing and returns FT_OK)
@@ -345,7 +345,7 @@ ft_status_t ft_moe_step_hybrid(const ft_moe_desc_t *desc, const ft_banks_t *dev_
 
 /*
  * Full-layer double-buffered prefill of one chunk of T tokens through n_layers MoE layers whose
- * complete expert sets live in host memory (Section 3.3, prefill: prefill routes nearly every
+ * complete expert sets live in host memory (Section 3.1, "Prefill Codesign": prefill routes nearly every
  * expert of a layer, so experts are not fetched on demand; two full-layer buffers from the slot
  * pool take turns, a transfer stream loading all experts of layer l + 1 into one, before that
  * layer's routing is known, while the GPU evaluates layer l from the other.  Section 5,

@@ -5,8 +5,9 @@ product library never imports or calls it.  It shares no code with the HIP path.
 
 It is a plain, slow, obviously correct restatement of what one MoE layer computes when only
 the experts resident in the GPU expert cache are evaluated (Section 3.2 and Section 4.1 of the
-paper: the router and the cache lookup run on the GPU, resident experts execute there, the
-misses go elsewhere, and the partial sums from both sides add up to the exact layer output).
+paper: gating and the slot lookup happen on the device, cache-resident experts are evaluated
+there, the remaining experts are handled by the host, and adding the two partial sums gives the
+layer output exactly).
 Every floating-point step runs in float64 on exactly decoded weights; results are cast to
 float32 at the end.
 

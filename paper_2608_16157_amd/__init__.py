@@ -172,6 +172,86 @@ def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
     return t.data_ptr()
 
 
+# ------------------------------------------------------------------------------ validation
+# The C ABI carries device pointers without capacities, so every wrapper checks the tensors it
+# passes (device, dtype, element count) against the sizes the call will touch, and raises
+# ValueError before the library is entered.
+
+_X_DTYPES = {FT_DT_F32: torch.float32, FT_DT_BF16: torch.bfloat16}
+_W_DTYPES = {FT_DT_F32: (torch.float32,), FT_DT_BF16: (torch.bfloat16, torch.int16),
+             FT_DT_FP8E4M3FN_B128: (torch.uint8, torch.float8_e4m3fn), FT_DT_MXFP4: (torch.uint8,)}
+_S_DTYPES = {FT_DT_FP8E4M3FN_B128: (torch.float32,), FT_DT_MXFP4: (torch.uint8,)}
+
+
+def expert_bank_bytes(desc: dict) -> tuple:
+    """Bytes of one expert in each bank (w13, w2, s13, s2) for the layout of ``desc``."""
+    H, I, wd = int(desc["hidden"]), int(desc["inter"]), int(desc["w_dtype"])
+    if wd == FT_DT_F32:
+        return 8 * I * H, 4 * H * I, 0, 0
+    if wd == FT_DT_BF16:
+        return 4 * I * H, 2 * H * I, 0, 0
+    if wd == FT_DT_FP8E4M3FN_B128:
+        return 2 * I * H, H * I, (2 * I // 128) * (H // 128) * 4, (H // 128) * (I // 128) * 4
+    return I * H, H * I // 2, 2 * I * (H // 32), H * (I // 32)
+
+
+def _need(t, name: str, dtypes, numel: int, device: str = "cuda") -> None:
+    """Raise ValueError unless ``t`` is a tensor on ``device`` of one of ``dtypes`` holding at
+    least ``numel`` elements."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if device == "cuda" and not t.is_cuda:
+        raise ValueError(f"{name}: must be a device (cuda) tensor")
+    if device == "cpu" and t.is_cuda:
+        raise ValueError(f"{name}: must be a host tensor")
+    if not isinstance(dtypes, tuple):
+        dtypes = (dtypes,)
+    if t.dtype not in dtypes:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {' or '.join(map(str, dtypes))}")
+    if t.numel() < numel:
+        raise ValueError(f"{name}: {t.numel()} elements, the call needs {numel}")
+
+
+def _need_bytes(t, name: str, dtypes, nbytes: int, device: str = "cuda") -> None:
+    _need(t, name, dtypes, 0, device)
+    if t.numel() * t.element_size() < nbytes:
+        raise ValueError(f"{name}: {t.numel() * t.element_size()} bytes, the call needs {nbytes}")
+
+
+def _need_banks(desc: dict, banks: dict, rows: int, name: str, device: str = "cuda") -> None:
+    """Every bank holds ``rows`` expert rows of the layout of ``desc``."""
+    if rows <= 0:
+        return
+    wd = int(desc["w_dtype"])
+    b13, b2, bs13, bs2 = expert_bank_bytes(desc)
+    _need_bytes(banks.get("w13"), f"{name}['w13']", _W_DTYPES[wd], rows * b13, device)
+    _need_bytes(banks.get("w2"), f"{name}['w2']", _W_DTYPES[wd], rows * b2, device)
+    if wd in _S_DTYPES:
+        _need_bytes(banks.get("s13"), f"{name}['s13']", _S_DTYPES[wd], rows * bs13, device)
+        _need_bytes(banks.get("s2"), f"{name}['s2']", _S_DTYPES[wd], rows * bs2, device)
+
+
+def _need_route(route, desc: dict, T: int) -> None:
+    if not isinstance(route, RouteBuffers):
+        raise ValueError("route: expected a RouteBuffers")
+    E, k = int(desc["n_experts"]), int(desc["top_k"])
+    if route.E != E or route.k != k or route.T < T:
+        raise ValueError(f"route: sized for T={route.T}, k={route.k}, E={route.E}; the call needs "
+                         f"T={T}, k={k}, E={E}")
+
+
+def _need_layer_inputs(desc: dict, logits, slot_table, T: int, x=None, out=None) -> None:
+    E, H = int(desc["n_experts"]), int(desc["hidden"])
+    _need(logits, "logits", torch.float32, T * E)
+    _need(slot_table, "slot_table", torch.int32, E)
+    if x is not None or out is not None:
+        xd = _X_DTYPES.get(int(desc["x_dtype"]))
+        if xd is None:
+            raise ValueError(f"x_dtype {desc['x_dtype']} is not supported")
+        _need(x, "x", xd, T * H)
+        _need(out, "out_partial", torch.float32, T * H)
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
         return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
@@ -238,14 +318,27 @@ def alloc_workspace(desc: dict, max_tokens: int, device="cuda") -> torch.Tensor:
 
 def ft_route_only(desc: dict, logits: torch.Tensor, slot_table: torch.Tensor, T: int,
                   route: RouteBuffers, ws: torch.Tensor, stream=None) -> None:
+    _need_layer_inputs(desc, logits, slot_table, T)
+    _need_route(route, desc, T)
+    _need(ws, "ws", torch.uint8, 0)
     st = load().ft_route_only(ctypes.byref(make_desc(desc)), _ptr(logits), _ptr(slot_table), int(T),
                               ctypes.byref(route.c()), _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "ft_route_only")
 
 
+def _need_forward(desc, banks, logits, slot_table, x, T, out_partial, route, ws) -> None:
+    if int(T) <= 0:
+        return
+    _need_layer_inputs(desc, logits, slot_table, T, x, out_partial)
+    _need_route(route, desc, T)
+    _need(ws, "ws", torch.uint8, 0)
+    _need_banks(desc, banks, int(desc["n_slots"]), "banks")
+
+
 def ft_moe_forward(desc: dict, banks: dict, logits: torch.Tensor, slot_table: torch.Tensor,
                    x: torch.Tensor, T: int, out_partial: torch.Tensor, route: RouteBuffers,
                    ws: torch.Tensor, stream=None) -> None:
+    _need_forward(desc, banks, logits, slot_table, x, T, out_partial, route, ws)
     b = ft_banks_t(_ptr(banks.get("w13")), _ptr(banks.get("w2")), _ptr(banks.get("s13")),
                    _ptr(banks.get("s2")))
     st = load().ft_moe_forward(ctypes.byref(make_desc(desc)), ctypes.byref(b), _ptr(logits),
@@ -258,6 +351,7 @@ def ft_moe_forward_profiled(desc: dict, banks: dict, logits: torch.Tensor, slot_
                             x: torch.Tensor, T: int, out_partial: torch.Tensor, route: RouteBuffers,
                             ws: torch.Tensor, events, stream=None) -> None:
     """``events``: FT_PROF_STAGES + 1 hipEvent_t handles (ints) or None entries."""
+    _need_forward(desc, banks, logits, slot_table, x, T, out_partial, route, ws)
     b = ft_banks_t(_ptr(banks.get("w13")), _ptr(banks.get("w2")), _ptr(banks.get("s13")),
                    _ptr(banks.get("s2")))
     ev = ft_prof_events_t()
@@ -272,6 +366,12 @@ def ft_moe_forward_profiled(desc: dict, banks: dict, logits: torch.Tensor, slot_
 
 def ft_miss_list_to_host(desc: dict, route: RouteBuffers, T: int, host: HostMissBuffers,
                          stream=None) -> None:
+    _need_route(route, desc, T)
+    pk, E = int(T) * int(desc["top_k"]), int(desc["n_experts"])
+    for n, dt, cnt in (("counts", torch.int32, 4), ("miss_pairs", torch.int32, pk),
+                       ("miss_off", torch.int32, E + 1), ("topk_ids", torch.int32, pk),
+                       ("topk_w", torch.float32, pk)):
+        _need(getattr(host, n, None), f"host.{n}", dt, cnt, "cpu")
     st = load().ft_miss_list_to_host(ctypes.byref(make_desc(desc)), ctypes.byref(route.c()), int(T),
                                      ctypes.byref(host.c()), _stream(stream))
     _check(st, "ft_miss_list_to_host")
@@ -304,9 +404,22 @@ class FillPlanBuffers:
         return ft_fill_plan_t(*[_ptr(getattr(self, n)) for n, _ in ft_fill_plan_t._fields_])
 
 
+def _need_plan(desc: dict, slot_table, state, plan, max_fill: int) -> None:
+    E, S = int(desc["n_experts"]), int(desc["n_slots"])
+    _need(slot_table, "slot_table", torch.int32, E)
+    _need(state.slot_expert, "state.slot_expert", torch.int32, S)
+    _need(state.slot_stamp, "state.slot_stamp", (torch.int32, torch.uint32), S)
+    for n in ("fill_expert", "fill_slot", "evict_expert"):
+        _need(getattr(plan, n), f"plan.{n}", torch.int32, int(max_fill))
+    _need(plan.cpu_expert, "plan.cpu_expert", torch.int32, E)
+    _need(plan.counts, "plan.counts", torch.int32, 4)
+
+
 def ft_cache_plan(desc: dict, route: RouteBuffers, T: int, slot_table: torch.Tensor,
                   state: CacheState, b_pcie: float, b_host: float, max_fill: int, step: int,
                   plan: FillPlanBuffers, stream=None) -> None:
+    _need_route(route, desc, T)
+    _need_plan(desc, slot_table, state, plan, max_fill)
     pol = ft_cache_policy_t(float(b_pcie), float(b_host), int(max_fill), int(step))
     st = load().ft_cache_plan(ctypes.byref(make_desc(desc)), ctypes.byref(route.c()), int(T),
                               _ptr(slot_table), ctypes.byref(state.c()), ctypes.byref(pol),
@@ -318,6 +431,18 @@ def ft_cpu_experts(desc: dict, host_pool: dict, x: torch.Tensor, T: int, topk_id
                    topk_w: torch.Tensor, experts: torch.Tensor, out: torch.Tensor,
                    n_threads: int = 0) -> None:
     """CPU branch on host tensors: ``host_pool`` holds w13, w2 (s13, s2) indexed by expert id."""
+    if int(T) > 0:
+        E, H, k = int(desc["n_experts"]), int(desc["hidden"]), int(desc["top_k"])
+        xd = _X_DTYPES.get(int(desc["x_dtype"]))
+        if xd is None:
+            raise ValueError(f"x_dtype {desc['x_dtype']} is not supported")
+        _need(x, "x", xd, int(T) * H, "cpu")
+        _need(topk_ids, "topk_ids", torch.int32, int(T) * k, "cpu")
+        _need(topk_w, "topk_w", torch.float32, int(T) * k, "cpu")
+        _need(experts, "experts", torch.int32, 0, "cpu")
+        _need(out, "out", torch.float32, int(T) * H, "cpu")
+        if experts.numel() > 0:
+            _need_banks(desc, host_pool, E, "host_pool", "cpu")
     b = ft_banks_t(_ptr(host_pool.get("w13")), _ptr(host_pool.get("w2")), _ptr(host_pool.get("s13")),
                    _ptr(host_pool.get("s2")))
     st = load().ft_cpu_experts(ctypes.byref(make_desc(desc)), ctypes.byref(b), _ptr(x), int(T),
@@ -332,6 +457,11 @@ def _banks(b: dict) -> ft_banks_t:
 
 def ft_cache_fill(desc: dict, host_pool: dict, dev_banks: dict, plan: FillPlanBuffers, max_fill: int,
                   stream=None) -> None:
+    _need_banks(desc, host_pool, int(desc["n_experts"]), "host_pool", "cpu")
+    _need_banks(desc, dev_banks, int(desc["n_slots"]), "dev_banks")
+    for n in ("fill_expert", "fill_slot"):
+        _need(getattr(plan, n), f"plan.{n}", torch.int32, int(max_fill))
+    _need(plan.counts, "plan.counts", torch.int32, 4)
     st = load().ft_cache_fill(ctypes.byref(make_desc(desc)), ctypes.byref(_banks(host_pool)),
                               ctypes.byref(_banks(dev_banks)), ctypes.byref(plan.c()), int(max_fill),
                               _stream(stream))
@@ -385,6 +515,14 @@ def ft_prefill_layers(desc: dict, host_layers: list, dev_bufs: list, slot_table:
     n = len(host_layers)
     if not (len(logits) == len(x) == len(out) == n) or len(dev_bufs) != 2:
         raise ValueError("one logits, x and out tensor per layer and two device buffers")
+    if int(T) > 0:
+        for l in range(n):
+            _need_banks(desc, host_layers[l], int(desc["n_slots"]), f"host_layers[{l}]", "cpu")
+            _need_layer_inputs(desc, logits[l], slot_table, T, x[l], out[l])
+        for b in range(2):
+            _need_banks(desc, dev_bufs[b], int(desc["n_slots"]), f"dev_bufs[{b}]")
+        _need_route(route, desc, T)
+        _need(ws, "ws", torch.uint8, 0)
     hl = (ft_banks_t * max(n, 1))(*[_banks(h) for h in host_layers])
     db = (ft_banks_t * 2)(*[_banks(d) for d in dev_bufs])
     arr = lambda ts: (ctypes.c_void_p * max(n, 1))(*[_ptr(t) for t in ts])

@@ -1,4 +1,4 @@
-// Full-layer double-buffered prefill (Section 3.3, prefill design; Section 5, "Pipelined
+// Full-layer double-buffered prefill (Section 3.1, "Prefill Codesign"; Section 5, "Pipelined
 // prefill").  Prefill routes nearly every expert of every layer, so no expert is fetched on
 // demand: two device buffers, each able to hold the complete expert set of one layer, take
 // turns.  While the GPU evaluates layer l from one buffer, a transfer stream loads all experts

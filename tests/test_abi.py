@@ -232,3 +232,34 @@ def test_missing_library_fails_loudly(tmp_path):
                        timeout=120)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "not built" in r.stdout
+
+
+def test_binding_rejects_host_tensors_and_bad_sizes_before_the_call():
+    """The binding checks device, dtype and size of every tensor it hands to the C ABI (which
+    carries no capacities) and raises ValueError before entering the library."""
+    import torch
+    d = _desc()
+    T, E, H = 4, d["n_experts"], d["hidden"]
+    route = ftm.RouteBuffers.__new__(ftm.RouteBuffers)
+    route.T, route.k, route.E = T, d["top_k"], E
+    with pytest.raises(ValueError, match="device"):
+        ftm.ft_route_only(d, torch.zeros(T, E), torch.zeros(E, dtype=torch.int32), T, route,
+                          torch.zeros(16, dtype=torch.uint8))
+    with pytest.raises(ValueError, match="route"):
+        ftm._need_route(route, d, T + 1)
+    with pytest.raises(ValueError, match="route"):
+        ftm._need_route(route, dict(d, n_experts=E + 1), T)
+    # host-side checks of the CPU branch run without a GPU
+    ids = torch.zeros(T, d["top_k"], dtype=torch.int32)
+    w = torch.zeros(T, d["top_k"])
+    lst = torch.zeros(1, dtype=torch.int32)
+    x = torch.zeros(T, H)
+    with pytest.raises(ValueError, match="out"):
+        ftm.ft_cpu_experts(d, {}, x, T, ids, w, lst, torch.zeros(T * H - 1))
+    with pytest.raises(ValueError, match="dtype"):
+        ftm.ft_cpu_experts(d, {}, x, T, ids.float(), w, lst, torch.zeros(T, H))
+    with pytest.raises(ValueError, match="host_pool"):
+        ftm.ft_cpu_experts(d, {"w13": torch.zeros(1), "w2": torch.zeros(1)}, x, T, ids, w, lst,
+                           torch.zeros(T, H))
+    assert ftm.expert_bank_bytes(dict(d, w_dtype=ftm.FT_DT_FP8E4M3FN_B128, hidden=256, inter=128)) == \
+        (2 * 128 * 256, 256 * 128, 2 * 2 * 4, 2 * 1 * 4)

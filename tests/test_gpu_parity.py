@@ -158,7 +158,9 @@ def test_invalid_slot_tables_flagged_and_treated_as_misses(T):
 
 @pytest.mark.parametrize("name,T", [("tiny", 16), ("qwen3_decode", 1), ("qwen3_decode", 8),
                                     ("qwen3_decode", 32), ("dsv3_decode", 1), ("dsv3_decode", 16),
-                                    ("dsv4flash_decode", 1), ("dsv4flash_decode", 16)])
+                                    ("dsv3_decode", 64), ("dsv4flash_decode", 1),
+                                    ("dsv4flash_decode", 16), ("dsv4flash_decode", 64),
+                                    ("qwen3_prefill", 4096)])
 def test_forward_configs_full(name, T):
     _say(f"forward {name} T={T}")
     lay = workloads.make_layer(name, T, device="cuda")
@@ -168,17 +170,37 @@ def test_forward_configs_full(name, T):
     check_output(out, ref, lay.w_dtype)
 
 
-@pytest.mark.parametrize("name,T,rows", [("dsv3_decode", 64, [0, 13, 63]),
-                                         ("qwen3_prefill", 4096, list(range(0, 4096, 97)) + [4095]),
-                                         ("dsv3_prefill", 8192, [0, 1023, 1024, 3000, 8191]),
-                                         ("dsv4flash_decode", 64, [0, 31, 63]),
-                                         ("dsv4flash_prefill", 8192, [0, 1023, 1024, 5000, 8191])])
-def test_forward_configs_sampled(name, T, rows):
-    _say(f"forward {name} T={T} sampled rows {rows}")
+GEMM_BM = 128      # token rows of one M tile of the many-token (matrix-core) path
+
+
+def tile_covering_tokens(r, T, k, shared):
+    """Tokens whose rows cover the first and the last row of every M tile of every evaluation
+    group: each hit expert's rows in the oracle's hit-list order, then the shared expert's T rows
+    in token order.  Every tile, every band of tiles and every ragged tail then holds a checked
+    row.  Derived from the oracle's routing only."""
+    toks = set()
+    hit_pairs, hit_off = r["hit_pairs"], r["hit_off"]
+    groups = [[int(p) // k for p in hit_pairs[hit_off[e]:hit_off[e + 1]]]
+              for e in range(len(hit_off) - 1) if hit_off[e + 1] > hit_off[e]]
+    if shared:
+        groups.append(list(range(T)))
+    for g in groups:
+        for m0 in range(0, len(g), GEMM_BM):
+            toks.add(g[m0])
+            toks.add(g[min(len(g), m0 + GEMM_BM) - 1])
+    return sorted(toks)
+
+
+@pytest.mark.parametrize("name,T", [("dsv3_prefill", 8192), ("dsv4flash_prefill", 8192)])
+def test_forward_configs_tile_covering(name, T):
     lay = workloads.make_layer(name, T, device="cuda")
     out, route = run_forward(lay)
-    ref, r = oracle.moe_partial(*oracle_inputs(lay), tokens=rows)
-    check_route(route, r, T, lay.top_k)
+    inp = oracle_inputs(lay)
+    r = oracle.route(*[inp[0], inp[2], inp[3]])
+    rows = tile_covering_tokens(r, T, lay.top_k, lay.shared_slot >= 0)
+    _say(f"forward {name} T={T}: {len(rows)} tile-covering rows")
+    ref, r2 = oracle.moe_partial(*inp, tokens=rows)
+    check_route(route, r2, T, lay.top_k)
     check_output(out, ref, lay.w_dtype, rows=rows)
 
 
@@ -216,6 +238,11 @@ RANDOM_FWD = [
     (24, workloads.DT_BF16, 0, 16, 4, 16, 16, True, 384, 256, 0.0),    # bf16, T = 16 exactly
     (25, workloads.DT_FP8, 1, 8, 4, 60, 8, True, 256, 256, 0.0),       # fp8 wide gate/up, 4 M tiles a pass
     (26, workloads.DT_MXFP4, 0, 16, 4, 100, 12, True, 256, 256, 0.7),  # MXFP4 wide gate/up, 4 M tiles a pass
+    # groups above 1024 rows (more than one band of 8 M tiles, the last band short): strong skew
+    # puts most tokens on the top experts, and the shared expert's 2900 rows make 23 M tiles
+    (27, workloads.DT_BF16, 0, 16, 4, 2900, 12, True, 256, 256, 3.0),
+    (28, workloads.DT_FP8, 1, 16, 4, 2900, 12, True, 256, 256, 3.0),
+    (29, workloads.DT_MXFP4, 0, 16, 4, 2900, 12, True, 256, 256, 3.0),
 ]
 
 
@@ -232,6 +259,9 @@ def test_forward_random_shapes(case):
     check_output(out, ref, wdt)
     if n_res == 0 and not shared:
         assert not out.any()
+    if T >= 2000:
+        sizes = np.diff(r["hit_off"])
+        assert sizes.max() > 8 * GEMM_BM, "a group must span more than one band of M tiles"
 
 
 def test_forward_T0_is_noop():
@@ -245,17 +275,28 @@ def test_forward_T0_is_noop():
     assert bool((out == 7.0).all())
 
 
-def test_miss_list_to_host():
-    lay = workloads.make_layer("tiny", 16, device="cuda")
+@pytest.mark.parametrize("case", ["tiny", "random"])
+def test_miss_list_to_host(case):
+    """The host copies of the miss list equal the oracle's routing."""
+    if case == "tiny":
+        lay = workloads.make_layer("tiny", 16, device="cuda")
+    else:
+        lay = workloads.random_layer(31, hidden=128, inter=128, n_experts=40, top_k=6, tokens=77,
+                                     n_resident=15, shared=True, tie_logits=True, device="cuda")
+    T, k = lay.tokens, lay.top_k
     out, route = run_forward(lay)
-    host = ftm.HostMissBuffers(16, lay.top_k, lay.n_experts)
-    ftm.ft_miss_list_to_host(lay.desc(), route, 16, host)
+    host = ftm.HostMissBuffers(T, k, lay.n_experts)
+    ftm.ft_miss_list_to_host(lay.desc(), route, T, host)
     torch.cuda.synchronize()
-    assert torch.equal(host.counts, route.counts.cpu())
-    assert torch.equal(host.miss_pairs, route.miss_pairs.cpu())
-    assert torch.equal(host.miss_off, route.miss_off.cpu())
-    assert torch.equal(host.topk_ids, route.topk_ids.cpu())
-    assert torch.equal(host.topk_w, route.topk_w.cpu())
+    desc, banks, logits, st, x = oracle_inputs(lay)
+    r = oracle.route(desc, logits, st)
+    assert r["n_miss"] > 0
+    assert host.counts.tolist() == [r["n_hit"], r["n_miss"], r["m_unique_miss"], r["status"]]
+    mp = host.miss_pairs.numpy()[: T * k]
+    assert np.array_equal(mp[: r["n_miss"]], r["miss_pairs"]) and np.all(mp[r["n_miss"]:] == -1)
+    assert np.array_equal(host.miss_off.numpy(), r["miss_off"])
+    assert np.array_equal(host.topk_ids.numpy()[: T * k].reshape(T, k), r["topk_ids"])
+    np.testing.assert_allclose(host.topk_w.numpy()[: T * k].reshape(T, k), r["topk_w"], rtol=0, atol=2e-6)
 
 
 def test_forward_deterministic_and_slot_table_change():
@@ -280,3 +321,30 @@ def test_forward_deterministic_and_slot_table_change():
     lay.slot_table = torch.full_like(st, -1)
     out, route = run_forward(lay)
     assert not out.any() and int(route.counts[0]) == 0
+
+
+def test_binding_rejects_undersized_or_mistyped_device_tensors():
+    """Buffers too small for T, k or E, or of the wrong dtype, raise before the library runs."""
+    lay = workloads.make_layer("tiny", 16, device="cuda")
+    desc, T = lay.desc(), 16
+    ws = ftm.alloc_workspace(desc, T)
+    banks = ftm.banks_of(lay)
+    out = torch.empty(T, lay.hidden, device="cuda")
+    ok_route = ftm.RouteBuffers(T, lay.top_k, lay.n_experts)
+    fwd = lambda **kw: ftm.ft_moe_forward(desc, kw.get("banks", banks), kw.get("logits", lay.logits),
+                                          lay.slot_table, kw.get("x", lay.x), T, kw.get("out", out),
+                                          kw.get("route", ok_route), ws)
+    with pytest.raises(ValueError, match="route"):
+        fwd(route=ftm.RouteBuffers(T - 1, lay.top_k, lay.n_experts))
+    with pytest.raises(ValueError, match="route"):
+        fwd(route=ftm.RouteBuffers(T, lay.top_k, lay.n_experts - 1))
+    with pytest.raises(ValueError, match="logits"):
+        fwd(logits=lay.logits.double())
+    with pytest.raises(ValueError, match="x"):
+        fwd(x=lay.x[: T - 1])
+    with pytest.raises(ValueError, match="out_partial"):
+        fwd(out=out[: T - 1])
+    with pytest.raises(ValueError, match="w13"):
+        fwd(banks=dict(banks, w13=lay.w13[:-1]))
+    fwd()
+    torch.cuda.synchronize()
