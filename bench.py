@@ -7,9 +7,17 @@ its inputs already resident in HBM.  Steps rotate over --layers distinct layer i
 with its own slot-pool weights and routing, so a cycle's working set exceeds the 256 MB
 Infinity Cache and weights really stream from HBM.
 
+The default workload is the DeepSeek-V3-shaped prefill chunk (T = 8192 tokens, fp8 block-scaled
+weights, 102 of 256 routed experts resident plus the shared expert, hot set re-drawn every 1024
+tokens), the largest configuration of the metric that fits one GPU; its roofline is the bf16
+MFMA peak, since fp8 weights are widened exactly to bf16 for the matrix cores.  Two decode points
+(Qwen3-30B-A3B-shaped T = 32, DeepSeek-V3-shaped T = 64) are timed in the same run and reported
+under "decode" with their HBM roofline.
+
 Prints ONE JSON line: tokens/s (whole job), ms per step, the dominant kernel's roofline
-fraction (algorithmic bytes of one launch / its HIP-event-timed duration on the library's
-stream), and the CPU oracle timed on a bounded sample on this host.
+fraction (algorithmic flops or bytes of one launch / its HIP-event-timed duration on the
+library's stream), and the CPU oracle timed on a bounded sample on this host (one thread and
+every CPU of the affinity mask).
 """
 import argparse
 import ctypes
@@ -467,41 +475,153 @@ def placement_replay(n_prefill, n_decode, fractions, n_layers):
         "results": rows, "seconds": round(time.perf_counter() - t0, 1)}), flush=True)
 
 
-def cpu_baseline(layers, budget_s):
-    """The float64 oracle on this host over a bounded sample of the same layer instances."""
-    import oracle
-    from tests._util import oracle_inputs
+def _cpu_model() -> str:
     try:
-        import threadpoolctl
-        info = threadpoolctl.threadpool_info()
-        cores = max([i.get("num_threads", 1) for i in info] or [1])
-    except Exception:
-        cores = 1
-    # many-token chunks are sampled 64 tokens at a time (the oracle's per-token work does not
-    # depend on the chunk it sits in, apart from decoding each expert's weights once per call)
-    done_tokens, elapsed, calls = 0, 0.0, 0
-    for rnd in range(8):                  # cycle over the instances until the budget is spent
-        for lay in layers:
-            inp = oracle_inputs(lay)      # host copy, outside the timed part
-            chunk = lay.tokens if lay.tokens <= 64 else 64
-            for c0 in range(0, lay.tokens, chunk):
-                toks = None if chunk == lay.tokens else list(range(c0, min(lay.tokens, c0 + chunk)))
-                t0 = time.perf_counter()
-                oracle.moe_partial(*inp, tokens=toks)
-                elapsed += time.perf_counter() - t0
-                done_tokens += chunk if toks is None else len(toks)
-                calls += 1
-                if elapsed >= budget_s:
-                    break
-            if elapsed >= budget_s:
-                break
-        if elapsed >= budget_s:
-            break
-    return {"value": round(done_tokens / elapsed, 2), "unit": "tokens/s", "cores": cores,
-            "kind": "oracle",
-            "sample": f"{calls} oracle calls of <= {min(64, layers[0].tokens)} tokens cycling over the "
-                      f"{len(layers)} layer instances ({done_tokens} tokens), {elapsed:.1f} s of "
-                      f"float64 oracle time"}
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(lay, tokens):
+    """The float64 oracle on this host, on a bounded sample of the timed workload: one
+    oracle.moe_partial call over ``tokens`` of one layer instance (every hit pair of those tokens
+    plus the shared expert's rows; each touched expert's weights decoded once, as the oracle
+    does), timed once on one thread and once on every CPU of this process's affinity mask."""
+    import oracle
+    import threadpoolctl
+    from tests._util import oracle_inputs
+    inp = oracle_inputs(lay)             # host copy, outside the timed part
+    n_aff = len(os.sched_getaffinity(0))
+
+    def run(threads):
+        with threadpoolctl.threadpool_limits(limits=threads):
+            t0 = time.perf_counter()
+            oracle.moe_partial(*inp, tokens=tokens)
+            return time.perf_counter() - t0
+
+    t_all = run(n_aff)
+    t_one = run(1)
+    n = len(tokens)
+    return {"value": round(n / t_all, 3), "unit": "tokens/s", "cores": n_aff, "kind": "oracle",
+            "single_thread": {"value": round(n / t_one, 3), "unit": "tokens/s", "cores": 1,
+                              "seconds": round(t_one, 2)},
+            "affinity_cpus": n_aff, "cpu_model": _cpu_model(),
+            "sample": f"one float64 oracle call over {n} tokens of layer instance 0 ({tokens[0]}, "
+                      f"{tokens[1]}, ... {tokens[-1]}): all their hit pairs and shared-expert rows, "
+                      f"each touched expert decoded once; {t_all:.1f} s on {n_aff} threads (BLAS "
+                      f"pool limited to the affinity mask; the decodes are single-threaded numpy), "
+                      f"{t_one:.1f} s on one thread"}
+
+
+def measure_forward(config, T, n_layers, steps, warmup, hip, stage_times=True):
+    """Time ``steps`` back-to-back ft_moe_forward calls over ``n_layers`` rotating instances of
+    ``config`` at T tokens (inputs resident in HBM), then the same steps with stage events.
+    Returns the throughput, the per-stage times and the dominant kernel's roofline, and the
+    layer instances (for the CPU baseline)."""
+    import torch
+    import paper_2608_16157_amd as ftm
+    import workloads
+    cfg = workloads.CONFIGS[config]
+    print(f"# building {n_layers} layer instances of {config} T={T}", file=sys.stderr, flush=True)
+    layers = [workloads.make_layer(config, T, layer=i, device="cuda") for i in range(n_layers)]
+    desc = layers[0].desc()
+    ws = ftm.alloc_workspace(desc, T)
+    routes = [ftm.RouteBuffers(T, cfg.top_k, cfg.n_experts) for _ in layers]
+    out = torch.empty(T, cfg.hidden, dtype=torch.float32, device="cuda")
+    banks = [ftm.banks_of(l) for l in layers]
+
+    def step(i, events=None):
+        j = i % len(layers)
+        l = layers[j]
+        if events is None:
+            ftm.ft_moe_forward(desc, banks[j], l.logits, l.slot_table, l.x, T, out, routes[j], ws)
+        else:
+            ftm.ft_moe_forward_profiled(desc, banks[j], l.logits, l.slot_table, l.x, T, out,
+                                        routes[j], ws, events)
+
+    for i in range(len(layers)):          # route every instance once (setup, untimed)
+        step(i)
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    work = [algorithmic_work(l, r) for l, r in zip(layers, routes)]
+    K = steps
+    stream = torch.cuda.current_stream().cuda_stream
+    start, stop = hip.create(), hip.create()
+
+    # timed region 1: plain back-to-back steps -> throughput
+    torch.cuda.synchronize()
+    hip.hip.hipEventRecord(start, stream)
+    for i in range(K):
+        step(i)
+    hip.hip.hipEventRecord(stop, stream)
+    torch.cuda.synchronize()
+    total_ms = hip.elapsed_ms(start, stop)
+    ms_step = total_ms / K
+
+    # timed region 2: the same steps with HIP events at the stage boundaries, recorded by the
+    # library on its stream -> per-kernel durations (the events add gaps between kernels, so
+    # this region is not used for throughput).  Timing-only events without the system-scope
+    # fence, whose cache writeback would otherwise be charged to the stage after each boundary.
+    stage_ev = [[hip.create(HIP_EVENT_DISABLE_SYSTEM_FENCE) for _ in range(ftm.FT_PROF_STAGES + 1)]
+                for _ in range(K)]
+    torch.cuda.synchronize()
+    for i in range(K):
+        step(i, stage_ev[i])
+    torch.cuda.synchronize()
+    stage_ms = [[hip.elapsed_ms(e[s], e[s + 1]) for s in range(ftm.FT_PROF_STAGES)] for e in stage_ev]
+    for e in stage_ev:
+        for ev in e:
+            hip.destroy(ev)
+    hip.destroy(start)
+    hip.destroy(stop)
+
+    step_work = [work[i % len(layers)] for i in range(K)]
+    layer_bytes = sum(w["layer_bytes"] for w in step_work) / K
+    layer_flops = sum(w["flops"] for w in step_work) / K
+    gu_ms = sum(s[1] for s in stage_ms) / K
+    gu_bytes = sum(w["gateup_bytes"] for w in step_work) / K
+    gu_flops = sum(w["gateup_flops"] for w in step_work) / K
+    stage_avg = [sum(s[j] for s in stage_ms) / K for j in range(ftm.FT_PROF_STAGES)]
+    mfma_path = T >= 256      # the library's many-token (MFMA GEMM) path
+    traffic = measured_traffic(f"{config}:T{T}")
+    if mfma_path:
+        # fp8 and MXFP4 weights are widened to bf16 in registers, so every contraction runs on
+        # bf16 MFMA
+        achieved = gu_flops / (gu_ms / 1e3) / 1e12
+        roof = {"kernel": "grouped gate/up GEMM + SiLU-mul (grouped_gemm<gate/up>)", "bound": "mfma",
+                "achieved": round(achieved, 1), "peak": MFMA_PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
+                "frac": round(achieved / MFMA_PEAK_TFLOPS["bf16"], 4),
+                "traffic": traffic, "flops_per_launch": round(gu_flops),
+                "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
+    else:
+        achieved = gu_bytes / (gu_ms / 1e3) / 1e9
+        roof = {"kernel": "grouped gate/up GEMV + SiLU-mul (grouped_gemv<gate/up>)", "bound": "hbm",
+                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
+    wdt = {0: "f32", 1: "bf16", 2: "fp8 e4m3 + 128x128 float32 block scales, widened exactly to bf16",
+           3: "MXFP4, widened exactly to bf16"}[cfg.w_dtype]
+    res = {
+        "value": round(T * K / (total_ms / 1e3), 1),
+        "ms_per_step": round(ms_step, 5),
+        "workload": f"{config}: MoE layer over a GPU expert cache, T={T} tokens, E={cfg.n_experts} "
+                    f"top-{cfg.top_k}, H={cfg.hidden} I={cfg.inter}, weights {wdt}, "
+                    f"{layers[0].n_slots} slots, {n_layers} rotating layer instances",
+        "layer_hbm_gbps": round(layer_bytes / (ms_step / 1e3) / 1e9, 1),
+        "layer_hbm_frac": round(layer_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+        "layer_tflops": round(layer_flops / (ms_step / 1e3) / 1e12, 2),
+        "layer_mfma_frac": round(layer_flops / (ms_step / 1e3) / 1e12 / MFMA_PEAK_TFLOPS["bf16"], 4),
+        "stage_ms": {"route": round(stage_avg[0], 5), "gate_up": round(stage_avg[1], 5),
+                     "down": round(stage_avg[2], 5), "combine": round(stage_avg[3], 5)},
+        "roofline": roof,
+    }
+    return res, layers
 
 
 def main():
@@ -509,11 +629,13 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="qwen3_decode")
-    ap.add_argument("--tokens", type=int, default=32)
-    ap.add_argument("--layers", type=int, default=16)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--config", default="dsv3_prefill")
+    ap.add_argument("--tokens", type=int, default=8192)
+    ap.add_argument("--layers", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-extras", default="qwen3_decode:32,dsv3_decode:64",
+                    help="decode points (config:T, comma-separated) timed after the headline in the "
+                         "same run, reported under 'decode'; '' for none")
     ap.add_argument("--measure-bandwidths", action="store_true",
                     help="measure B_P (fills over PCIe) and B_H (CPU branch) for --config, then exit")
     ap.add_argument("--hybrid", action="store_true",
@@ -574,121 +696,53 @@ def main():
                       args.b_host, args.max_fill)
         return
     ftm.load()
-    cfg = workloads.CONFIGS[args.config]
-    T = args.tokens
-    print(f"# building {args.layers} layer instances of {args.config} T={T}", file=sys.stderr, flush=True)
-    layers = [workloads.make_layer(args.config, T, layer=i, device="cuda") for i in range(args.layers)]
-    desc = layers[0].desc()
-    ws = ftm.alloc_workspace(desc, T)
-    routes = [ftm.RouteBuffers(T, cfg.top_k, cfg.n_experts) for _ in layers]
-    out = torch.empty(T, cfg.hidden, dtype=torch.float32, device="cuda")
-    banks = [ftm.banks_of(l) for l in layers]
-
-    def step(i, events=None):
-        l = layers[i % len(layers)]
-        if events is None:
-            ftm.ft_moe_forward(desc, banks[i % len(layers)], l.logits, l.slot_table, l.x, T, out,
-                               routes[i % len(layers)], ws)
-        else:
-            ftm.ft_moe_forward_profiled(desc, banks[i % len(layers)], l.logits, l.slot_table, l.x, T,
-                                        out, routes[i % len(layers)], ws, events)
-
-    for i in range(len(layers)):          # route every instance once (setup, untimed)
-        step(i)
-    for i in range(args.warmup):
-        step(i)
-    torch.cuda.synchronize()
-    work = [algorithmic_work(l, r) for l, r in zip(layers, routes)]
-
     hip = HipEvents()
-    K = args.steps
-    stream = torch.cuda.current_stream().cuda_stream
-    start, stop = hip.create(), hip.create()
-
-    # timed region 1: plain back-to-back steps -> throughput
-    torch.cuda.synchronize()
-    hip.hip.hipEventRecord(start, stream)
-    for i in range(K):
-        step(i)
-    hip.hip.hipEventRecord(stop, stream)
-    torch.cuda.synchronize()
-    total_ms = hip.elapsed_ms(start, stop)
-    ms_step = total_ms / K
-
-    # timed region 2: the same steps with HIP events at the stage boundaries, recorded by the
-    # library on its stream -> per-kernel durations (the events add gaps between kernels, so
-    # this region is not used for throughput).  Timing-only events without the system-scope
-    # fence, whose cache writeback would otherwise be charged to the stage after each boundary.
-    stage_ev = [[hip.create(HIP_EVENT_DISABLE_SYSTEM_FENCE) for _ in range(ftm.FT_PROF_STAGES + 1)]
-                for _ in range(K)]
-    torch.cuda.synchronize()
-    for i in range(K):
-        step(i, stage_ev[i])
-    torch.cuda.synchronize()
-    stage_ms = [[hip.elapsed_ms(e[s], e[s + 1]) for s in range(ftm.FT_PROF_STAGES)] for e in stage_ev]
-    for e in stage_ev:
-        for ev in e:
-            hip.destroy(ev)
-
-    tokens_per_s = T * K / (total_ms / 1e3)
-    step_work = [work[i % len(layers)] for i in range(K)]
-    layer_bytes = sum(w["layer_bytes"] for w in step_work) / K
-    layer_flops = sum(w["flops"] for w in step_work) / K
-    gu_ms = sum(s[1] for s in stage_ms) / K
-    gu_bytes = sum(w["gateup_bytes"] for w in step_work) / K
-    stage_avg = [sum(s[j] for s in stage_ms) / K for j in range(ftm.FT_PROF_STAGES)]
-
-    gu_flops = sum(w["gateup_flops"] for w in step_work) / K
-    mfma_path = T >= 256      # the library's many-token (MFMA GEMM) path
-    key = f"{args.config}:T{T}"
-    traffic = measured_traffic(key)
-    if mfma_path:
-        # fp8 and MXFP4 weights are widened to bf16 in registers, so every contraction runs on
-        # bf16 MFMA
-        achieved = gu_flops / (gu_ms / 1e3) / 1e12
-        roof = {"kernel": "grouped gate/up GEMM + SiLU-mul (grouped_gemm<gate/up>)", "bound": "mfma",
-                "achieved": round(achieved, 1), "peak": MFMA_PEAK_TFLOPS["bf16"], "unit": "TFLOP/s",
-                "frac": round(achieved / MFMA_PEAK_TFLOPS["bf16"], 4),
-                "traffic": traffic, "flops_per_launch": round(gu_flops),
-                "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
-    else:
-        achieved = gu_bytes / (gu_ms / 1e3) / 1e9
-        roof = {"kernel": "grouped gate/up GEMV + SiLU-mul (grouped_gemv<gate/up>)", "bound": "hbm",
-                "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
-    dtype = {0: "f32", 1: "bf16", 2: "fp8e4m3->bf16", 3: "mxfp4->bf16"}[cfg.w_dtype]
-    res = {
+    T = args.tokens
+    res, layers = measure_forward(args.config, T, args.layers, args.steps, args.warmup, hip)
+    cfg = workloads.CONFIGS[args.config]
+    line = {
         "metric": METRIC,
-        "value": round(tokens_per_s, 1),
+        "value": res["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": K,
+        "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 5),
+        "ms_per_step": res["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16" if cfg.w_dtype != 0 else "f32",
         "data": "synthetic",
-        "config": {
-            "workload": f"{args.config}: MoE layer over a GPU expert cache, T={T} tokens, "
-                        f"E={cfg.n_experts} top-{cfg.top_k}, H={cfg.hidden} I={cfg.inter}, "
-                        f"weights {dtype}, {layers[0].n_slots} slots, "
-                        f"{args.layers} rotating layer instances",
-            "tokens": T, "layers": args.layers,
-        },
-        "layer_hbm_gbps": round(layer_bytes / (ms_step / 1e3) / 1e9, 1),
-        "layer_hbm_frac": round(layer_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
-        "layer_tflops": round(layer_flops / (ms_step / 1e3) / 1e12, 2),
-        "stage_ms": {"route": round(stage_avg[0], 5), "gate_up": round(stage_avg[1], 5),
-                     "down": round(stage_avg[2], 5), "combine": round(stage_avg[3], 5)},
-        "roofline": roof,
+        "config": {"workload": res["workload"], "tokens": T, "layers": args.layers},
     }
+    for k in ("layer_hbm_gbps", "layer_hbm_frac", "layer_tflops", "layer_mfma_frac", "stage_ms",
+              "roofline"):
+        line[k] = res[k]
     if not args.no_cpu_baseline:
         print("# timing the CPU oracle", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(layers, args.cpu_seconds)
-    print(json.dumps(res), flush=True)
+        if T <= 64:
+            toks = list(range(T))
+        else:   # eight tokens from each eighth of the chunk (every hot-set segment of dsv3_prefill)
+            toks = sorted({i * (T // 8) + j for i in range(8) for j in range(min(8, T // 8))})
+        line["cpu_baseline"] = cpu_baseline(layers[0], toks)
+    del layers
+    torch.cuda.empty_cache()
+    # decode points of the metric's other half (achieved HBM bandwidth), timed in the same run
+    if args.decode_extras:
+        extras = {}
+        for spec in args.decode_extras.split(","):
+            name, t = spec.split(":")
+            n_dec = 16 if name.startswith("qwen3") else 8
+            r, lays = measure_forward(name, int(t), n_dec, max(10 * args.steps, 100), args.warmup, hip)
+            del lays
+            torch.cuda.empty_cache()
+            extras[f"{name}:T{t}"] = {k: r[k] for k in ("value", "ms_per_step", "workload",
+                                                        "layer_hbm_gbps", "layer_hbm_frac",
+                                                        "stage_ms", "roofline")}
+            extras[f"{name}:T{t}"]["unit"] = "tokens/s"
+            extras[f"{name}:T{t}"]["steps"] = max(10 * args.steps, 100)
+        line["decode"] = extras
+    print(json.dumps(line), flush=True)
 
 
 if __name__ == "__main__":
