@@ -182,6 +182,27 @@ ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, c
                            size_t ws_bytes, void *stream);
 
 /*
+ * ft_moe_forward without a workspace argument, for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).  The
+ * workspace is a device array inside the library of FT_NOALLOC_SCRATCH_BYTES per GPU, which that
+ * GPU holds from the library's load until the process ends; the call itself allocates and frees
+ * nothing.  Every argument and every result is as for ft_moe_forward.
+ *   Returns FT_ERR_CAPACITY, before enqueuing anything, when ft_moe_workspace_bytes(desc, T)
+ *   exceeds FT_NOALLOC_SCRATCH_BYTES (e.g. 64 MiB holds a Qwen3-30B-A3B-shaped layer up to 4096
+ *   tokens and a DeepSeek-V3-shaped one up to 1024).  FT_ERR_HIP if the array's device address
+ *   cannot be found: it is looked up on the first call on each device (make that first call, a
+ *   T = 0 call will do, before capturing a graph).
+ *   All calls on one GPU share its array and nothing in it is kept between calls: calls that may
+ *   overlap on one GPU (different streams without ordering between them) race on it and must be
+ *   serialised by the caller.
+ */
+#define FT_NOALLOC_SCRATCH_BYTES (64u << 20)
+ft_status_t ft_moe_forward_noalloc(const ft_moe_desc_t *desc, const ft_banks_t *banks,
+                                   const float *logits, const int32_t *slot_table, const void *x,
+                                   int32_t T, float *out_partial, const ft_route_t *route,
+                                   void *stream);
+
+/*
  * Stage boundaries of one ft_moe_forward call, for attributing device time per stage without
  * a profiler.  ev[i] is recorded on the call's stream when stage i starts and ev[FT_PROF_STAGES]
  * when the last stage ends: stage 0 routing (top-k, classification, permutation), stage 1 the

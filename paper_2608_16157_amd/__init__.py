@@ -9,6 +9,7 @@ of the C ABI declared in ``include/ftmoe.h``:
     ft_moe_forward(desc, banks, logits, slot_table, x, T, out_partial, route, ws, stream=None)
     ft_moe_forward_profiled(desc, banks, logits, slot_table, x, T, out_partial, route, ws,
                             events, stream=None)
+    ft_moe_forward_noalloc(desc, banks, logits, slot_table, x, T, out_partial, route, stream=None)
     ft_miss_list_to_host(desc, route, T, host, stream=None)
     ft_cache_plan(desc, route, T, slot_table, state, policy, plan, stream=None)
     ft_cpu_experts(desc, host_pool, x, T, topk_ids, topk_w, experts, out, n_threads=0)
@@ -40,10 +41,11 @@ FT_DT_F32, FT_DT_BF16, FT_DT_FP8E4M3FN_B128, FT_DT_MXFP4 = 0, 1, 2, 3
 FT_SLOT_MISS = -1
 FT_DEV_SLOT_RANGE, FT_DEV_SLOT_DUP, FT_DEV_SLOT_SHARED = 1, 2, 4
 
-EXPORTED = ("ft_moe_workspace_bytes", "ft_route_only", "ft_moe_forward",
+EXPORTED = ("ft_moe_workspace_bytes", "ft_route_only", "ft_moe_forward", "ft_moe_forward_noalloc",
             "ft_moe_forward_profiled", "ft_miss_list_to_host", "ft_cache_plan", "ft_cpu_experts",
             "ft_cache_fill", "ft_moe_step_hybrid", "ft_prefill_layers", "ft_status_string")
 FT_PROF_STAGES = 4
+FT_NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class FtError(RuntimeError):
@@ -118,6 +120,10 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ft_moe_forward.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), ctypes.c_void_p, ctypes.c_void_p,
                                    ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, P(ft_route_t),
                                    ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.ft_moe_forward_noalloc.restype = ctypes.c_int
+    lib.ft_moe_forward_noalloc.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
+                                           ctypes.c_void_p, P(ft_route_t), ctypes.c_void_p]
     lib.ft_moe_forward_profiled.restype = ctypes.c_int
     lib.ft_moe_forward_profiled.argtypes = lib.ft_moe_forward.argtypes + [P(ft_prof_events_t)]
     lib.ft_miss_list_to_host.restype = ctypes.c_int
@@ -345,6 +351,22 @@ def ft_moe_forward(desc: dict, banks: dict, logits: torch.Tensor, slot_table: to
                                _ptr(slot_table), _ptr(x), int(T), _ptr(out_partial),
                                ctypes.byref(route.c()), _ptr(ws), ws.numel(), _stream(stream))
     _check(st, "ft_moe_forward")
+
+
+def ft_moe_forward_noalloc(desc: dict, banks: dict, logits: torch.Tensor, slot_table: torch.Tensor,
+                           x: torch.Tensor, T: int, out_partial: torch.Tensor, route: RouteBuffers,
+                           stream=None) -> None:
+    """ft_moe_forward on the library's own device scratch array (no workspace argument)."""
+    if int(T) > 0:
+        _need_layer_inputs(desc, logits, slot_table, T, x, out_partial)
+        _need_route(route, desc, T)
+        _need_banks(desc, banks, int(desc["n_slots"]), "banks")
+    b = ft_banks_t(_ptr(banks.get("w13")), _ptr(banks.get("w2")), _ptr(banks.get("s13")),
+                   _ptr(banks.get("s2")))
+    st = load().ft_moe_forward_noalloc(ctypes.byref(make_desc(desc)), ctypes.byref(b), _ptr(logits),
+                                       _ptr(slot_table), _ptr(x), int(T), _ptr(out_partial),
+                                       ctypes.byref(route.c()), _stream(stream))
+    _check(st, "ft_moe_forward_noalloc")
 
 
 def ft_moe_forward_profiled(desc: dict, banks: dict, logits: torch.Tensor, slot_table: torch.Tensor,

@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <mutex>
 #include <thread>
 #include <vector>
 
@@ -191,6 +192,51 @@ ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, c
                            size_t ws_bytes, void *stream) {
     return forward_impl(desc, banks, logits, slot_table, x, T, out_partial, route, ws, ws_bytes,
                         stream, nullptr);
+}
+
+// ---- the allocation-free variant of ft_moe_forward
+//
+// Its workspace is a file-scope device array instead of a caller buffer.  In host code the
+// array's name is only a host-side stand-in, so its device address is looked up once per device
+// (with that device current) and only that address is ever handed to kernels.
+
+}  // extern "C"
+
+namespace {
+
+static __device__ __align__(256) uint8_t scratch[FT_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kScratchDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_addr[kScratchDevices] = {};
+
+// Device address of `scratch` on the current device (looked up on its first use there).
+ft_status_t scratch_address(void **addr) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return FT_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return FT_ERR_HIP;
+        g_scratch_addr[dev] = p;
+    }
+    *addr = g_scratch_addr[dev];
+    return FT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ft_status_t ft_moe_forward_noalloc(const ft_moe_desc_t *desc, const ft_banks_t *banks,
+                                   const float *logits, const int32_t *slot_table, const void *x,
+                                   int32_t T, float *out_partial, const ft_route_t *route,
+                                   void *stream) {
+    void *ws = nullptr;
+    if (ft_status_t s = scratch_address(&ws); s != FT_OK) return s;
+    // the workspace check inside rejects any call whose workspace exceeds the array
+    return forward_impl(desc, banks, logits, slot_table, x, T, out_partial, route, ws,
+                        FT_NOALLOC_SCRATCH_BYTES, stream, nullptr);
 }
 
 ft_status_t ft_moe_forward_profiled(const ft_moe_desc_t *desc, const ft_banks_t *banks,
