@@ -73,11 +73,11 @@ enum {
  *            FT_DT_MXFP4 with x_dtype FT_DT_BF16.  Activations stay bf16 and products accumulate
  *            in float32.  MXFP4 weights times their scale are exact in bf16, so both paths
  *            widen them exactly.
- *            fp8 weights: with T < 256 tokens each code is widened exactly and the block scale
- *            multiplies the float32 partial sum of its 128-wide K block; with T >= 256 (matrix
- *            core path) each code times its block scale is rounded to bf16 once (relative
- *            error at most 2^-9 per weight) before the bf16 matrix multiply.  The SwiGLU
- *            activation between the two projections is rounded to bf16 (float32 for f32).
+ *            fp8 weights (weight-only dequantisation): each code is widened exactly to bf16 and
+ *            the block scale multiplies the float32 partial sum of its 128-wide K block, on both
+ *            the streaming (T < 256) and the matrix-core (T >= 256) path; a block scale of 0
+ *            makes its block contribute exactly nothing.  The SwiGLU activation between the two
+ *            projections is rounded to bf16 (float32 for f32).
  *   n_slots: number of bank rows (cache slots) in the banks, >= 0.
  *   shared_slot: bank row of an always-resident shared expert with gate 1 for every token,
  *                or -1 for none.

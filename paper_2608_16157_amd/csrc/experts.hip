@@ -483,6 +483,8 @@ static hipError_t launch_stream_path(const ExpertArgs &a, hipStream_t s, const P
 
 // Many-token chunks whose shapes tile evenly go to the MFMA GEMM.
 static bool gemm_path(const ExpertArgs &a) {
+    // the MXFP4 scale DMA of the GEMM is laid out for 256-row weight tiles
+    if (a.w_dtype == FT_DT_MXFP4 && kGemmBN != 256) return false;
     return a.T >= kGemmMinTokens && a.max_groups > 0 && a.H % kGemmBN == 0 && a.I % (kGemmBN / 2) == 0 &&
            a.H <= 8192 && a.I <= 8192;
 }

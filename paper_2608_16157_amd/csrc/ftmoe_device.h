@@ -27,32 +27,19 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
     return static_cast<uint16_t>(u >> 16);
 }
 
-// pack the high halves of two exactly-representable floats into a bf16 pair (exact for fp8 values)
-__device__ __forceinline__ uint32_t pack_bf16_trunc(float lo, float hi) {
-    return __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
-}
-
-// 8 fp8 e4m3fn codes (two 32-bit words, code 0 in the low byte) -> 8 bf16, exact
-__device__ __forceinline__ u32x4_t fp8x8_to_bf16x8(uint32_t w0, uint32_t w1) {
-    const floatx2_t a = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w0), false);
-    const floatx2_t b = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w0), true);
-    const floatx2_t c = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w1), false);
-    const floatx2_t d = __builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w1), true);
-    return u32x4_t{pack_bf16_trunc(a[0], a[1]), pack_bf16_trunc(b[0], b[1]),
-                   pack_bf16_trunc(c[0], c[1]), pack_bf16_trunc(d[0], d[1])};
-}
-
-// 8 fp8 e4m3fn codes times one float32 block scale -> 8 bf16, each product (exact in float32)
-// rounded to nearest-even once
+// 8 fp8 e4m3fn codes (two 32-bit words, code 0 in the low byte) -> 8 bf16, exact.  gfx950's
+// scaled conversion multiplies by a power of two taken from its scale operand's exponent; with
+// scale 1.0 it is a plain widening, exact because every e4m3fn value (3 mantissa bits, exponents
+// 2^-9 .. 2^8) is a bf16 value.  Element order is kept: the low half of each result holds the
+// lower-addressed code.
 typedef __bf16 bf16x2_vec_t __attribute__((ext_vector_type(2)));
-__device__ __forceinline__ u32x4_t fp8x8_scaled_to_bf16x8(uint32_t w0, uint32_t w1, float s) {
-    auto pk = [s](floatx2_t f) {
-        return __builtin_bit_cast(uint32_t, __builtin_convertvector(f * s, bf16x2_vec_t));
-    };
-    return u32x4_t{pk(__builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w0), false)),
-                   pk(__builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w0), true)),
-                   pk(__builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w1), false)),
-                   pk(__builtin_amdgcn_cvt_pk_f32_fp8(static_cast<int>(w1), true))};
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t w) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
+}
+__device__ __forceinline__ u32x4_t fp8x8_to_bf16x8(uint32_t w0, uint32_t w1) {
+    return u32x4_t{fp8x2_to_bf16x2<false>(w0), fp8x2_to_bf16x2<true>(w0), fp8x2_to_bf16x2<false>(w1),
+                   fp8x2_to_bf16x2<true>(w1)};
 }
 
 // Scale operand of the scaled fp4 conversion for an e8m0 scale byte e (2^(e - 127); e = 0 the

@@ -38,11 +38,19 @@
 // branches, so the compiler can tell the stage being read from the stages still being written
 // and adds no wait of its own.
 //
-// fp8 weights carry one float32 scale per 128 x 128 block.  A wave's 64 columns lie in at most
-// two scale blocks (the gate and the up half of a gate/up tile, one block for down), so each fp8
-// weight is widened, multiplied by its block scale and rounded to bf16 as it is read for the
-// MFMA.  The gate/up B tile puts each wave's 32 gate rows next to the 32 matching up rows, so
-// SiLU(gate) * up is formed in registers.
+// fp8 weights carry one float32 scale per 128 x 128 block, and the product is formed exactly as
+// weight-only dequantisation defines it: the codes are widened to bf16 unscaled (exact), the
+// MFMAs sum each 128-wide K block's products in float32, and the block's scale multiplies that
+// partial sum.  A wave's 64 columns lie in at most two scale blocks (the gate and the up half of
+// a gate/up tile, one block for down), so one scale per column half and K block applies to all
+// of the wave's accumulators of that half.  Rather than keeping a second accumulator set for the
+// running block, the accumulators carry the sum in units of the current block's scale: at the
+// start of block k they are multiplied by s(k-1) / s(k), the MFMAs then add block k's unscaled
+// partial sum, and after the last block one multiply by its scale gives sum_k s(k) P(k).  A block
+// with scale 0 contributes nothing: its ratio is 1 (the previous scale is carried on) and, in the
+// tiles that hold such a block, its widened codes are masked to zero.  The gate/up B tile puts
+// each wave's 32 gate rows next to the 32 matching up rows, so SiLU(gate) * up is formed in
+// registers.
 #include <type_traits>
 
 #include "ftmoe_device.h"
@@ -54,7 +62,7 @@ namespace ftmoe {
 #define FT_GEMM_WAVE_ROWS 128
 #endif
 constexpr int kWaveRows = FT_GEMM_WAVE_ROWS, kWaveCols = 64;   // per-wave output tile
-constexpr int kWavesM = kGemmBM / kWaveRows, kWavesN = 4;
+constexpr int kWavesM = kGemmBM / kWaveRows, kWavesN = kGemmBN / kWaveCols;
 constexpr int kGemmWaves = kWavesM * kWavesN;
 constexpr int kGemmThreads = kGemmWaves * kWave;
 #ifndef FT_GEMM_OCC
@@ -178,6 +186,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     static_assert(NS >= 2 && NS <= 4, "ring depth");
     static_assert(NS * PER_STAGE < 64, "vmcnt range");
     static_assert(!kFp8 || 128 % BK == 0, "an fp8 K stage lies in one scale block");
+    static_assert(!kFp8 || (NS * BK) % 128 == 0, "fp8: a ring turn spans whole scale blocks");
     // one array per stage (see the header comment); unused ones shrink to 16 bytes
     __shared__ __attribute__((aligned(1024))) uint8_t sA0[ASTAGE], sA1[ASTAGE];
     __shared__ __attribute__((aligned(1024))) uint8_t sA2[NS > 2 ? ASTAGE : 16];
@@ -189,7 +198,13 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     __shared__ __attribute__((aligned(512))) uint8_t sX2[kFp4 && NS > 2 ? XSTAGE : 16];
     __shared__ __attribute__((aligned(512))) uint8_t sX3[kFp4 && NS > 3 ? XSTAGE : 16];
     constexpr int kMaxKb = 64;                       // K <= 8192
-    __shared__ float s_scale[kWavesN][2][kMaxKb];
+    // fp8: per wave and column half, the factor applied to the accumulators at the start of each
+    // 128-wide K block, a mask that zeroes the widened codes of blocks with scale 0, and the scale
+    // of the last block (applied after the K loop)
+    __shared__ float s_ratio[kFp8 ? kWavesN : 1][2][kFp8 ? kMaxKb : 1];
+    __shared__ uint32_t s_keep[kFp8 ? kWavesN : 1][2][kFp8 ? kMaxKb : 1];
+    __shared__ float s_last[kWavesN][2];
+    __shared__ int32_t s_anyzero;
     __shared__ int32_t s_tok[kBM];
     __shared__ float s_gate[kBM];
     auto stA = [&](auto s) -> uint8_t * {
@@ -314,13 +329,17 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         }
     };
     const int nkb = K / 128;
-    // fp8 block scales of each wave's columns (gate half and up half of a gate/up tile; one
-    // block for down), one per 128-wide K block, staged in LDS before the pipeline starts: a
-    // vector load inside the loop would make the compiler drain the DMA stages
+    // fp8 block-scale tables of each wave's columns (gate half and up half of a gate/up tile; one
+    // block for down), staged in LDS before the pipeline starts: a vector load inside the loop
+    // would make the compiler drain the DMA stages.  One lane per (wave, half) walks the K blocks
+    // in order: s' = the block's scale, or the previous s' when the scale is 0 (1 before the
+    // first nonzero block); the ratio of block k is s'(k-1) / s'(k) (1 for block 0).
     if constexpr (kFp8) {
-        const float *s = static_cast<const float *>(EPI == GEMM_GATEUP ? a.s13 : a.s2);
-        for (int idx = t; idx < kWavesN * 2 * nkb; idx += kGemmThreads) {
-            const int w = idx / (2 * nkb), which = (idx / nkb) & 1, kb = idx % nkb;
+        if (t == 0) s_anyzero = 0;
+        __syncthreads();
+        if (t < kWavesN * 2) {
+            const float *sp = static_cast<const float *>(EPI == GEMM_GATEUP ? a.s13 : a.s2);
+            const int w = t >> 1, which = t & 1;
             int r;
             if constexpr (EPI == GEMM_GATEUP) {
                 const int hc0 = nt * (kBN / 2) + w * (kWaveCols / 2);
@@ -328,7 +347,19 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
             } else {
                 r = (nt * kBN + w * kWaveCols) / 128;
             }
-            s_scale[w][which][kb] = s[(static_cast<size_t>(slot) * (nrows / 128) + r) * nkb + kb];
+            const float *row = sp + (static_cast<size_t>(slot) * (nrows / 128) + r) * nkb;
+            float prev = 1.0f;
+            int zero = 0;
+            for (int kb = 0; kb < nkb; ++kb) {
+                const float sc = row[kb];
+                const float cur = sc != 0.0f ? sc : prev;
+                s_ratio[w][which][kb] = kb == 0 ? 1.0f : prev / cur;
+                s_keep[w][which][kb] = sc != 0.0f ? 0xFFFFFFFFu : 0u;
+                zero |= sc == 0.0f;
+                prev = cur;
+            }
+            s_last[w][which] = prev;
+            if (zero) atomicOr(&s_anyzero, 1);
         }
     }
     // token and gate of each row of the tile (down projection epilogue)
@@ -363,10 +394,13 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         u32x4_t a[kMI];
         u32x4_t b[kNJ];
         uint32_t xb[kNJ];   // MXFP4 e8m0 scale byte of each column tile
-        float sc[2];     // fp8 block scale of the gate (or down) and the up columns
+        float sc[2];        // fp8: accumulator factor of this K block, gate (or down) and up half
+        uint32_t keep[2];   // fp8: code mask of this K block (0 for a block with scale 0)
     };
-    auto load_frag = [&](auto rs, auto ks, auto ml, Frag &f, const Frag &prev, int kt) {
+    // zs: the tile holds an fp8 K block with scale 0 (codes of such blocks are masked)
+    auto load_frag = [&](auto rs, auto ks, auto ml, auto zs, Frag &f, const Frag &prev, int kt) {
         constexpr int KSI = decltype(ks)::value, ML = decltype(ml)::value;
+        constexpr bool ZS = decltype(zs)::value;
         const uint8_t *A = stA(rs);
         const uint8_t *B = stB(rs);
         const int ca = kFp8 ? 4 * (KSI / 2) + 2 * fq + (KSI % 2) : (kFp4 ? 4 * fq + KSI : 2 * KSI + fq);
@@ -398,28 +432,50 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         if constexpr (kFp8) {
             if constexpr (KSI == 0) {
                 const int kb = (kt * BK) / 128;
-                f.sc[0] = s_scale[wn][0][kb];
-                f.sc[1] = s_scale[wn][1][kb];
+                f.sc[0] = s_ratio[wn][0][kb];
+                f.sc[1] = s_ratio[wn][1][kb];
+                if constexpr (ZS) {
+                    f.keep[0] = s_keep[wn][0][kb];
+                    f.keep[1] = s_keep[wn][1][kb];
+                }
             } else {
                 f.sc[0] = prev.sc[0];
                 f.sc[1] = prev.sc[1];
+                if constexpr (ZS) {
+                    f.keep[0] = prev.keep[0];
+                    f.keep[1] = prev.keep[1];
+                }
             }
         }
     };
-    auto mma = [&](const Frag &f, auto ks, auto ml) {
+    // rs: this sub-step opens a 128-wide K block (fp8: the accumulators take the block's factor)
+    auto mma = [&](const Frag &f, auto ks, auto ml, auto zs, auto rs) {
         constexpr int KSI = decltype(ks)::value, ML = decltype(ml)::value;
+        constexpr bool ZS = decltype(zs)::value, RS = decltype(rs)::value;
         u32x4_t bf[kNJ];
 #pragma unroll
         for (int j = 0; j < kNJ; ++j) {
             if constexpr (kFp4) {
                 bf[j] = fp4x8_scaled_to_bf16x8(f.b[j][KSI], fp4_scale_operand(f.xb[j]));
             } else if constexpr (kFp8) {
-                const float s = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.sc[1] : f.sc[0];
-                bf[j] = KSI % 2 == 0 ? fp8x8_scaled_to_bf16x8(f.b[j][0], f.b[j][1], s)
-                                     : fp8x8_scaled_to_bf16x8(f.b[j][2], f.b[j][3], s);
+                bf[j] = KSI % 2 == 0 ? fp8x8_to_bf16x8(f.b[j][0], f.b[j][1]) : fp8x8_to_bf16x8(f.b[j][2], f.b[j][3]);
+                if constexpr (ZS) {
+                    const uint32_t keep = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.keep[1] : f.keep[0];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) bf[j][q] &= keep;
+                }
             } else {
                 bf[j] = f.b[j];
             }
+        }
+        if constexpr (kFp8 && RS) {
+#pragma unroll
+            for (int i = 0; i < ML; ++i)
+#pragma unroll
+                for (int j = 0; j < kNJ; ++j) {
+                    const float r = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.sc[1] : f.sc[0];
+                    acc[i][j] *= r;
+                }
         }
 #pragma unroll
         for (int i = 0; i < ML; ++i)
@@ -441,10 +497,12 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     // Order of one sub-step's instructions: its MFMAs with the next sub-step's operand reads
     // (sub-step ks2 of the same or the next stage) threaded between them, one read after each
     // MFMA.  Measured 2-4 % faster than issuing all the reads first behind an explicit wait.
-    auto interleave = [&](auto ks2, auto ml) {
+    auto interleave = [&](auto ks2, auto ml, auto zs) {
         constexpr int K2 = decltype(ks2)::value, ML = decltype(ml)::value;
+        constexpr bool ZS = decltype(zs)::value;
         constexpr bool kReadsB = kFp4 ? K2 == 0 : (kFp8 ? K2 % 2 == 0 : true);
-        constexpr int kReads = ML + (kReadsB ? kNJ : 0) + (kFp4 && K2 == 0 ? kNJ : 0) + (kFp8 && K2 == 0 ? 2 : 0);
+        constexpr int kReads = ML + (kReadsB ? kNJ : 0) + (kFp4 && K2 == 0 ? kNJ : 0) +
+                               (kFp8 && K2 == 0 ? (ZS ? 4 : 2) : 0);
         constexpr int kMfma = ML * kNJ;
         constexpr int kPairs = kReads < kMfma ? kReads : kMfma;
         static_for<0, kPairs>([&](auto) {
@@ -454,11 +512,13 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         if constexpr (kMfma > kPairs) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kPairs, 0);
         if constexpr (kReads > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kPairs, 0);
     };
-    auto mainloop = [&](auto ml) {
+    auto mainloop = [&](auto ml, auto zs) {
         Frag cur, nxt;
-        // stage kt, in ring slot S (= kt mod NS)
+        // stage kt, in ring slot S (= kt mod NS); fp8 K blocks open at the stages with
+        // S * BK = 0 mod 128 (the ring turn NS * BK is a multiple of 128)
         auto stage = [&](auto s, int kt) {
             constexpr int S = decltype(s)::value;
+            constexpr bool kOpens = kFp8 && (S * BK) % 128 == 0;
             static_for<0, KS>([&](auto ks) {
                 constexpr int KSI = decltype(ks)::value;
                 if constexpr (KSI + 1 == KS) {
@@ -468,12 +528,12 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
                     issue(min(kt + NS, nk - 1), stA(s), stB(s), s);
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                mma(cur, ks, ml);
+                mma(cur, ks, ml, zs, ic<(kOpens && KSI == 0) ? 1 : 0>{});
                 if constexpr (KSI + 1 < KS)
-                    load_frag(s, ic<KSI + 1>{}, ml, nxt, cur, kt);
+                    load_frag(s, ic<KSI + 1>{}, ml, zs, nxt, cur, kt);
                 else
-                    load_frag(ic<(S + 1) % NS>{}, ic<0>{}, ml, nxt, cur, min(kt + 1, nk - 1));
-                interleave(ic<(KSI + 1) % KS>{}, ml);
+                    load_frag(ic<(S + 1) % NS>{}, ic<0>{}, ml, zs, nxt, cur, min(kt + 1, nk - 1));
+                interleave(ic<(KSI + 1) % KS>{}, ml, zs);
                 __builtin_amdgcn_sched_barrier(0);
                 cur = nxt;
             });
@@ -481,7 +541,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         wait_vmcnt<(NS - 1) * PER_STAGE>();
         wait_lgkmcnt0();
         stage_barrier();
-        load_frag(ic<0>{}, ic<0>{}, ml, cur, cur, 0);
+        load_frag(ic<0>{}, ic<0>{}, ml, zs, cur, cur, 0);
         // whole turns of the ring without branches (a branch around a stage would make the
         // compiler lose track of which slot each DMA writes, and drain them all), then the rest
         int kt0 = 0;
@@ -504,9 +564,24 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     // (a wave of a tall tile may hold no real rows; it still moves its share of the stages)
     static_for<(kWavesM > 1 ? 0 : 1), kMI / MLQ + 1>([&](auto q) {
         constexpr int ML = decltype(q)::value * MLQ;
-        if (mlive == ML) mainloop(ic<ML>{});
+        if (mlive == ML) {
+            if constexpr (kFp8) {
+                if (s_anyzero) mainloop(ic<ML>{}, ic<1>{});
+                else mainloop(ic<ML>{}, ic<0>{});
+            } else {
+                mainloop(ic<ML>{}, ic<0>{});
+            }
+        }
     });
     wait_vmcnt<0>();   // the redundant tail stages
+    if constexpr (kFp8) {
+        // the accumulators hold the sum in units of the last block's scale
+        const float sg = s_last[wn][0], su = s_last[wn][1];
+#pragma unroll
+        for (int i = 0; i < kMI; ++i)
+#pragma unroll
+            for (int j = 0; j < kNJ; ++j) acc[i][j] *= (EPI == GEMM_GATEUP && j >= kNJ / 2) ? su : sg;
+    }
 
     // ---- epilogue: element e of a 32 x 32 tile in lane (fn, fq) is row 8 (e / 4) + 4 fq + e % 4,
     // column fn

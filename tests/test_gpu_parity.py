@@ -264,6 +264,29 @@ def test_forward_random_shapes(case):
         assert sizes.max() > 8 * GEMM_BM, "a group must span more than one band of M tiles"
 
 
+@pytest.mark.parametrize("T", [20, 300])
+def test_fp8_zero_block_scales(T):
+    """fp8 block scales of 0 (the weights of that block are 0) on the streaming path (T = 20) and
+    the matrix-core path (T = 300): a zero first block, a run of zero blocks, a zero last block,
+    and one expert whose gate/up scales are all zero."""
+    lay = workloads.random_layer(50 + T, hidden=512, inter=384, n_experts=8, top_k=3, tokens=T,
+                                 w_dtype=workloads.DT_FP8, gating=1, n_resident=8, shared=True,
+                                 device="cuda")
+    s13, s2 = lay.s13, lay.s2               # [slots][2I/128][H/128], [slots][H/128][I/128]
+    s13[0, :, 0] = 0
+    s13[1, 1, 1:3] = 0
+    s13[2, :, -1] = 0
+    s13[3] = 0
+    s2[0, :, 0] = 0
+    s2[4, 2, :] = 0
+    s2[5, :, 1] = 0
+    _say(f"fp8 zero block scales T={T}")
+    out, route = run_forward(lay)
+    ref, r = oracle.moe_partial(*oracle_inputs(lay))
+    check_route(route, r, T, lay.top_k)
+    check_output(out, ref, lay.w_dtype)
+
+
 def test_forward_T0_is_noop():
     lay = workloads.make_layer("tiny", 16, device="cuda")
     desc = lay.desc()
