@@ -230,25 +230,30 @@ def measure_bandwidths(cfg_name, n_fill, reps):
     w = torch.full((1, k), 1.0 / k)
     out = torch.empty(1, cfg.hidden)
     lst = torch.arange(k, dtype=torch.int32)
-    ftm.ft_cpu_experts(desc_c, pool, x, 1, ids, w, lst, out)
+    workers = ftm.ft_cpu_pool_create(0, pin=True)      # one worker per physical core
+    ftm.ft_cpu_experts(desc_c, pool, x, 1, ids, w, lst, out, pool=workers)
     t0 = time.perf_counter()
     for _ in range(reps):
-        ftm.ft_cpu_experts(desc_c, pool, x, 1, ids, w, lst, out)
+        ftm.ft_cpu_experts(desc_c, pool, x, 1, ids, w, lst, out, pool=workers)
     t_cpu = (time.perf_counter() - t0) / reps
+    ftm.ft_cpu_pool_destroy(workers)
     print(json.dumps({
         "measurement": "expert transfer (B_P) and host expert-processing (B_H) bandwidths",
         "workload": f"{cfg_name} experts ({S} bytes each), {n_fill} experts per call",
         "b_pcie_gbs": round(n_fill * S / t_fill / 1e9, 2), "fill_ms": round(t_fill * 1e3, 3),
         "fill_copy_exact": ok,
         "b_host_gbs": round(n_fill * S / t_cpu / 1e9, 2), "cpu_ms": round(t_cpu * 1e3, 3),
-        "cpu_threads": os.cpu_count(),
+        "cpu_pool": "one pinned worker per physical core of the affinity mask",
+        "affinity_cpus": len(os.sched_getaffinity(0)),
     }), flush=True)
 
 
 def hybrid_decode(cfg_name, T, steps, warmup, n_slots, b_pcie, b_host, max_fill):
-    """Complete decode layer steps over the GPU expert cache and the host: route, plan, fill,
-    GPU evaluation of hits and fills, CPU branch for the rest, exact merge (wall clock per step,
-    the CPU branch included)."""
+    """Complete decode layer steps over the GPU expert cache and the host: route once, plan,
+    fill, GPU evaluation of hits and fills, CPU branch for the rest (a host function on a
+    persistent pinned worker pool), exact merge.  Timed twice by wall clock over back-to-back
+    steps: enqueued eagerly, and as replays of one captured HIP graph (new inputs copied into its
+    fixed buffers before each replay)."""
     import numpy as np
     import torch
     import paper_2608_16157_amd as ftm
@@ -262,15 +267,7 @@ def hybrid_decode(cfg_name, T, steps, warmup, n_slots, b_pcie, b_host, max_fill)
     del dev_pool
     desc = dict(hidden=H, inter=cfg.inter, n_experts=E, top_k=cfg.top_k, gating=cfg.gating,
                 w_dtype=cfg.w_dtype, x_dtype=cfg.x_dtype, n_slots=n_slots, shared_slot=-1)
-    table = torch.full((E,), -1, dtype=torch.int32, device="cuda")
-    state = ftm.CacheState(torch.full((n_slots,), -1, dtype=torch.int32, device="cuda"),
-                           torch.zeros(n_slots, dtype=torch.int32, device="cuda"))
-    route = ftm.RouteBuffers(T, cfg.top_k, E)
-    plan = ftm.FillPlanBuffers(max_fill, E)
-    ws = ftm.alloc_workspace(desc, T)
-    host = ftm.HybridHostBuffers(T, cfg.top_k, E, H, torch.bfloat16)
-    out = torch.empty(T, H, dtype=torch.float32, device="cuda")
-    cpu_dev = torch.empty(T, H, dtype=torch.float32, device="cuda")
+    workers = ftm.ft_cpu_pool_create(0, pin=True)
     g = torch.Generator(device="cuda")
     g.manual_seed(77)
     rank = torch.randperm(E, generator=g, device="cuda").float() + 1
@@ -278,25 +275,62 @@ def hybrid_decode(cfg_name, T, steps, warmup, n_slots, b_pcie, b_host, max_fill)
     n = warmup + steps
     logits = [torch.randn(T, E, generator=g, device="cuda") + bias[None, :] for _ in range(n)]
     xs = [torch.randn(T, H, generator=g, device="cuda").to(torch.bfloat16) for _ in range(n)]
-    fills = cpus = misses = 0
-    for i in range(n):
-        if i == warmup:
+    res = {}
+    for mode in ("eager", "graph"):
+        table = torch.full((E,), -1, dtype=torch.int32, device="cuda")
+        state = ftm.CacheState(torch.full((n_slots,), -1, dtype=torch.int32, device="cuda"),
+                               torch.zeros(n_slots, dtype=torch.int32, device="cuda"),
+                               torch.zeros(1, dtype=torch.int32, device="cuda"))
+        for t in dev.values():
+            if t is not None:
+                t.zero_()
+        route = ftm.RouteBuffers(T, cfg.top_k, E)
+        plan = ftm.FillPlanBuffers(max_fill, E)
+        ws = ftm.alloc_workspace(desc, T)
+        host = ftm.HybridHostBuffers(T, cfg.top_k, E, H, torch.bfloat16)
+        out = torch.empty(T, H, dtype=torch.float32, device="cuda")
+        lg_buf = torch.empty(T, E, device="cuda")
+        x_buf = torch.empty(T, H, dtype=torch.bfloat16, device="cuda")
+        counts = torch.zeros(n, 4, dtype=torch.int32, device="cuda")
+
+        def call(i, lg, xx, stream=None):
+            ftm.ft_moe_step_hybrid(desc, dev, pool, lg, table, state, b_pcie, b_host, max_fill, i + 1,
+                                   xx, T, out, route, plan, host, ws, workers, stream=stream)
+
+        if mode == "graph":
+            graph = torch.cuda.CUDAGraph()
+            cap = torch.cuda.Stream()
             torch.cuda.synchronize()
-            t0 = time.perf_counter()
-        ftm.ft_moe_step_hybrid(desc, dev, pool, logits[i], table, state, b_pcie, b_host, max_fill,
-                               i + 1, xs[i], T, out, cpu_dev, route, plan, host, ws)
-        if i >= warmup:
-            c = host.plan_counts.tolist()
-            fills, cpus, misses = fills + c[0], cpus + c[1], misses + c[2]
-    torch.cuda.synchronize()
-    dt = (time.perf_counter() - t0) / steps
+            with torch.cuda.graph(graph, stream=cap, capture_error_mode="relaxed"):
+                call(0, lg_buf, x_buf, stream=cap)
+            torch.cuda.synchronize()
+        for i in range(n):
+            if i == warmup:
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+            if mode == "eager":
+                call(i, logits[i], xs[i])
+            else:
+                lg_buf.copy_(logits[i])
+                x_buf.copy_(xs[i])
+                graph.replay()
+            counts[i].copy_(plan.counts)
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / steps
+        c = counts[warmup:].float().mean(0).tolist()
+        res[mode] = {"ms_per_step": round(dt * 1e3, 4), "tokens_per_s": round(T / dt, 1),
+                     "fills_per_step": round(c[0], 2), "cpu_experts_per_step": round(c[1], 2),
+                     "missing_experts_per_step": round(c[2], 2)}
+        if mode == "graph":
+            del graph
+    ftm.ft_cpu_pool_destroy(workers)
     print(json.dumps({
-        "measurement": "hybrid decode layer step (GPU expert cache + fills + CPU branch + merge)",
+        "measurement": "hybrid decode layer step (GPU expert cache + fills + CPU branch + merge), "
+                       "back-to-back steps, wall clock",
         "workload": f"{cfg_name} shapes, T={T}, {n_slots} of {E} experts cacheable, Zipf "
-                    f"{cfg.zipf_s} routing, B_P={b_pcie} B_H={b_host} GB/s, K={max_fill}",
-        "tokens_per_s": round(T / dt, 1), "ms_per_step": round(dt * 1e3, 4),
-        "missing_experts_per_step": round(misses / steps, 2), "fills_per_step": round(fills / steps, 2),
-        "cpu_experts_per_step": round(cpus / steps, 2)}), flush=True)
+                    f"{cfg.zipf_s} routing, B_P={b_pcie} B_H={b_host} GB/s, K={max_fill}, CPU branch "
+                    f"on one pinned worker per CPU of the affinity mask",
+        **res}), flush=True)
 
 
 def cache_plan_timing(cfg_name, T, steps, warmup, n_slots, b_pcie, b_host, max_fill):
@@ -518,7 +552,7 @@ def cpu_baseline(lay, tokens):
                       f"{t_one:.1f} s on one thread"}
 
 
-def measure_forward(config, T, n_layers, steps, warmup, hip, stage_times=True):
+def measure_forward(config, T, n_layers, steps, warmup, hip, combine=0):
     """Time ``steps`` back-to-back ft_moe_forward calls over ``n_layers`` rotating instances of
     ``config`` at T tokens (inputs resident in HBM), then the same steps with stage events.
     Returns the throughput, the per-stage times and the dominant kernel's roofline, and the
@@ -529,7 +563,7 @@ def measure_forward(config, T, n_layers, steps, warmup, hip, stage_times=True):
     cfg = workloads.CONFIGS[config]
     print(f"# building {n_layers} layer instances of {config} T={T}", file=sys.stderr, flush=True)
     layers = [workloads.make_layer(config, T, layer=i, device="cuda") for i in range(n_layers)]
-    desc = layers[0].desc()
+    desc = dict(layers[0].desc(), combine=combine)
     ws = ftm.alloc_workspace(desc, T)
     routes = [ftm.RouteBuffers(T, cfg.top_k, cfg.n_experts) for _ in layers]
     out = torch.empty(T, cfg.hidden, dtype=torch.float32, device="cuda")
@@ -736,11 +770,16 @@ def main():
             r, lays = measure_forward(name, int(t), n_dec, max(10 * args.steps, 100), args.warmup, hip)
             del lays
             torch.cuda.empty_cache()
-            extras[f"{name}:T{t}"] = {k: r[k] for k in ("value", "ms_per_step", "workload",
-                                                        "layer_hbm_gbps", "layer_hbm_frac",
-                                                        "stage_ms", "roofline")}
-            extras[f"{name}:T{t}"]["unit"] = "tokens/s"
-            extras[f"{name}:T{t}"]["steps"] = max(10 * args.steps, 100)
+            ra, lays = measure_forward(name, int(t), n_dec, max(10 * args.steps, 100), args.warmup, hip,
+                                       combine=ftm.FT_COMBINE_ATOMIC)
+            del lays
+            torch.cuda.empty_cache()
+            e = {k: r[k] for k in ("value", "ms_per_step", "workload", "layer_hbm_gbps", "layer_hbm_frac",
+                                   "stage_ms", "roofline")}
+            e.update(unit="tokens/s", steps=max(10 * args.steps, 100), combine="ordered (bit-reproducible)",
+                     atomic_combine={k: ra[k] for k in ("value", "ms_per_step", "layer_hbm_gbps",
+                                                        "layer_hbm_frac", "stage_ms")})
+            extras[f"{name}:T{t}"] = e
         line["decode"] = extras
     print(json.dumps(line), flush=True)
 

@@ -18,9 +18,12 @@
  *
  * Conventions for every entry point:
  *   - All array arguments are DEVICE pointers owned by the caller, except where a field says
- *     host.  The library never allocates, frees or synchronises inside a call; it validates
- *     the arguments on the host, then enqueues kernels on `stream` (a hipStream_t; NULL means
- *     the null stream) and returns.
+ *     host.  No call allocates or frees device memory or waits for the device: each validates
+ *     its arguments on the host, then enqueues work on `stream` (a hipStream_t; NULL means the
+ *     null stream) and returns.  Exceptions, all host-side: ft_cpu_experts computes on the
+ *     calling thread or the pool's workers and returns when done; ft_cpu_pool_create starts
+ *     threads; ft_prefill_layers creates five timing-free hipEvents per call (each released by
+ *     the runtime once its work completes).
  *   - Host-checkable errors return a status before anything is enqueued.
  *   - The library keeps no state between calls and is reentrant; calls that share a
  *     workspace or output buffers must be ordered by the caller (same stream).
@@ -47,6 +50,15 @@ typedef enum {
 } ft_status_t;
 
 enum { FT_GATE_SOFTMAX_TOPK_RENORM = 0, FT_GATE_SIGMOID_TOPK_RENORM = 1 };
+
+/* How the streaming (few-token) path sums a token's gate-weighted expert outputs (ft_moe_desc_t
+ * .combine).  ORDERED: every expert output is stored by pair index and one kernel sums each
+ * output element in a fixed order (routed pairs by ascending j, then the shared expert), so the
+ * layer output is bit-reproducible; it costs one kernel launch and T*(k+1)*H*4 bytes of
+ * workspace traffic.  ATOMIC: float32 atomic adds straight from the down projection, the order
+ * of a token's k sums (and so the last bits) may differ between calls.  The matrix-core path
+ * (T >= 256) always adds atomically. */
+enum { FT_COMBINE_ORDERED = 0, FT_COMBINE_ATOMIC = 1 };
 
 enum {
     FT_DT_F32 = 0,              /* IEEE float32 */
@@ -81,9 +93,10 @@ enum {
  *   n_slots: number of bank rows (cache slots) in the banks, >= 0.
  *   shared_slot: bank row of an always-resident shared expert with gate 1 for every token,
  *                or -1 for none.
+ *   combine: FT_COMBINE_* (0, the ordered combine, for a zero-initialised struct).
  */
 typedef struct {
-    int32_t hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot;
+    int32_t hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot, combine;
 } ft_moe_desc_t;
 
 /*
@@ -170,9 +183,9 @@ ft_status_t ft_route_only(const ft_moe_desc_t *desc, const float *logits, const 
  * CPU partial sums merge exactly).
  *   x           [T][H] device, x_dtype
  *   out_partial [T][H] float32 device, fully overwritten; a token with no hit (and no shared
- *               expert) gets exact zeros.  The gate-weighted expert outputs are summed with
- *               float32 atomic adds, so the order of that sum (and the last bits) may differ
- *               between calls; the routing outputs are bit-reproducible.
+ *               expert) gets exact zeros.  The routing outputs are bit-reproducible; so is
+ *               out_partial with desc->combine = FT_COMBINE_ORDERED below 256 tokens (else the
+ *               order of a token's sum, and its last bits, may differ between calls).
  *   x, out_partial, banks->w13 and banks->w2 (and for MXFP4 banks->s13 and banks->s2) must be
  *   16-byte aligned (FT_ERR_SHAPE otherwise).
  */
@@ -189,7 +202,8 @@ ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, c
  * nothing.  Every argument and every result is as for ft_moe_forward.
  *   Returns FT_ERR_CAPACITY, before enqueuing anything, when ft_moe_workspace_bytes(desc, T)
  *   exceeds FT_NOALLOC_SCRATCH_BYTES (e.g. 64 MiB holds a Qwen3-30B-A3B-shaped layer up to 4096
- *   tokens and a DeepSeek-V3-shaped one up to 1024).  FT_ERR_HIP if the array's device address
+ *   tokens, and a DeepSeek-V3-shaped one up to 1811 tokens except 228..255 with the ordered
+ *   combine, whose per-pair outputs take T*(k+1)*H*4 bytes).  FT_ERR_HIP if the array's device address
  *   cannot be found: it is looked up on the first call on each device (make that first call, a
  *   T = 0 call will do, before capturing a graph).
  *   All calls on one GPU share its array and nothing in it is kept between calls: calls that may
@@ -273,6 +287,9 @@ ft_status_t ft_miss_list_to_host(const ft_moe_desc_t *desc, const ft_route_t *ro
 typedef struct {
     int32_t *slot_expert;
     uint32_t *slot_stamp;
+    uint32_t *clock;   /* [1] device step counter, or NULL.  When set, the step's stamp is
+                          clock + 1 (written back), and policy->step is ignored: a captured step
+                          then advances on every replay */
 } ft_cache_state_t;
 
 typedef struct {
@@ -296,23 +313,37 @@ ft_status_t ft_cache_plan(const ft_moe_desc_t *desc, const ft_route_t *route, in
                           void *stream);
 
 /*
+ * Persistent CPU worker pool of the CPU branch (Section 4.1: a native worker pool with SIMD
+ * kernels).  n_threads workers (<= 0: one per CPU of the process's affinity mask); pin != 0
+ * pins each worker to one CPU of the mask, one hardware thread of every physical core first,
+ * then their second hardware threads.  Returns NULL if
+ * the threads cannot be started.  A pool runs one job at a time (calls that share it are
+ * serialised); destroy it only when no call that uses it is running or enqueued.  A pool
+ * holds a small mailbox in pinned host memory through which hybrid steps hand their CPU branch
+ * to a listener thread of the pool (created without a GPU, the pool has none and serves
+ * ft_cpu_experts only; hybrid steps then hand over with a host function).
+ */
+typedef struct ft_cpu_pool ft_cpu_pool_t;
+ft_cpu_pool_t *ft_cpu_pool_create(int32_t n_threads, int32_t pin);
+void ft_cpu_pool_destroy(ft_cpu_pool_t *pool);
+
+/*
  * CPU branch of a layer step (Section 3.2: the missing experts the split leaves to the CPU
  * execute from the host expert pool, concurrently with the GPU, and the two partial sums add up
- * to the exact layer output; Section 4.1: a native worker pool with SIMD kernels and in-kernel
- * dequantisation).  HOST pointers, caller-owned; runs synchronously on the calling thread plus
- * n_threads - 1 workers (n_threads <= 0: one per hardware thread).
+ * to the exact layer output; Section 4.1: in-kernel dequantisation).  HOST pointers,
+ * caller-owned; runs synchronously on the workers of `pool` (NULL: on the calling thread).
  *   host_pool   the complete expert pool in host memory, indexed by EXPERT id, in the bank
  *               layout of ft_banks_t: w13 [E][2I][H], w2 [E][H][I], s13/s2 per expert (fp8)
  *   x           [T][H] x_dtype;  topk_ids, topk_w [T][k]: this step's routing
  *   experts     n_list distinct expert ids to evaluate (e.g. ft_fill_plan_t.cpu_expert)
  *   out         [T][H] float32, overwritten: out[t] = sum over (t, j) with topk_ids[t][j] in
  *               experts of topk_w[t][j] * FFN_e(x_t), every product accumulated in float32 and
- *               every element summed in a fixed order (independent of n_threads)
+ *               every element summed in a fixed order (independent of the pool)
  * Returns FT_ERR_DTYPE if the host CPU lacks AVX2 and FMA.
  */
 ft_status_t ft_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_pool, const void *x,
                            int32_t T, const int32_t *topk_ids, const float *topk_w,
-                           const int32_t *experts, int32_t n_list, float *out, int32_t n_threads);
+                           const int32_t *experts, int32_t n_list, float *out, ft_cpu_pool_t *pool);
 
 /*
  * Cache fills of one step (Section 3.2: the q planned experts are copied into their slots over
@@ -331,8 +362,16 @@ ft_status_t ft_cache_fill(const ft_moe_desc_t *desc, const ft_banks_t *host_pool
                           void *stream);
 
 /*
- * Host staging of ft_moe_step_hybrid: pinned host buffers, caller-owned, capacity for T tokens.
+ * Host side of ft_moe_step_hybrid, caller-owned, capacity for T tokens: pinned host buffers
+ * (hipHostMalloc; x and cpu_out 16-byte aligned) that the device writes the step's routing and
+ * plan into and reads the CPU partial from, over PCIe, and `task`, plain host memory the call
+ * writes what its CPU branch needs into.  All of it must stay valid while the step (or any graph
+ * captured from it) can run.
  */
+typedef struct {
+    uint64_t opaque[24];
+} ft_hybrid_task_t;
+
 typedef struct {
     int32_t *plan_counts;   /* [4] */
     int32_t *cpu_expert;    /* [E] */
@@ -340,29 +379,42 @@ typedef struct {
     float *topk_w;          /* [T*k] */
     void *x;                /* [T][H] x_dtype */
     float *cpu_out;         /* [T][H] the CPU partial */
+    ft_hybrid_task_t *task; /* written by the call (not pinned memory) */
 } ft_hybrid_host_t;
 
 /*
- * One complete MoE layer step over the GPU expert cache and the host (Section 3.2): route on the
- * current slot table, plan the cache (ft_cache_plan), fill the planned slots (ft_cache_fill),
- * evaluate hits and fills on the GPU (ft_moe_forward on the updated slot table) while the host
- * evaluates the experts the plan leaves to the CPU (ft_cpu_experts), then add the CPU partial to
- * the GPU's: `out` receives the exact layer output over all routed experts (+ shared expert).
- * Blocks the calling thread until the CPU branch is done; the GPU part (fills, evaluation, the
- * copy of the CPU partial and the merge) is enqueued on `stream`, so `out`, the cache state and
- * host->cpu_out must not be used or reused before the stream is synchronised.
+ * One complete MoE layer step over the GPU expert cache and the host (Section 3.2; Section 4.1
+ * keeps the whole step in fixed-shape buffers with device-resident counts, so it can be captured
+ * in a graph and replayed).  Enqueues on `stream`, without waiting for the device:
+ *   1. the routing on the current slot table (ft_route_only) and the cache plan (ft_cache_plan,
+ *      which updates the slot table and rewrites the routed slot ids of the experts it fills);
+ *   2. one kernel that writes the plan counts, the CPU list, the routing and x into the pinned
+ *      host staging, and one that posts the step to the pool's mailbox; the pool's listener
+ *      thread, polling it, evaluates the experts the plan leaves to the CPU into host->cpu_out
+ *      on the pool's workers (NULL pool: a host function, hipLaunchHostFunc, evaluates them on
+ *      the runtime's callback thread before the stream goes on);
+ *   3. the fills (ft_cache_fill) and the grouped evaluation of G = H u F straight from the
+ *      rewritten slot ids (the step routes once), overlapping the CPU branch;
+ *   4. a kernel that waits for the pool to report the step done (bounded: after tens of seconds
+ *      without an answer it gives up, counting a timeout in the mailbox, and the output lacks the
+ *      CPU partial), and the addition of the CPU partial (read over PCIe): `out` receives the
+ *      exact layer output over all routed experts (+ shared expert).
+ * Synchronise `stream` before using `out`, the cache state or the staging buffers.  Capturing
+ * the call on `stream` gives a graph whose replays each run one step on the same buffers; give
+ * `state` a device clock so that the stamps advance.  Steps that share a pool run their CPU
+ * branches one at a time.
  *   slot_table, state  updated in place as by ft_cache_plan
  *   out          [T][H] float32 device: the full layer output
- *   cpu_out_dev  [T][H] float32 device scratch (16-byte aligned) for the CPU partial
- *   route, plan, ws    as for the calls above; route holds the second (post-fill) routing
+ *   route, plan, ws    as for the calls above
+ *   Returns FT_ERR_SHAPE if a staging buffer is not pinned host memory or is misaligned.
  */
 ft_status_t ft_moe_step_hybrid(const ft_moe_desc_t *desc, const ft_banks_t *dev_banks,
                                const ft_banks_t *host_pool, const float *logits, int32_t *slot_table,
                                const ft_cache_state_t *state, const ft_cache_policy_t *policy,
-                               const void *x, int32_t T, float *out, float *cpu_out_dev,
+                               const void *x, int32_t T, float *out,
                                const ft_route_t *route, const ft_fill_plan_t *plan,
                                const ft_hybrid_host_t *host, void *ws, size_t ws_bytes,
-                               int32_t n_threads, void *stream);
+                               ft_cpu_pool_t *pool, void *stream);
 
 /*
  * Full-layer double-buffered prefill of one chunk of T tokens through n_layers MoE layers whose

@@ -12,10 +12,11 @@ of the C ABI declared in ``include/ftmoe.h``:
     ft_moe_forward_noalloc(desc, banks, logits, slot_table, x, T, out_partial, route, stream=None)
     ft_miss_list_to_host(desc, route, T, host, stream=None)
     ft_cache_plan(desc, route, T, slot_table, state, policy, plan, stream=None)
-    ft_cpu_experts(desc, host_pool, x, T, topk_ids, topk_w, experts, out, n_threads=0)
+    ft_cpu_pool_create(n_threads=0, pin=True) -> CpuPool;  ft_cpu_pool_destroy(pool)
+    ft_cpu_experts(desc, host_pool, x, T, topk_ids, topk_w, experts, out, pool=None)
     ft_cache_fill(desc, host_pool, dev_banks, plan, max_fill, stream=None)
-    ft_moe_step_hybrid(desc, dev_banks, host_pool, logits, slot_table, state, policy, x, T, out,
-                       cpu_out_dev, route, plan, host, ws, n_threads=0, stream=None)
+    ft_moe_step_hybrid(desc, dev_banks, host_pool, logits, slot_table, state, b_pcie, b_host,
+                       max_fill, step, x, T, out, route, plan, host, ws, pool, stream=None)
     ft_prefill_layers(desc, host_layers, dev_bufs, slot_table, logits, x, T, out, route, ws,
                       overlap=True, stream=None, copy_stream=None)
     ft_status_string(status) -> str
@@ -37,13 +38,15 @@ LIB_PATH = os.path.join(HERE, "libftmoe.so")
 
 FT_OK, FT_ERR_NULL, FT_ERR_SHAPE, FT_ERR_DTYPE, FT_ERR_CAPACITY, FT_ERR_HIP = range(6)
 FT_GATE_SOFTMAX_TOPK_RENORM, FT_GATE_SIGMOID_TOPK_RENORM = 0, 1
+FT_COMBINE_ORDERED, FT_COMBINE_ATOMIC = 0, 1
 FT_DT_F32, FT_DT_BF16, FT_DT_FP8E4M3FN_B128, FT_DT_MXFP4 = 0, 1, 2, 3
 FT_SLOT_MISS = -1
 FT_DEV_SLOT_RANGE, FT_DEV_SLOT_DUP, FT_DEV_SLOT_SHARED = 1, 2, 4
 
 EXPORTED = ("ft_moe_workspace_bytes", "ft_route_only", "ft_moe_forward", "ft_moe_forward_noalloc",
             "ft_moe_forward_profiled", "ft_miss_list_to_host", "ft_cache_plan", "ft_cpu_experts",
-            "ft_cache_fill", "ft_moe_step_hybrid", "ft_prefill_layers", "ft_status_string")
+            "ft_cache_fill", "ft_moe_step_hybrid", "ft_prefill_layers", "ft_status_string",
+            "ft_cpu_pool_create", "ft_cpu_pool_destroy")
 FT_PROF_STAGES = 4
 FT_NOALLOC_SCRATCH_BYTES = 64 << 20
 
@@ -56,7 +59,8 @@ class FtError(RuntimeError):
 
 class ft_moe_desc_t(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("hidden", "inter", "n_experts", "top_k", "gating",
-                                              "w_dtype", "x_dtype", "n_slots", "shared_slot")]
+                                              "w_dtype", "x_dtype", "n_slots", "shared_slot",
+                                              "combine")]
 
 
 class ft_banks_t(ctypes.Structure):
@@ -79,7 +83,8 @@ class ft_host_miss_t(ctypes.Structure):
 
 
 class ft_cache_state_t(ctypes.Structure):
-    _fields_ = [("slot_expert", ctypes.c_void_p), ("slot_stamp", ctypes.c_void_p)]
+    _fields_ = [("slot_expert", ctypes.c_void_p), ("slot_stamp", ctypes.c_void_p),
+                ("clock", ctypes.c_void_p)]
 
 
 class ft_cache_policy_t(ctypes.Structure):
@@ -94,7 +99,10 @@ class ft_fill_plan_t(ctypes.Structure):
 
 class ft_hybrid_host_t(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in ("plan_counts", "cpu_expert", "topk_ids", "topk_w", "x",
-                                               "cpu_out")]
+                                               "cpu_out", "task")]
+
+
+FT_HYBRID_TASK_BYTES = 24 * 8
 
 
 _lib: Optional[ctypes.CDLL] = None
@@ -133,19 +141,23 @@ def load(path: str = None) -> ctypes.CDLL:
     lib.ft_cache_plan.argtypes = [P(ft_moe_desc_t), P(ft_route_t), ctypes.c_int32, ctypes.c_void_p,
                                   P(ft_cache_state_t), P(ft_cache_policy_t), P(ft_fill_plan_t),
                                   ctypes.c_void_p]
+    lib.ft_cpu_pool_create.restype = ctypes.c_void_p
+    lib.ft_cpu_pool_create.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    lib.ft_cpu_pool_destroy.restype = None
+    lib.ft_cpu_pool_destroy.argtypes = [ctypes.c_void_p]
     lib.ft_cpu_experts.restype = ctypes.c_int
     lib.ft_cpu_experts.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), ctypes.c_void_p, ctypes.c_int32,
                                    ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int32,
-                                   ctypes.c_void_p, ctypes.c_int32]
+                                   ctypes.c_void_p, ctypes.c_void_p]
     lib.ft_cache_fill.restype = ctypes.c_int
     lib.ft_cache_fill.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), P(ft_banks_t), P(ft_fill_plan_t),
                                   ctypes.c_int32, ctypes.c_void_p]
     lib.ft_moe_step_hybrid.restype = ctypes.c_int
     lib.ft_moe_step_hybrid.argtypes = [P(ft_moe_desc_t), P(ft_banks_t), P(ft_banks_t), ctypes.c_void_p,
                                        ctypes.c_void_p, P(ft_cache_state_t), P(ft_cache_policy_t),
-                                       ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p,
                                        P(ft_route_t), P(ft_fill_plan_t), P(ft_hybrid_host_t),
-                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32, ctypes.c_void_p]
+                                       ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
     lib.ft_prefill_layers.restype = ctypes.c_int
     lib.ft_prefill_layers.argtypes = [P(ft_moe_desc_t), ctypes.c_int32, P(ft_banks_t), P(ft_banks_t),
                                       ctypes.c_void_p, P(ctypes.c_void_p), P(ctypes.c_void_p),
@@ -267,7 +279,8 @@ def _stream(stream) -> Optional[int]:
 
 
 def make_desc(d: dict) -> ft_moe_desc_t:
-    return ft_moe_desc_t(**{f: int(d[f]) for f, _ in ft_moe_desc_t._fields_})
+    """ft_moe_desc_t from a dict; ``combine`` defaults to FT_COMBINE_ORDERED."""
+    return ft_moe_desc_t(**{f: int(d.get(f, 0) if f == "combine" else d[f]) for f, _ in ft_moe_desc_t._fields_})
 
 
 class RouteBuffers:
@@ -400,15 +413,18 @@ def ft_miss_list_to_host(desc: dict, route: RouteBuffers, T: int, host: HostMiss
 
 
 class CacheState:
-    """Device tensors behind one ft_cache_state_t: slot -> expert (-1 empty) and the slot stamps
-    (uint32 in the ABI; held as int32 here, stamps stay below 2**31)."""
+    """Device tensors behind one ft_cache_state_t: slot -> expert (-1 empty), the slot stamps
+    (uint32 in the ABI; held as int32 here, stamps stay below 2**31) and an optional one-element
+    device step clock."""
 
-    def __init__(self, slot_expert: torch.Tensor, slot_stamp: torch.Tensor):
+    def __init__(self, slot_expert: torch.Tensor, slot_stamp: torch.Tensor,
+                 clock: Optional[torch.Tensor] = None):
         self.slot_expert = slot_expert
         self.slot_stamp = slot_stamp
+        self.clock = clock
 
     def c(self) -> ft_cache_state_t:
-        return ft_cache_state_t(_ptr(self.slot_expert), _ptr(self.slot_stamp))
+        return ft_cache_state_t(_ptr(self.slot_expert), _ptr(self.slot_stamp), _ptr(self.clock))
 
 
 class FillPlanBuffers:
@@ -449,10 +465,49 @@ def ft_cache_plan(desc: dict, route: RouteBuffers, T: int, slot_table: torch.Ten
     _check(st, "ft_cache_plan")
 
 
+class CpuPool:
+    """A persistent CPU worker pool (ft_cpu_pool_t); destroyed with ft_cpu_pool_destroy or when
+    garbage-collected."""
+
+    def __init__(self, handle: int, n_threads: int, pin: bool):
+        self.handle, self.n_threads, self.pin = handle, n_threads, pin
+
+    def close(self) -> None:
+        if self.handle:
+            load().ft_cpu_pool_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def ft_cpu_pool_create(n_threads: int = 0, pin: bool = True) -> CpuPool:
+    h = load().ft_cpu_pool_create(int(n_threads), 1 if pin else 0)
+    if not h:
+        raise RuntimeError("ft_cpu_pool_create failed")
+    return CpuPool(h, n_threads, pin)
+
+
+def ft_cpu_pool_destroy(pool: CpuPool) -> None:
+    pool.close()
+
+
+def _pool_handle(pool) -> Optional[int]:
+    if pool is None:
+        return None
+    if not isinstance(pool, CpuPool) or not pool.handle:
+        raise ValueError("pool: expected an open CpuPool or None")
+    return pool.handle
+
+
 def ft_cpu_experts(desc: dict, host_pool: dict, x: torch.Tensor, T: int, topk_ids: torch.Tensor,
                    topk_w: torch.Tensor, experts: torch.Tensor, out: torch.Tensor,
-                   n_threads: int = 0) -> None:
-    """CPU branch on host tensors: ``host_pool`` holds w13, w2 (s13, s2) indexed by expert id."""
+                   pool: Optional[CpuPool] = None) -> None:
+    """CPU branch on host tensors: ``host_pool`` holds w13, w2 (s13, s2) indexed by expert id;
+    runs on ``pool``'s workers, or on the calling thread without one."""
     if int(T) > 0:
         E, H, k = int(desc["n_experts"]), int(desc["hidden"]), int(desc["top_k"])
         xd = _X_DTYPES.get(int(desc["x_dtype"]))
@@ -469,7 +524,7 @@ def ft_cpu_experts(desc: dict, host_pool: dict, x: torch.Tensor, T: int, topk_id
                    _ptr(host_pool.get("s2")))
     st = load().ft_cpu_experts(ctypes.byref(make_desc(desc)), ctypes.byref(b), _ptr(x), int(T),
                                _ptr(topk_ids), _ptr(topk_w), _ptr(experts), int(experts.numel()),
-                               _ptr(out), int(n_threads))
+                               _ptr(out), _pool_handle(pool))
     _check(st, "ft_cpu_experts")
 
 
@@ -502,6 +557,8 @@ class HybridHostBuffers:
         self.topk_w = torch.empty(pk, dtype=torch.float32, **kw)
         self.x = torch.empty(max(T, 1), hidden, dtype=x_dtype, **kw)
         self.cpu_out = torch.empty(max(T, 1), hidden, dtype=torch.float32, **kw)
+        self.task = torch.zeros(FT_HYBRID_TASK_BYTES, dtype=torch.uint8)   # plain host memory
+        self.T, self.k, self.E, self.H = T, top_k, n_experts, hidden
 
     def c(self) -> ft_hybrid_host_t:
         return ft_hybrid_host_t(*[_ptr(getattr(self, n)) for n, _ in ft_hybrid_host_t._fields_])
@@ -510,16 +567,29 @@ class HybridHostBuffers:
 def ft_moe_step_hybrid(desc: dict, dev_banks: dict, host_pool: dict, logits: torch.Tensor,
                        slot_table: torch.Tensor, state: CacheState, b_pcie: float, b_host: float,
                        max_fill: int, step: int, x: torch.Tensor, T: int, out: torch.Tensor,
-                       cpu_out_dev: torch.Tensor, route: RouteBuffers, plan: FillPlanBuffers,
-                       host: HybridHostBuffers, ws: torch.Tensor, n_threads: int = 0,
+                       route: RouteBuffers, plan: FillPlanBuffers,
+                       host: HybridHostBuffers, ws: torch.Tensor, pool: Optional[CpuPool],
                        stream=None) -> None:
+    """One complete hybrid layer step, enqueued on ``stream`` without waiting for the device."""
+    if int(T) > 0:
+        _need_layer_inputs(desc, logits, slot_table, T, x, out)
+        _need_route(route, desc, T)
+        _need(ws, "ws", torch.uint8, 0)
+        _need_banks(desc, dev_banks, int(desc["n_slots"]), "dev_banks")
+        _need_banks(desc, host_pool, int(desc["n_experts"]), "host_pool", "cpu")
+        _need_plan(desc, slot_table, state, plan, max_fill)
+        if host.T < T or host.k != int(desc["top_k"]) or host.E != int(desc["n_experts"]) or \
+                host.H != int(desc["hidden"]):
+            raise ValueError("host: HybridHostBuffers sized for another layer or fewer tokens")
+        if state.clock is not None:
+            _need(state.clock, "state.clock", (torch.int32, torch.uint32), 1)
     pol = ft_cache_policy_t(float(b_pcie), float(b_host), int(max_fill), int(step))
     st = load().ft_moe_step_hybrid(ctypes.byref(make_desc(desc)), ctypes.byref(_banks(dev_banks)),
                                    ctypes.byref(_banks(host_pool)), _ptr(logits), _ptr(slot_table),
                                    ctypes.byref(state.c()), ctypes.byref(pol), _ptr(x), int(T),
-                                   _ptr(out), _ptr(cpu_out_dev), ctypes.byref(route.c()),
+                                   _ptr(out), ctypes.byref(route.c()),
                                    ctypes.byref(plan.c()), ctypes.byref(host.c()), _ptr(ws),
-                                   ws.numel(), int(n_threads), _stream(stream))
+                                   ws.numel(), _pool_handle(pool), _stream(stream))
     _check(st, "ft_moe_step_hybrid")
 
 

@@ -2,6 +2,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cstring>
 #include <mutex>
 #include <thread>
 #include <vector>
@@ -20,6 +21,7 @@ bool desc_ok(const ft_moe_desc_t *d) {
     if (d->top_k < 1 || d->top_k > d->n_experts || d->top_k > kMaxTopK) return false;
     if (d->n_slots < 0) return false;
     if (d->shared_slot < -1 || d->shared_slot >= d->n_slots) return false;
+    if (d->combine != FT_COMBINE_ORDERED && d->combine != FT_COMBINE_ATOMIC) return false;
     return true;
 }
 
@@ -49,7 +51,7 @@ ft_status_t check_common(const ft_moe_desc_t *desc, const float *logits, const i
 }
 
 WsView carve(const ft_moe_desc_t *d, int T, void *ws) {
-    const WsLayout L = ws_layout(d->n_experts, d->hidden, d->inter, d->top_k, d->w_dtype, T);
+    const WsLayout L = ws_layout(d->n_experts, d->hidden, d->inter, d->top_k, d->w_dtype, d->combine, T);
     uint8_t *b = static_cast<uint8_t *>(ws);
     WsView v;
     v.eff_slot = reinterpret_cast<int32_t *>(b + L.eff_slot);
@@ -62,7 +64,9 @@ WsView carve(const ft_moe_desc_t *d, int T, void *ws) {
     v.mt_group = reinterpret_cast<int32_t *>(b + L.mt_group);
     v.row_tok = reinterpret_cast<int32_t *>(b + L.row_tok);
     v.row_gate = reinterpret_cast<float *>(b + L.row_gate);
+    v.row_pair = reinterpret_cast<int32_t *>(b + L.row_pair);
     v.h = b + L.h;
+    v.ypart = L.ypart_bytes ? reinterpret_cast<float *>(b + L.ypart) : nullptr;
     return v;
 }
 
@@ -122,7 +126,7 @@ extern "C" {
 size_t ft_moe_workspace_bytes(const ft_moe_desc_t *desc, int32_t max_tokens) {
     if (!desc_ok(desc) || max_tokens < 0) return 0;
     const int T = max_tokens > 0 ? max_tokens : 1;
-    return ws_layout(desc->n_experts, desc->hidden, desc->inter, desc->top_k, desc->w_dtype, T).total;
+    return ws_layout(desc->n_experts, desc->hidden, desc->inter, desc->top_k, desc->w_dtype, desc->combine, T).total;
 }
 
 ft_status_t ft_route_only(const ft_moe_desc_t *desc, const float *logits, const int32_t *slot_table,
@@ -141,6 +145,10 @@ ft_status_t ft_route_only(const ft_moe_desc_t *desc, const float *logits, const 
 
 namespace {
 
+hipError_t enqueue_experts(const ft_moe_desc_t *desc, const ft_banks_t *banks, const void *x, int32_t T,
+                           float *out_partial, const ft_route_t *route, const WsView &wv, hipStream_t s,
+                           const Prof &prof);
+
 ft_status_t forward_impl(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
                          const int32_t *slot_table, const void *x, int32_t T, float *out_partial,
                          const ft_route_t *route, void *ws, size_t ws_bytes, void *stream,
@@ -155,7 +163,19 @@ ft_status_t forward_impl(const ft_moe_desc_t *desc, const ft_banks_t *banks, con
     const RouteArgs ra = route_args(desc, logits, slot_table, T, route, wv);
     if (!prof.mark(0)) return FT_ERR_HIP;
     if (launch_route(ra, s) != hipSuccess) return FT_ERR_HIP;
+    if (enqueue_experts(desc, banks, x, T, out_partial, route, wv, s, prof) != hipSuccess) return FT_ERR_HIP;
+    if (!prof.mark(FT_PROF_STAGES)) return FT_ERR_HIP;
+    return FT_OK;
+}
 
+}  // namespace
+
+namespace {
+
+// The grouped expert FFN and the combine over the groups the workspace holds.
+hipError_t enqueue_experts(const ft_moe_desc_t *desc, const ft_banks_t *banks, const void *x, int32_t T,
+                           float *out_partial, const ft_route_t *route, const WsView &wv, hipStream_t s,
+                           const Prof &prof) {
     ExpertArgs ea{};
     ea.w13 = banks->w13;
     ea.w2 = banks->w2;
@@ -175,11 +195,9 @@ ft_status_t forward_impl(const ft_moe_desc_t *desc, const ft_banks_t *banks, con
     if (routed_slots < mg) mg = routed_slots;
     if (static_cast<long>(T) * desc->top_k < mg) mg = static_cast<long>(T) * desc->top_k;
     ea.max_groups = static_cast<int>(mg) + ea.shared;
-    ea.ro = ra.ro;
+    ea.ro = route_out(route);
     ea.wv = wv;
-    if (launch_experts(ea, s, prof) != hipSuccess) return FT_ERR_HIP;
-    if (!prof.mark(FT_PROF_STAGES)) return FT_ERR_HIP;
-    return FT_OK;
+    return launch_experts(ea, s, prof);
 }
 
 }  // namespace
@@ -224,6 +242,10 @@ ft_status_t scratch_address(void **addr) {
     return FT_OK;
 }
 
+}  // namespace
+
+namespace {
+void hybrid_cpu_task(void *p);
 }  // namespace
 
 extern "C" {
@@ -286,6 +308,7 @@ ft_status_t ft_cache_plan(const ft_moe_desc_t *desc, const ft_route_t *route, in
     a.slot_table = slot_table;
     a.slot_expert = state->slot_expert;
     a.slot_stamp = state->slot_stamp;
+    a.clock = state->clock;
     a.fill_expert = plan->fill_expert;
     a.fill_slot = plan->fill_slot;
     a.evict_expert = plan->evict_expert;
@@ -294,25 +317,33 @@ ft_status_t ft_cache_plan(const ft_moe_desc_t *desc, const ft_route_t *route, in
     return launch_cache_plan(a, static_cast<hipStream_t>(stream)) == hipSuccess ? FT_OK : FT_ERR_HIP;
 }
 
-ft_status_t ft_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_pool, const void *x,
-                           int32_t T, const int32_t *topk_ids, const float *topk_w,
-                           const int32_t *experts, int32_t n_list, float *out, int32_t n_threads) {
+ft_cpu_pool_t *ft_cpu_pool_create(int32_t n_threads, int32_t pin) {
+    if (n_threads > 4096) return nullptr;
+    return reinterpret_cast<ft_cpu_pool_t *>(CpuPool::create(n_threads, pin != 0, hybrid_cpu_task));
+}
+
+void ft_cpu_pool_destroy(ft_cpu_pool_t *pool) { delete reinterpret_cast<CpuPool *>(pool); }
+
+}  // extern "C"
+
+namespace {
+
+ft_status_t check_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_pool, int32_t T, int32_t n_list) {
     using namespace ftmoe;
     if (!desc || !host_pool) return FT_ERR_NULL;
     if (!desc_ok(desc)) return FT_ERR_SHAPE;
     if (ft_status_t st = dtype_status(desc); st != FT_OK) return st;
     if (T < 0 || n_list < 0 || n_list > desc->n_experts) return FT_ERR_SHAPE;
-    if (T == 0) return FT_OK;
-    if (!x || !topk_ids || !topk_w || !out || (n_list > 0 && !experts)) return FT_ERR_NULL;
     if (n_list > 0 && (!host_pool->w13 || !host_pool->w2)) return FT_ERR_NULL;
-    if (has_scales(desc->w_dtype) && n_list > 0 && (!host_pool->s13 || !host_pool->s2)) return FT_ERR_NULL;
-    std::vector<char> seen(desc->n_experts, 0);
-    for (int i = 0; i < n_list; ++i) {
-        const int e = experts[i];
-        if (e < 0 || e >= desc->n_experts || seen[e]) return FT_ERR_SHAPE;
-        seen[e] = 1;
-    }
+    if (n_list > 0 && has_scales(desc->w_dtype) && (!host_pool->s13 || !host_pool->s2)) return FT_ERR_NULL;
     if (!__builtin_cpu_supports("avx2") || !__builtin_cpu_supports("fma")) return FT_ERR_DTYPE;
+    return FT_OK;
+}
+
+void run_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_pool, const void *x, int32_t T,
+                     const int32_t *topk_ids, const float *topk_w, const int32_t *experts, int32_t n_list,
+                     float *out, ft_cpu_pool_t *pool) {
+    using namespace ftmoe;
     CpuExpertArgs a{};
     a.E = desc->n_experts;
     a.H = desc->hidden;
@@ -322,7 +353,7 @@ ft_status_t ft_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_poo
     a.w_dtype = desc->w_dtype;
     a.x_dtype = desc->x_dtype;
     a.n_list = n_list;
-    a.n_threads = n_threads > 0 ? n_threads : std::max(1u, std::thread::hardware_concurrency());
+    a.pool = reinterpret_cast<CpuPool *>(pool);
     a.w13 = host_pool->w13;
     a.w2 = host_pool->w2;
     a.s13 = host_pool->s13;
@@ -333,6 +364,25 @@ ft_status_t ft_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_poo
     a.list = experts;
     a.out = out;
     cpu_experts(a);
+}
+
+}  // namespace
+
+extern "C" {
+
+ft_status_t ft_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_pool, const void *x,
+                           int32_t T, const int32_t *topk_ids, const float *topk_w,
+                           const int32_t *experts, int32_t n_list, float *out, ft_cpu_pool_t *pool) {
+    if (ft_status_t st = check_cpu_experts(desc, host_pool, T, n_list); st != FT_OK) return st;
+    if (T == 0) return FT_OK;
+    if (!x || !topk_ids || !topk_w || !out || (n_list > 0 && !experts)) return FT_ERR_NULL;
+    std::vector<char> seen(desc->n_experts, 0);
+    for (int i = 0; i < n_list; ++i) {
+        const int e = experts[i];
+        if (e < 0 || e >= desc->n_experts || seen[e]) return FT_ERR_SHAPE;
+        seen[e] = 1;
+    }
+    run_cpu_experts(desc, host_pool, x, T, topk_ids, topk_w, experts, n_list, out, pool);
     return FT_OK;
 }
 
@@ -376,61 +426,132 @@ ft_status_t ft_cache_fill(const ft_moe_desc_t *desc, const ft_banks_t *host_pool
     return launch_cache_fill(a, max_fill, static_cast<hipStream_t>(stream)) == hipSuccess ? FT_OK : FT_ERR_HIP;
 }
 
+}  // extern "C"
+
+namespace {
+
+// What the CPU branch of one hybrid step needs when its host function runs; written by the call
+// into the caller's ft_hybrid_task_t, read at every execution of the step (also graph replays).
+struct HybridTask {
+    ft_moe_desc_t desc;
+    ft_banks_t host_pool;
+    ft_hybrid_host_t host;
+    ft_cpu_pool_t *pool;
+    int32_t T;
+};
+static_assert(sizeof(HybridTask) <= sizeof(ft_hybrid_task_t), "ft_hybrid_task_t too small");
+
+// The step's CPU branch (on the pool's driver thread, or inline without a pool; makes no HIP
+// call).
+void hybrid_cpu_task(void *p) {
+    const HybridTask *t = static_cast<const HybridTask *>(p);
+    const int n_cpu = t->host.plan_counts[1];
+    if (n_cpu > 0)
+        run_cpu_experts(&t->desc, &t->host_pool, t->host.x, t->T, t->host.topk_ids, t->host.topk_w,
+                        t->host.cpu_expert, n_cpu, t->host.cpu_out, t->pool);
+    else
+        std::memset(t->host.cpu_out, 0, sizeof(float) * static_cast<size_t>(t->T) * t->desc.hidden);
+}
+
+}  // namespace
+
+extern "C" {
+
 ft_status_t ft_moe_step_hybrid(const ft_moe_desc_t *desc, const ft_banks_t *dev_banks,
                                const ft_banks_t *host_pool, const float *logits, int32_t *slot_table,
                                const ft_cache_state_t *state, const ft_cache_policy_t *policy,
-                               const void *x, int32_t T, float *out, float *cpu_out_dev,
+                               const void *x, int32_t T, float *out,
                                const ft_route_t *route, const ft_fill_plan_t *plan,
                                const ft_hybrid_host_t *host, void *ws, size_t ws_bytes,
-                               int32_t n_threads, void *stream) {
+                               ft_cpu_pool_t *pool, void *stream) {
     using namespace ftmoe;
     if (!desc || !dev_banks || !host_pool || !state || !policy || !route || !plan || !host)
         return FT_ERR_NULL;
     if (T == 0) return desc_ok(desc) ? FT_OK : FT_ERR_SHAPE;
-    if (!out || !cpu_out_dev || !x || !host->plan_counts || !host->cpu_expert || !host->topk_ids ||
-        !host->topk_w || !host->x || !host->cpu_out)
+    if (!out || !x || !host->plan_counts || !host->cpu_expert || !host->topk_ids || !host->topk_w ||
+        !host->x || !host->cpu_out || !host->task)
         return FT_ERR_NULL;
-    if (reinterpret_cast<uintptr_t>(cpu_out_dev) % 16) return FT_ERR_SHAPE;
+    if ((reinterpret_cast<uintptr_t>(host->x) | reinterpret_cast<uintptr_t>(host->cpu_out)) % 16)
+        return FT_ERR_SHAPE;
+    if (ft_status_t st = check_forward(desc, dev_banks, logits, slot_table, x, T, out, route, ws, ws_bytes);
+        st != FT_OK)
+        return st;
+    if (ft_status_t st = check_cpu_experts(desc, host_pool, T, desc->n_experts); st != FT_OK) return st;
+    // device-visible addresses of the pinned host staging (pageable memory is rejected)
+    void *dh[6] = {};
+    const void *hh[6] = {host->plan_counts, host->cpu_expert, host->topk_ids, host->topk_w, host->x,
+                         host->cpu_out};
+    for (int i = 0; i < 6; ++i)
+        if (hipHostGetDevicePointer(&dh[i], const_cast<void *>(hh[i]), 0) != hipSuccess || !dh[i])
+            return FT_ERR_SHAPE;
     const hipStream_t s = static_cast<hipStream_t>(stream);
-    // 1. routing and the cache plan on the current slot table
+    // 1. the step's only routing, then the cache plan, which rewrites the routed slot ids of the
+    //    experts it fills
     if (ft_status_t st = ft_route_only(desc, logits, slot_table, T, route, ws, ws_bytes, stream); st != FT_OK)
         return st;
     if (ft_status_t st = ft_cache_plan(desc, route, T, slot_table, state, policy, plan, stream); st != FT_OK)
         return st;
-    // 2. what the CPU branch needs goes to the host, at full fixed capacity
-    const size_t pk = static_cast<size_t>(T) * desc->top_k;
-    const size_t xb = static_cast<size_t>(T) * desc->hidden * (desc->x_dtype == FT_DT_F32 ? 4 : 2);
-    const hipMemcpyKind d2h = hipMemcpyDeviceToHost;
-    if (hipMemcpyAsync(host->plan_counts, plan->counts, 4 * sizeof(int32_t), d2h, s) != hipSuccess ||
-        hipMemcpyAsync(host->cpu_expert, plan->cpu_expert, desc->n_experts * sizeof(int32_t), d2h, s) != hipSuccess ||
-        hipMemcpyAsync(host->topk_ids, route->topk_ids, pk * sizeof(int32_t), d2h, s) != hipSuccess ||
-        hipMemcpyAsync(host->topk_w, route->topk_w, pk * sizeof(float), d2h, s) != hipSuccess ||
-        hipMemcpyAsync(host->x, x, xb, d2h, s) != hipSuccess)
-        return FT_ERR_HIP;
-    hipEvent_t staged;
-    if (hipEventCreateWithFlags(&staged, hipEventDisableTiming) != hipSuccess) return FT_ERR_HIP;
-    if (hipEventRecord(staged, s) != hipSuccess) {
-        (void)hipEventDestroy(staged);
+    // 2. the CPU branch: one kernel writes what it needs into the pinned host staging at full
+    //    fixed capacity, and a host function submits the experts the plan left to the CPU to the
+    //    pool, which evaluates them into host->cpu_out
+    HybridTask *task = reinterpret_cast<HybridTask *>(host->task);
+    task->desc = *desc;
+    task->host_pool = *host_pool;
+    task->host = *host;
+    task->pool = pool;
+    task->T = T;
+    StageArgs sa{};
+    sa.counts = plan->counts;
+    sa.cpu_expert = plan->cpu_expert;
+    sa.topk_ids = route->topk_ids;
+    sa.topk_w = route->topk_w;
+    sa.x = x;
+    sa.h_counts = static_cast<int32_t *>(dh[0]);
+    sa.h_cpu = static_cast<int32_t *>(dh[1]);
+    sa.h_ids = static_cast<int32_t *>(dh[2]);
+    sa.h_w = static_cast<float *>(dh[3]);
+    sa.h_x = dh[4];
+    sa.E = desc->n_experts;
+    sa.pk = static_cast<size_t>(T) * desc->top_k;
+    sa.x16 = static_cast<size_t>(T) * desc->hidden * (desc->x_dtype == FT_DT_F32 ? 4 : 2) / 16;
+    if (launch_stage_host(sa, s) != hipSuccess) return FT_ERR_HIP;
+    // with a pool the hand-off is the pool's mailbox in pinned memory (device kernels and a
+    // polling listener: no host function on the stream, so the fills and the GPU evaluation
+    // below overlap the CPU branch); without one a host function evaluates the branch in line
+    CpuPool *cp = reinterpret_cast<CpuPool *>(pool);
+    if (cp && !cp->mbox_dev) cp = nullptr;   // a pool without a mailbox: the host-function hand-off
+    if (cp) {
+        if (launch_mailbox_post(cp->mbox_dev, reinterpret_cast<uint64_t>(task), s) != hipSuccess)
+            return FT_ERR_HIP;
+    } else if (hipLaunchHostFunc(s, hybrid_cpu_task, task) != hipSuccess) {
         return FT_ERR_HIP;
     }
-    // 3. the GPU fills the planned slots and evaluates hits and fills (the second routing sees
-    //    the updated slot table), while the host runs the CPU branch
-    ft_status_t st = ft_cache_fill(desc, host_pool, dev_banks, plan, policy->max_fill, stream);
-    if (st == FT_OK)
-        st = ft_moe_forward(desc, dev_banks, logits, slot_table, x, T, out, route, ws, ws_bytes, stream);
-    if (hipEventSynchronize(staged) != hipSuccess) st = st == FT_OK ? FT_ERR_HIP : st;
-    (void)hipEventDestroy(staged);
-    if (st != FT_OK) return st;
-    const int n_cpu = host->plan_counts[1];
-    if (n_cpu <= 0) return FT_OK;
-    st = ft_cpu_experts(desc, host_pool, host->x, T, host->topk_ids, host->topk_w, host->cpu_expert,
-                        n_cpu, host->cpu_out, n_threads);
-    if (st != FT_OK) return st;
-    // 4. exact merge: out += CPU partial
-    const size_t n = static_cast<size_t>(T) * desc->hidden;
-    if (hipMemcpyAsync(cpu_out_dev, host->cpu_out, n * sizeof(float), hipMemcpyHostToDevice, s) != hipSuccess)
-        return FT_ERR_HIP;
-    return launch_add_partial(out, cpu_out_dev, n, s) == hipSuccess ? FT_OK : FT_ERR_HIP;
+    // 3. meanwhile the GPU fills the planned slots and evaluates G = H u F from the plan's slot
+    //    ids (no second routing)
+    if (ft_status_t st = ft_cache_fill(desc, host_pool, dev_banks, plan, policy->max_fill, stream); st != FT_OK)
+        return st;
+    const WsView wv = carve(desc, T, ws);
+    RegroupArgs rg{};
+    rg.E = desc->n_experts;
+    rg.T = T;
+    rg.k = desc->top_k;
+    rg.shared_slot = desc->shared_slot;
+    rg.hit_off = route->hit_off;
+    rg.miss_off = route->miss_off;
+    rg.hit_pairs = route->hit_pairs;
+    rg.miss_pairs = route->miss_pairs;
+    rg.topk_slot = route->topk_slot;
+    rg.topk_w = route->topk_w;
+    rg.wv = wv;
+    if (launch_regroup(rg, s) != hipSuccess) return FT_ERR_HIP;
+    if (enqueue_experts(desc, dev_banks, x, T, out, route, wv, s, Prof(nullptr, s)) != hipSuccess) return FT_ERR_HIP;
+    // 4. exact merge once the CPU branch is done: out += CPU partial, read from pinned host
+    //    memory over PCIe
+    if (cp && launch_mailbox_wait(cp->mbox_dev, s) != hipSuccess) return FT_ERR_HIP;
+    return launch_add_partial(out, static_cast<const float *>(dh[5]), static_cast<size_t>(T) * desc->hidden, s) ==
+                   hipSuccess
+               ? FT_OK
+               : FT_ERR_HIP;
 }
 
 ft_status_t ft_miss_list_to_host(const ft_moe_desc_t *desc, const ft_route_t *route, int32_t T,

@@ -42,6 +42,9 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
 
     // ---- 1
     const int status = a.route_counts[3], m = a.route_counts[2];
+    // the step's stamp: from the device clock when there is one (a captured step replays with
+    // the same arguments), else from the call
+    const uint32_t step = a.clock ? a.clock[0] + 1u : a.step;
     // this thread's expert e = tid: its missed pairs [mo0, mo1), whether it hit, its slot
     const int e_me = tid;
     const bool has_e = e_me < E;
@@ -89,6 +92,7 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
 
     // ---- 4
     if (tid == 0) {
+        if (a.clock) a.clock[0] = step;   // every thread read the clock before the first barrier
         int q = 0;
         if (status == 0 && m > 0) {
             q = a.b_host <= a.b_pcie ? m : static_cast<int>(floor(m * (a.b_pcie / a.b_host) + 0.5));
@@ -115,7 +119,7 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
             if (old >= 0) a.slot_table[old] = -1;
             a.slot_table[e] = v;
             a.slot_expert[v] = e;
-            a.slot_stamp[v] = a.step;
+            a.slot_stamp[v] = step;
             for (int j = mo0; j < mo1; ++j) a.topk_slot[a.miss_pairs[j]] = v;
         } else {
             // position among the missing experts left to the CPU, in id order
@@ -124,7 +128,7 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
             a.cpu_expert[pos] = e;
         }
     }
-    if (status == 0 && hit) a.slot_stamp[slot_me] = a.step;   // hits keep their slot
+    if (status == 0 && hit) a.slot_stamp[slot_me] = step;   // hits keep their slot
     for (int i = q + tid; i < K; i += kPlanThreads) {
         a.fill_expert[i] = -1;
         a.fill_slot[i] = -1;

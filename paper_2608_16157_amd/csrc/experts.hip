@@ -1,12 +1,15 @@
 // Grouped SwiGLU expert evaluation over slot-resident weights (Section 3.2: grouped evaluation
 // of the GPU execution set; Section 4.2: every bank row is one slot, so a group's weights are
-// addressed as bank + slot * expert_stride with no relayout), with the gate-weighted combine
-// fused into the down projection.
+// addressed as bank + slot * expert_stride with no relayout), and the gate-weighted combine.
 //
 // Streaming (GEMV-like) path, any token count and any weight dtype:
 //   grouped_gemv<GATEUP>: h[r] = silu(W1 x_tok(r)) * (W3 x_tok(r))       per group, 8 h-columns/WG
-//                         (also zeroes out_partial)
-//   grouped_gemv<DOWN>  : out[tok(r)] += gate(r) * W2 h[r]               per group, 16 columns/WG
+//   grouped_gemv<DOWN>  : y[pair(r)] = gate(r) * W2 h[r]                 per group, 16 columns/WG
+//   combine             : out[t] = sum_j y[t k + j] over the pairs evaluated on the GPU, in
+//                         j order, then the shared expert's row: every output element is summed
+//                         in one fixed order, so the layer output is bit-reproducible
+// With the atomic combine the down projection adds gate(r) * W2 h[r] into out[tok(r)] with
+// float32 atomics instead (the gate/up kernel zeroes out first): one launch less.
 // The weights stream from HBM once per (group, column tile).  Tokens of a group are the MFMA M
 // dimension (16-row tiles), weight rows the N dimension; the contraction (hidden or intermediate
 // dimension) is split over the 4 waves of a workgroup in contiguous runs of 128-wide blocks (the
@@ -206,8 +209,8 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
     // until the barrier, while other waves may still be streaming into theirs.
     __shared__ __attribute__((aligned(1024))) uint8_t s_lds[kGemvWaves * PW];
     auto s_red = [&](int w) { return reinterpret_cast<float (*)[COLS + 1]>(s_lds + w * PW); };
-    if constexpr (EPI == EPI_GATEUP) {
-        // zero the output that the down projection accumulates into
+    if (EPI == EPI_GATEUP && !a.wv.ypart) {
+        // atomic combine: zero the output the down projection adds into
         const size_t n4 = static_cast<size_t>(a.T) * a.H / 4;
         float4 *o4 = reinterpret_cast<float4 *>(a.out);
         for (size_t i = static_cast<size_t>(blockIdx.x) * kGemvThreads + threadIdx.x; i < n4;
@@ -395,7 +398,7 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
                     }
                 }
             } else {
-                // gate-weighted scatter-add of 16 rows x NB*16 output columns
+                // gate-weighted outputs of 16 rows x NB*16 columns, stored by pair index
                 for (int idx = threadIdx.x; idx < 16 * COLS; idx += kGemvThreads) {
                     const int m = idx / COLS, c = idx % COLS;
                     const int r = rt + m;
@@ -403,9 +406,14 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
                         float sum = 0.f;
 #pragma unroll
                         for (int w = 0; w < kGemvWaves; ++w) sum += s_red(w)[m][c];
-                        const int tok = a.wv.row_tok[beg + r];
-                        unsafeAtomicAdd(a.out + static_cast<size_t>(tok) * H + tile * COLS + c,
-                                        a.wv.row_gate[beg + r] * sum);
+                        const float y = a.wv.row_gate[beg + r] * sum;
+                        if (a.wv.ypart) {
+                            const int p = a.wv.row_pair[beg + r];
+                            a.wv.ypart[static_cast<size_t>(p) * H + tile * COLS + c] = y;
+                        } else {
+                            const int tok = a.wv.row_tok[beg + r];
+                            unsafeAtomicAdd(a.out + static_cast<size_t>(tok) * H + tile * COLS + c, y);
+                        }
                     }
                 }
             }
@@ -419,6 +427,38 @@ __global__ __launch_bounds__(256) void zero_out(float *out, size_t n4) {
     for (size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; i < n4;
          i += static_cast<size_t>(gridDim.x) * 256)
         o4[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// out[t] = sum over j of y[t k + j] for the pairs evaluated on the GPU (routed slot >= 0), in
+// ascending j, then + y[T k + t] for the shared expert; tokens without any are exactly 0.
+__global__ __launch_bounds__(256) void combine_kernel(float *out, const float *y, const int32_t *topk_slot,
+                                                      int T, int k, int H, int shared) {
+    const int h4 = H / 4;
+    const size_t n4 = static_cast<size_t>(T) * h4;
+    const float4 *y4 = reinterpret_cast<const float4 *>(y);
+    for (size_t i = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x; i < n4;
+         i += static_cast<size_t>(gridDim.x) * 256) {
+        const int t = static_cast<int>(i / h4), c = static_cast<int>(i % h4);
+        float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int j = 0; j < k; ++j) {
+            const int p = t * k + j;
+            if (topk_slot[p] >= 0) {
+                const float4 v = y4[static_cast<size_t>(p) * h4 + c];
+                acc.x += v.x;
+                acc.y += v.y;
+                acc.z += v.z;
+                acc.w += v.w;
+            }
+        }
+        if (shared) {
+            const float4 v = y4[(static_cast<size_t>(T) * k + t) * h4 + c];
+            acc.x += v.x;
+            acc.y += v.y;
+            acc.z += v.z;
+            acc.w += v.w;
+        }
+        reinterpret_cast<float4 *>(out)[i] = acc;
+    }
 }
 
 template <int WT, int EPI>
@@ -467,27 +507,25 @@ static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
 
 template <int WT>
 static hipError_t launch_stream_path(const ExpertArgs &a, hipStream_t s, const Prof &prof) {
+    // the combine is a kernel of its own: folding it into the down kernel's last workgroup per
+    // column tile needed a device-scope fence in every workgroup, whose L2 writeback on this
+    // multi-XCD part cost far more than the launch (measured: Qwen3 T = 32 down 26 -> 395 us)
+    const size_t n4 = static_cast<size_t>(a.T) * a.H / 4;
+    const unsigned blocks = static_cast<unsigned>(std::min<size_t>(2048, (n4 + 255) / 256));
     if (!prof.mark(1)) return hipErrorUnknown;
-    if (a.max_groups > 0) {
-        launch_gemv<WT, EPI_GATEUP>(a, s);
-    } else {
-        const size_t n4 = static_cast<size_t>(a.T) * a.H / 4;
-        hipLaunchKernelGGL(zero_out, dim3(static_cast<unsigned>(std::min<size_t>(4096, (n4 + 255) / 256))),
-                           dim3(256), 0, s, a.out, n4);
-    }
+    if (a.max_groups > 0) launch_gemv<WT, EPI_GATEUP>(a, s);
+    else if (!a.wv.ypart) hipLaunchKernelGGL(zero_out, dim3(blocks), dim3(256), 0, s, a.out, n4);
     if (!prof.mark(2)) return hipErrorUnknown;
     if (a.max_groups > 0) launch_gemv<WT, EPI_DOWN>(a, s);
     if (!prof.mark(3)) return hipErrorUnknown;
+    if (a.wv.ypart)
+        hipLaunchKernelGGL(combine_kernel, dim3(blocks), dim3(256), 0, s, a.out, a.wv.ypart, a.ro.topk_slot, a.T,
+                           a.k, a.H, a.shared);
     return hipGetLastError();
 }
 
 // Many-token chunks whose shapes tile evenly go to the MFMA GEMM.
-static bool gemm_path(const ExpertArgs &a) {
-    // the MXFP4 scale DMA of the GEMM is laid out for 256-row weight tiles
-    if (a.w_dtype == FT_DT_MXFP4 && kGemmBN != 256) return false;
-    return a.T >= kGemmMinTokens && a.max_groups > 0 && a.H % kGemmBN == 0 && a.I % (kGemmBN / 2) == 0 &&
-           a.H <= 8192 && a.I <= 8192;
-}
+static bool gemm_path(const ExpertArgs &a) { return a.max_groups > 0 && gemm_shape(a.T, a.H, a.I, a.w_dtype); }
 
 hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof) {
     switch (a.w_dtype) {

@@ -11,7 +11,11 @@
 // A slot row is a complete expert, so a fill is a plain row copy, never a relayout (Section 4.2).
 //
 // add_partial_kernel: out += other, the exact additive merge of the GPU and CPU partial sums
-// (Section 3.2).
+// (Section 3.2); `other` may be pinned host memory read over PCIe.
+//
+// stage_host_kernel: what the CPU branch of a hybrid step needs (plan counts, CPU expert list,
+// routing, hidden states) written straight into pinned host staging over PCIe by one kernel,
+// instead of one copy-engine command per buffer.
 #include <algorithm>
 
 #include "ftmoe_device.h"
@@ -77,6 +81,62 @@ __global__ __launch_bounds__(256) void add_partial_kernel(float *out, const floa
         x.w += y.w;
         o[i] = x;
     }
+}
+
+__global__ __launch_bounds__(256) void stage_host_kernel(StageArgs a) {
+    const size_t tid = static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x;
+    const size_t nth = static_cast<size_t>(gridDim.x) * 256;
+    if (tid < 4) a.h_counts[tid] = a.counts[tid];
+    for (size_t i = tid; i < static_cast<size_t>(a.E); i += nth) a.h_cpu[i] = a.cpu_expert[i];
+    for (size_t i = tid; i < static_cast<size_t>(a.pk); i += nth) {
+        a.h_ids[i] = a.topk_ids[i];
+        a.h_w[i] = a.topk_w[i];
+    }
+    const u32x4_t *xs = reinterpret_cast<const u32x4_t *>(a.x);
+    u32x4_t *xd = reinterpret_cast<u32x4_t *>(a.h_x);
+    for (size_t i = tid; i < a.x16; i += nth) xd[i] = xs[i];
+    __threadfence_system();
+}
+
+// Post: the step's task address, then the next sequence number (after the staging kernel, whose
+// host writes are complete and fenced at system scope before this kernel starts).
+__global__ void mailbox_post_kernel(HostMailbox *mb, uint64_t task) {
+    if (threadIdx.x != 0) return;
+    const uint64_t seq = __hip_atomic_load(&mb->posted, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM) + 1;
+    __hip_atomic_store(&mb->task, task, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(&mb->posted, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// Wait until the pool reports the last posted number as done.  Bounded: after 2^24 polls (tens
+// of seconds) without an answer (the listener gone) it counts a timeout in the mailbox and
+// returns, so the stream never hangs; the step's output is then incomplete.
+constexpr uint64_t kMailboxSpins = 1ull << 24;
+__global__ void mailbox_wait_kernel(HostMailbox *mb) {
+    if (threadIdx.x != 0) return;
+    const uint64_t seq = __hip_atomic_load(&mb->posted, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM);
+    for (uint64_t i = 0; i < kMailboxSpins; ++i) {
+        if (__hip_atomic_load(&mb->done, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_SYSTEM) == seq) return;
+        __builtin_amdgcn_s_sleep(8);
+    }
+    const uint64_t n = __hip_atomic_load(&mb->timeouts, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    __hip_atomic_store(&mb->timeouts, n + 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+hipError_t launch_mailbox_post(HostMailbox *mbox_dev, uint64_t task, hipStream_t s) {
+    hipLaunchKernelGGL(mailbox_post_kernel, dim3(1), dim3(64), 0, s, mbox_dev, task);
+    return hipGetLastError();
+}
+
+hipError_t launch_mailbox_wait(HostMailbox *mbox_dev, hipStream_t s) {
+    hipLaunchKernelGGL(mailbox_wait_kernel, dim3(1), dim3(64), 0, s, mbox_dev);
+    return hipGetLastError();
+}
+
+hipError_t launch_stage_host(const StageArgs &a, hipStream_t s) {
+    const size_t work = std::max<size_t>(a.x16, std::max<size_t>(a.pk, a.E));
+    const unsigned blocks = static_cast<unsigned>(std::min<size_t>(256, (work + 255) / 256));
+    hipLaunchKernelGGL(stage_host_kernel, dim3(blocks ? blocks : 1), dim3(256), 0, s, a);
+    return hipGetLastError();
 }
 
 hipError_t launch_cache_fill(const FillArgs &a, int max_fill, hipStream_t s) {

@@ -5,6 +5,13 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <atomic>
+#include <condition_variable>
+#include <functional>
+#include <mutex>
+#include <thread>
+#include <vector>
+
 #include "ftmoe.h"
 
 namespace ftmoe {
@@ -26,6 +33,8 @@ constexpr int kGemmBN = FT_GEMM_BN;     // weight rows per MFMA GEMM tile
 #define FT_GEMM_MIN_TOKENS 256
 #endif
 constexpr int kGemmMinTokens = FT_GEMM_MIN_TOKENS;   // token count from which the MFMA GEMM path is used
+
+struct HostMailbox;   // a worker pool's device <-> host mailbox (defined with CpuPool)
 
 // Routing outputs (the caller's ft_route_t, flattened).
 struct RouteOut {
@@ -55,7 +64,10 @@ struct WsView {
     int32_t *mt_group;   // [max M tiles] group of each GEMM M tile
     int32_t *row_tok;    // [T*k + T]
     float *row_gate;     // [T*k + T]
+    int32_t *row_pair;   // [T*k + T] pair index p = t*k + j of the row (T*k + t for the shared rows)
     void *h;             // [T*k + T][I] SwiGLU activations (bf16, or f32 for f32 weights)
+    float *ypart;        // streaming path: [T*k + T][H] gate-weighted expert outputs by pair
+                         // index, summed per token in a fixed order by the combine (else null)
 };
 
 struct RouteArgs {
@@ -81,8 +93,16 @@ struct ExpertArgs {
 
 struct WsLayout {
     size_t eff_slot, blk_hist, grp_meta, grp_slot, grp_beg, grp_len, grp_mt_off, mt_group, row_tok,
-        row_gate, h, total;
+        row_gate, row_pair, h, ypart, ypart_bytes, total;
 };
+
+// Whether a call of T tokens runs the matrix-core GEMM path (many tokens, shapes that tile);
+// the launcher additionally needs at least one evaluation group.
+inline bool gemm_shape(int T, int H, int I, int w_dtype) {
+    if (w_dtype == FT_DT_F32) return false;
+    if (w_dtype == FT_DT_MXFP4 && kGemmBN != 256) return false;   // its scale DMA assumes 256-row tiles
+    return T >= kGemmMinTokens && H % kGemmBN == 0 && I % (kGemmBN / 2) == 0 && H <= 8192 && I <= 8192;
+}
 
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -93,7 +113,7 @@ inline size_t gemm_max_mtiles(int T, int k, int E) {
     return (rows + kGemmBM - 1) / kGemmBM + E + 1;
 }
 
-inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int T) {
+inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int combine, int T) {
     WsLayout L{};
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -113,7 +133,11 @@ inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int T) {
     L.mt_group = take(4u * gemm_max_mtiles(T, k, E));
     L.row_tok = take(4u * rows);
     L.row_gate = take(4u * rows);
+    L.row_pair = take(4u * rows);
     L.h = take(rows * I * (w_dtype == FT_DT_F32 ? 4u : 2u));
+    L.ypart_bytes = (gemm_shape(T, H, I, w_dtype) || combine != FT_COMBINE_ORDERED) ? 0 : rows * H * 4u;
+    L.ypart = take(L.ypart_bytes);
+
     L.total = o;
     return L;
 }
@@ -138,6 +162,7 @@ struct PlanArgs {
     int E, k, n_slots, shared_slot, K;
     double b_pcie, b_host;
     uint32_t step;
+    uint32_t *clock;   // device step counter, or null (then `step` is the stamp)
     const int32_t *hit_off, *miss_off, *miss_pairs, *route_counts;
     int32_t *topk_slot;
     int32_t *slot_table, *slot_expert;
@@ -156,6 +181,21 @@ struct FillArgs {
 };
 hipError_t launch_cache_fill(const FillArgs &a, int max_fill, hipStream_t s);
 hipError_t launch_add_partial(float *out, const float *other, size_t n, hipStream_t s);
+// Host staging of a hybrid step (device-visible addresses of pinned host buffers).
+struct StageArgs {
+    const int32_t *counts, *cpu_expert, *topk_ids;
+    const float *topk_w;
+    const void *x;
+    int32_t *h_counts, *h_cpu, *h_ids;
+    float *h_w;
+    void *h_x;
+    int E;
+    size_t pk, x16;   // routed pairs; 16-byte chunks of x (x rows are 16-byte multiples)
+};
+hipError_t launch_stage_host(const StageArgs &a, hipStream_t s);
+// Post a task to a pool's mailbox (device side), and wait until the pool reports it done.
+hipError_t launch_mailbox_post(HostMailbox *mbox_dev, uint64_t task, hipStream_t s);
+hipError_t launch_mailbox_wait(HostMailbox *mbox_dev, hipStream_t s);
 
 // Bytes of one expert in each bank (w13, w2, s13, s2) for a weight dtype; H, I multiples of 128.
 struct ExpertBytes {
@@ -176,13 +216,52 @@ ft_status_t check_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, co
                           const int32_t *slot_table, const void *x, int32_t T, const float *out_partial,
                           const ft_route_t *route, const void *ws, size_t ws_bytes);
 
+// Mailbox of a worker pool in pinned host memory, written by the device and the pool's listener
+// thread: the device posts a step (task pointer, then a new sequence number), the listener runs
+// the task and echoes the number into `done`, which a device kernel waits for.
+struct alignas(64) HostMailbox {
+    uint64_t posted;     // last posted sequence number (device writes)
+    uint64_t task;       // host address of the posted step's task (device writes)
+    uint64_t done;       // last finished sequence number (listener writes)
+    uint64_t timeouts;   // device waits that gave up (device writes)
+};
+
+// The CPU branch's persistent worker pool (host_experts.cpp), behind the opaque ft_cpu_pool_t.
+struct CpuPool {
+    struct Job {
+        int n;
+        const std::function<void(int, std::vector<float> &)> &fn;
+    };
+    std::vector<std::thread> workers;
+    std::vector<int> cpus;        // CPU each worker is pinned to, -1 if not pinned
+    std::mutex mu, run_mu;
+    std::condition_variable cv_work, cv_done;
+    const Job *current = nullptr;
+    uint64_t gen = 0;             // job generation
+    std::atomic<int> next{0};     // next work item of the current job
+    int busy = 0;                 // workers not yet done with the current job
+    bool stop = false;
+    // the listener thread polls the mailbox and runs each posted task (through run())
+    std::thread listener;
+    std::atomic<bool> quit{false};
+    HostMailbox *mbox = nullptr;       // pinned host memory
+    HostMailbox *mbox_dev = nullptr;   // its device-visible address
+    void (*task_fn)(void *) = nullptr; // what a posted task runs
+    static CpuPool *create(int n_threads, bool pin, void (*task_fn)(void *));
+    ~CpuPool();
+    void run(int n_items, const std::function<void(int, std::vector<float> &)> &fn);
+    void worker_loop();
+    void listen_loop();
+};
+
 // CPU branch of a layer step (host_experts.cpp).
 struct CpuBank {
     const void *w;       // one expert's matrix, row-major
     const void *s;       // its fp8 block scales (float32) or MXFP4 scales (uint8), or null
 };
 struct CpuExpertArgs {
-    int E, H, I, k, T, w_dtype, x_dtype, n_list, n_threads;
+    int E, H, I, k, T, w_dtype, x_dtype, n_list;
+    CpuPool *pool;                   // workers, or null: the calling thread alone
     const void *w13, *w2;            // host expert pool, [E][2I][H] and [E][H][I]
     const void *s13, *s2;            // fp8 / MXFP4 scales per expert, or null
     const void *x;                   // [T][H]
@@ -192,6 +271,15 @@ struct CpuExpertArgs {
     float *out;                      // [T][H], overwritten
 };
 void cpu_experts(const CpuExpertArgs &a);
+
+// Evaluation groups of a hybrid step from its routing after the cache plan (route.hip).
+struct RegroupArgs {
+    int E, T, k, shared_slot;
+    const int32_t *hit_off, *miss_off, *hit_pairs, *miss_pairs, *topk_slot;
+    const float *topk_w;
+    WsView wv;
+};
+hipError_t launch_regroup(const RegroupArgs &a, hipStream_t s);
 
 hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_cache_plan(const PlanArgs &a, hipStream_t s);

@@ -111,6 +111,8 @@ template <> struct GTr<FT_DT_MXFP4> {
 
 template <int V> using ic = std::integral_constant<int, V>;
 
+constexpr int gcd_c(int a, int b) { return b == 0 ? a : gcd_c(b, a % b); }
+
 // Calls f(ic<S>) for S = B .. E-1.
 template <int B, int E, class F>
 __device__ __forceinline__ void static_for(F &&f) {
@@ -186,7 +188,9 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     static_assert(NS >= 2 && NS <= 4, "ring depth");
     static_assert(NS * PER_STAGE < 64, "vmcnt range");
     static_assert(!kFp8 || 128 % BK == 0, "an fp8 K stage lies in one scale block");
-    static_assert(!kFp8 || (NS * BK) % 128 == 0, "fp8: a ring turn spans whole scale blocks");
+    // stages unrolled per main-loop turn: whole ring turns and, for fp8, whole 128-wide K blocks
+    constexpr int kStagesPerKb = kFp8 ? 128 / BK : 1;
+    constexpr int kUnit = NS / gcd_c(NS, kStagesPerKb) * kStagesPerKb;   // lcm
     // one array per stage (see the header comment); unused ones shrink to 16 bytes
     __shared__ __attribute__((aligned(1024))) uint8_t sA0[ASTAGE], sA1[ASTAGE];
     __shared__ __attribute__((aligned(1024))) uint8_t sA2[NS > 2 ? ASTAGE : 16];
@@ -514,11 +518,13 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     };
     auto mainloop = [&](auto ml, auto zs) {
         Frag cur, nxt;
-        // stage kt, in ring slot S (= kt mod NS); fp8 K blocks open at the stages with
-        // S * BK = 0 mod 128 (the ring turn NS * BK is a multiple of 128)
-        auto stage = [&](auto s, int kt) {
-            constexpr int S = decltype(s)::value;
-            constexpr bool kOpens = kFp8 && (S * BK) % 128 == 0;
+        // stage kt, the I-th stage of an unrolled unit of U stages (U a multiple of the ring depth
+        // and, for fp8, of the stages per 128-wide K block), in ring slot S = I mod NS; fp8 K
+        // blocks open at the stages with I * BK = 0 mod 128
+        auto stage = [&](auto i, int kt) {
+            constexpr int I = decltype(i)::value, S = I % NS;
+            constexpr bool kOpens = kFp8 && (I * BK) % 128 == 0;
+            const auto s = ic<S>{};
             static_for<0, KS>([&](auto ks) {
                 constexpr int KSI = decltype(ks)::value;
                 if constexpr (KSI + 1 == KS) {
@@ -545,10 +551,10 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         // whole turns of the ring without branches (a branch around a stage would make the
         // compiler lose track of which slot each DMA writes, and drain them all), then the rest
         int kt0 = 0;
-        for (; kt0 + NS <= nk; kt0 += NS)
-            static_for<0, NS>([&](auto s) { stage(s, kt0 + decltype(s)::value); });
-        static_for<0, NS - 1>([&](auto s) {
-            if (kt0 + decltype(s)::value < nk) stage(s, kt0 + decltype(s)::value);
+        for (; kt0 + kUnit <= nk; kt0 += kUnit)
+            static_for<0, kUnit>([&](auto i) { stage(i, kt0 + decltype(i)::value); });
+        static_for<0, kUnit - 1>([&](auto i) {
+            if (kt0 + decltype(i)::value < nk) stage(i, kt0 + decltype(i)::value);
         });
     };
 

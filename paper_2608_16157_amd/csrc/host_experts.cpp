@@ -5,8 +5,9 @@
 // Section 4.1: the CPU workers are a native thread pool with SIMD kernels and in-kernel
 // dequantisation, so the branch stays bandwidth-bound).
 //
-// Two phases over the listed experts, each split into independent work items that threads take
-// from a shared counter:
+// Two phases over the listed experts, each split into independent work items that the threads of
+// a persistent worker pool (created once, optionally pinned one per physical core) take from a
+// shared counter:
 //   gate/up: items of 32 intermediate rows of one expert: h = silu(W1 x) * (W3 x) for the
 //            expert's tokens (every weight row is decoded to float once and used for all of them);
 //   down   : items of 32 output columns: out[t][c] += gate * (W2[c] . h), experts in list order,
@@ -15,10 +16,20 @@
 // Weights are decoded exactly (bf16 by widening, fp8 e4m3fn and MXFP4 e2m1 from the format
 // definitions times their scales) and every product accumulates in float32.  All code in this file is
 // compiled for AVX2 + FMA; the entry point checks the CPU supports them before calling in.
+#include <pthread.h>
+#include <sched.h>
+
 #include <atomic>
+#include <chrono>
 #include <cmath>
+#include <condition_variable>
+#include <cstdio>
 #include <cstring>
+#include <functional>
+#include <mutex>
+#include <set>
 #include <thread>
+#include <utility>
 #include <vector>
 
 #include "ftmoe_internal.h"
@@ -115,19 +126,158 @@ float dot(const float *a, const float *b, int n) {
     return ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
 }
 
+}  // namespace
+
+#pragma clang attribute pop
+
+// ---- the worker pool (plain x86-64 code: created and driven without the AVX2 check)
+
+CpuPool::~CpuPool() {
+    quit.store(true);
+    if (listener.joinable()) listener.join();
+    {
+        std::lock_guard<std::mutex> lk(mu);
+        stop = true;
+    }
+    cv_work.notify_all();
+    for (auto &t : workers) t.join();
+    if (mbox) (void)hipHostFree(mbox);
+}
+
+// Polls the mailbox: a new posted number means the device has staged a step's inputs in host
+// memory; run its task, then report the number as done.  Spins with a pause while work arrives,
+// and backs off to short sleeps after a millisecond without any.
+void CpuPool::listen_loop() {
+    uint64_t seen = __atomic_load_n(&mbox->posted, __ATOMIC_ACQUIRE);
+    auto idle_since = std::chrono::steady_clock::now();
+    while (!quit.load(std::memory_order_relaxed)) {
+        const uint64_t v = __atomic_load_n(&mbox->posted, __ATOMIC_ACQUIRE);
+        if (v != seen) {
+            void *task = reinterpret_cast<void *>(__atomic_load_n(&mbox->task, __ATOMIC_ACQUIRE));
+            if (task) task_fn(task);
+            seen = v;
+            __atomic_store_n(&mbox->done, v, __ATOMIC_RELEASE);
+            idle_since = std::chrono::steady_clock::now();
+            continue;
+        }
+        if (std::chrono::steady_clock::now() - idle_since < std::chrono::milliseconds(1))
+            __builtin_ia32_pause();
+        else
+            std::this_thread::sleep_for(std::chrono::microseconds(20));
+    }
+}
+
+void CpuPool::worker_loop() {
+    std::vector<float> scratch;
+    uint64_t seen = 0;
+    for (;;) {
+        std::unique_lock<std::mutex> lk(mu);
+        cv_work.wait(lk, [&] { return stop || gen != seen; });
+        if (stop) return;
+        seen = gen;
+        const Job *job = current;
+        lk.unlock();
+        for (int it = next.fetch_add(1); it < job->n; it = next.fetch_add(1)) job->fn(it, scratch);
+        lk.lock();
+        if (--busy == 0) cv_done.notify_all();
+    }
+}
+
+void CpuPool::run(int n_items, const std::function<void(int, std::vector<float> &)> &fn) {
+    if (n_items <= 0) return;
+    std::lock_guard<std::mutex> one(run_mu);   // one job at a time
+    Job job{n_items, fn};
+    std::unique_lock<std::mutex> lk(mu);
+    current = &job;
+    next.store(0);
+    busy = static_cast<int>(workers.size());
+    ++gen;
+    cv_work.notify_all();
+    cv_done.wait(lk, [&] { return busy == 0; });
+    current = nullptr;
+}
+
+// The CPUs of this process's affinity mask, one hardware thread of every physical core first
+// (the first seen of each (package, core) pair, in CPU order), then the other hardware threads.
+static std::vector<int> physical_cores() {
+    cpu_set_t set;
+    CPU_ZERO(&set);
+    std::vector<int> out;
+    if (sched_getaffinity(0, sizeof(set), &set) != 0) return out;
+    std::set<std::pair<int, int>> seen;
+    std::vector<int> rest;
+    for (int c = 0; c < CPU_SETSIZE; ++c) {
+        if (!CPU_ISSET(c, &set)) continue;
+        int pkg = 0, core = c;
+        char path[128];
+        std::snprintf(path, sizeof(path), "/sys/devices/system/cpu/cpu%d/topology/core_id", c);
+        if (FILE *f = std::fopen(path, "r")) {
+            if (std::fscanf(f, "%d", &core) != 1) core = c;
+            std::fclose(f);
+        }
+        std::snprintf(path, sizeof(path), "/sys/devices/system/cpu/cpu%d/topology/physical_package_id", c);
+        if (FILE *f = std::fopen(path, "r")) {
+            if (std::fscanf(f, "%d", &pkg) != 1) pkg = 0;
+            std::fclose(f);
+        }
+        (seen.insert({pkg, core}).second ? out : rest).push_back(c);
+    }
+    out.insert(out.end(), rest.begin(), rest.end());
+    return out;
+}
+
+CpuPool *CpuPool::create(int n_threads, bool pin, void (*task_fn)(void *)) {
+    const std::vector<int> cores = physical_cores();
+    if (n_threads <= 0) n_threads = cores.empty() ? 1 : static_cast<int>(cores.size());
+    CpuPool *p = new (std::nothrow) CpuPool();
+    if (!p) return nullptr;
+    p->task_fn = task_fn;
+    // the mailbox needs pinned host memory the device can reach; without a device the pool
+    // still serves ft_cpu_experts (and hybrid steps hand it over with a host function)
+    void *mb = nullptr, *mbd = nullptr;
+    if (hipHostMalloc(&mb, sizeof(HostMailbox), hipHostMallocDefault) == hipSuccess && mb) {
+        p->mbox = static_cast<HostMailbox *>(mb);
+        std::memset(p->mbox, 0, sizeof(HostMailbox));
+        if (hipHostGetDevicePointer(&mbd, mb, 0) == hipSuccess && mbd)
+            p->mbox_dev = static_cast<HostMailbox *>(mbd);
+    } else {
+        (void)hipGetLastError();   // leave no sticky error for the caller's next HIP call
+    }
+    try {
+        if (p->mbox_dev) p->listener = std::thread([p] { p->listen_loop(); });
+        for (int i = 0; i < n_threads; ++i) {
+            p->workers.emplace_back([p] { p->worker_loop(); });
+            if (pin && !cores.empty()) {
+                cpu_set_t one;
+                CPU_ZERO(&one);
+                CPU_SET(cores[i % cores.size()], &one);
+                (void)pthread_setaffinity_np(p->workers.back().native_handle(), sizeof(one), &one);
+                p->cpus.push_back(cores[i % cores.size()]);
+            } else {
+                p->cpus.push_back(-1);
+            }
+        }
+    } catch (...) {
+        delete p;
+        return nullptr;
+    }
+    return p;
+}
+
+#pragma clang attribute push(__attribute__((target("avx2,fma"))), apply_to = function)
+
+namespace {
+
+// Runs fn(item, scratch) for every item, on the pool's workers (the caller waits) or, without a
+// pool, on the calling thread.
 template <class F>
-void run_items(int n_items, int n_threads, F &&fn) {
-    std::atomic<int> next{0};
-    auto worker = [&]() {
+void run_items(CpuPool *pool, int n_items, F &&fn) {
+    if (!pool || pool->workers.empty()) {
         std::vector<float> scratch;
-        for (int it = next.fetch_add(1); it < n_items; it = next.fetch_add(1)) fn(it, scratch);
-    };
-    const int nt = std::max(1, std::min(n_threads, n_items));
-    std::vector<std::thread> pool;
-    pool.reserve(nt - 1);
-    for (int i = 1; i < nt; ++i) pool.emplace_back(worker);
-    worker();
-    for (auto &t : pool) t.join();
+        for (int it = 0; it < n_items; ++it) fn(it, scratch);
+        return;
+    }
+    pool->run(n_items, std::function<void(int, std::vector<float> &)>(fn));
 }
 
 }  // namespace
@@ -176,7 +326,7 @@ void cpu_experts(const CpuExpertArgs &a) {
     for (int i = 0; i < a.n_list; ++i)
         if (!toks[i].empty())
             for (int b = 0; b < blocks_i; ++b) gu_items.push_back(i * blocks_i + b);
-    run_items(static_cast<int>(gu_items.size()), a.n_threads, [&](int it, std::vector<float> &scr) {
+    run_items(a.pool, static_cast<int>(gu_items.size()), [&](int it, std::vector<float> &scr) {
         const int li = gu_items[it] / blocks_i, b = gu_items[it] % blocks_i;
         const int e = a.list[li];
         const CpuBank bk = bank13(e);
@@ -195,7 +345,7 @@ void cpu_experts(const CpuExpertArgs &a) {
 
     // ---- down + gate-weighted combine
     const int blocks_c = (H + kRowsPerItem - 1) / kRowsPerItem;
-    run_items(blocks_c, a.n_threads, [&](int b, std::vector<float> &scr) {
+    run_items(a.pool, blocks_c, [&](int b, std::vector<float> &scr) {
         scr.resize(I);
         float *w = scr.data();
         for (int li = 0; li < a.n_list; ++li) {

@@ -192,6 +192,7 @@ __device__ void scatter_run(int p0, int p1, int k, int nbits, const int32_t *__r
             if (slot >= 0) {
                 ro.hit_pairs[pos] = p;
                 wv.row_tok[pos] = p / k;
+                wv.row_pair[pos] = p;
                 wv.row_gate[pos] = w[p];
             } else {
                 ro.miss_pairs[pos] = p;
@@ -289,6 +290,7 @@ __device__ void scan_experts(int E, int T, int k, int shared_slot, const int32_t
     if (shared_slot >= 0) {
         for (int t = threadIdx.x; t < T; t += blockDim.x) {
             wv.row_tok[nh + t] = t;
+            wv.row_pair[nh + t] = T * k + t;
             wv.row_gate[nh + t] = 1.0f;
         }
     }
@@ -556,6 +558,7 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
             if (slot >= 0) {
                 a.ro.hit_pairs[pos] = p;
                 a.wv.row_tok[pos] = p / k;
+                a.wv.row_pair[pos] = p;
                 a.wv.row_gate[pos] = s_w[p];
             } else {
                 a.ro.miss_pairs[pos] = p;
@@ -571,6 +574,7 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     if (a.shared_slot >= 0) {
         for (int t = tid; t < T; t += kFusedThreads) {
             a.wv.row_tok[nh + t] = t;
+            a.wv.row_pair[nh + t] = T * k + t;
             a.wv.row_gate[nh + t] = 1.0f;
         }
     }
@@ -743,6 +747,7 @@ __global__ __launch_bounds__(kWave) void route_wave(RouteArgs a) {
         if (sl >= 0) {
             a.ro.hit_pairs[pos] = lane;
             a.wv.row_tok[pos] = lane / k;
+            a.wv.row_pair[pos] = lane;
             a.wv.row_gate[pos] = pw;
         } else {
             a.ro.miss_pairs[pos] = lane;
@@ -752,6 +757,7 @@ __global__ __launch_bounds__(kWave) void route_wave(RouteArgs a) {
     }
     if (a.shared_slot >= 0 && lane < T) {
         a.wv.row_tok[nh + lane] = lane;
+        a.wv.row_pair[nh + lane] = T * k + lane;
         a.wv.row_gate[nh + lane] = 1.0f;
     }
 }
@@ -887,6 +893,124 @@ static hipError_t launch_route_npl(RouteArgs a, hipStream_t s) {
     const int scan_lds = 4 * (6 * a.E + 3 + a.scan_parts * a.E + ncnt);
     hipLaunchKernelGGL(route_scan, dim3(1), dim3(1024), scan_lds, s, a, nblk);
     hipLaunchKernelGGL(route_scatter, dim3(nblk), dim3(64), 0, s, a);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
+// Evaluation groups of a hybrid step, G = H u F (Section 3.2: after the planned fills the GPU
+// evaluates the hits and the freshly filled experts), built from the step's single routing after
+// the cache plan rewrote the routed slot ids: an expert with routed pairs forms a group iff its
+// first pair now carries a slot (hits keep theirs, filled experts carry their new slot, experts
+// left to the CPU keep FT_SLOT_MISS).  Its pairs are its hit list or, for a filled expert, its
+// miss list (an expert's pairs are all hits or all misses).  Writes the same group table, M-tile
+// map and row arrays as the router, in expert-id order, then the shared expert's rows.
+// One 1024-thread workgroup, thread e = expert e.
+__global__ __launch_bounds__(1024) void regroup_kernel(RegroupArgs a) {
+    __shared__ int32_t s_beg[kMaxExperts + 1];   // first row of group g
+    __shared__ int32_t s_src[kMaxExperts];       // list position of group g's first pair (miss list: + T*k)
+    __shared__ uint32_t s_wsum[3][1024 / kWave];
+    __shared__ int32_t s_tot[4];
+    const int E = a.E, T = a.T, k = a.k, tid = threadIdx.x;
+    const int lane = lane_id(), wv = tid / kWave;
+    const int PK = T * k;
+    // ---- this expert's group
+    int n = 0, src = 0, slot = -1;
+    if (tid < E) {
+        const int h0 = a.hit_off[tid], h1 = a.hit_off[tid + 1];
+        const int m0 = a.miss_off[tid], m1 = a.miss_off[tid + 1];
+        if (h1 > h0) {
+            n = h1 - h0;
+            src = h0;
+            slot = a.topk_slot[a.hit_pairs[h0]];
+        } else if (m1 > m0) {
+            n = m1 - m0;
+            src = PK + m0;
+            slot = a.topk_slot[a.miss_pairs[m0]];
+        }
+        if (slot < 0) n = 0;
+    }
+    const uint32_t in_g = n > 0 ? 1u : 0u;
+    const uint32_t rows = static_cast<uint32_t>(n);
+    const uint32_t mts = in_g ? static_cast<uint32_t>((n + kGemmBM - 1) / kGemmBM) : 0u;
+    // ---- block-wide exclusive scans of (group flag, rows, M tiles) over the experts
+    const uint32_t gi = wave_incl_scan_u32(in_g), ri = wave_incl_scan_u32(rows), ti = wave_incl_scan_u32(mts);
+    if (lane == kWave - 1) {
+        s_wsum[0][wv] = gi;
+        s_wsum[1][wv] = ri;
+        s_wsum[2][wv] = ti;
+    }
+    __syncthreads();
+    uint32_t gb = 0, rb = 0, tb = 0;
+    for (int w = 0; w < wv; ++w) {
+        gb += s_wsum[0][w];
+        rb += s_wsum[1][w];
+        tb += s_wsum[2][w];
+    }
+    const int g = static_cast<int>(gb + gi - in_g), r0 = static_cast<int>(rb + ri - rows),
+              t0 = static_cast<int>(tb + ti - mts);
+    if (in_g) {
+        a.wv.grp_slot[g] = slot;
+        a.wv.grp_beg[g] = r0;
+        a.wv.grp_len[g] = n;
+        a.wv.grp_mt_off[g] = t0;
+        for (uint32_t i = 0; i < mts; ++i) a.wv.mt_group[t0 + i] = g;
+        s_beg[g] = r0;
+        s_src[g] = src;
+    }
+    if (tid == 1023) {
+        // totals over every wave: thread 1023 is the last lane of the last wave
+        uint32_t U = 0, NR = 0, MT = 0;
+        for (int w = 0; w < 1024 / kWave; ++w) {
+            U += s_wsum[0][w];
+            NR += s_wsum[1][w];
+            MT += s_wsum[2][w];
+        }
+        s_tot[0] = static_cast<int>(U);
+        s_tot[1] = static_cast<int>(NR);
+        s_beg[U] = static_cast<int>(NR);
+        const uint32_t smt = a.shared_slot >= 0 ? (T + kGemmBM - 1) / kGemmBM : 0;
+        const uint32_t G = U + (a.shared_slot >= 0 ? 1 : 0);
+        a.wv.grp_meta[0] = G;
+        a.wv.grp_meta[1] = U;
+        a.wv.grp_meta[2] = NR;
+        a.wv.grp_meta[3] = T;
+        a.wv.grp_meta[4] = MT + smt;
+        if (a.shared_slot >= 0) {
+            a.wv.grp_slot[U] = a.shared_slot;
+            a.wv.grp_beg[U] = NR;
+            a.wv.grp_len[U] = T;
+            a.wv.grp_mt_off[U] = MT;
+            for (uint32_t i = 0; i < smt; ++i) a.wv.mt_group[MT + i] = U;
+        }
+        a.wv.grp_mt_off[G] = MT + smt;
+    }
+    __syncthreads();
+    // ---- rows: row r of group g is pair i = r - beg(g) of its list
+    const int U = s_tot[0], NR = s_tot[1];
+    for (int r = tid; r < NR; r += 1024) {
+        int lo = 0, hi = U - 1;           // the last group whose first row is <= r
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_beg[mid] <= r) lo = mid;
+            else hi = mid - 1;
+        }
+        const int at = s_src[lo] + (r - s_beg[lo]);
+        const int p = at < PK ? a.hit_pairs[at] : a.miss_pairs[at - PK];
+        a.wv.row_tok[r] = p / k;
+        a.wv.row_pair[r] = p;
+        a.wv.row_gate[r] = a.topk_w[p];
+    }
+    if (a.shared_slot >= 0) {
+        for (int t = tid; t < T; t += 1024) {
+            a.wv.row_tok[NR + t] = t;
+            a.wv.row_pair[NR + t] = PK + t;
+            a.wv.row_gate[NR + t] = 1.0f;
+        }
+    }
+}
+
+hipError_t launch_regroup(const RegroupArgs &a, hipStream_t s) {
+    hipLaunchKernelGGL(regroup_kernel, dim3(1), dim3(1024), 0, s, a);
     return hipGetLastError();
 }
 

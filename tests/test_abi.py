@@ -141,25 +141,37 @@ def test_fill_and_hybrid_reject_before_enqueue():
     assert lib.ft_cache_fill(ctypes.byref(d), ctypes.byref(b), ctypes.byref(b), ctypes.byref(pl), 65, None) == ftm.FT_ERR_SHAPE
     nb = ftm.ft_banks_t(None, FAKE, None, None)
     assert lib.ft_cache_fill(ctypes.byref(d), ctypes.byref(nb), ctypes.byref(b), ctypes.byref(pl), 4, None) == ftm.FT_ERR_NULL
-    st = ftm.ft_cache_state_t(FAKE, FAKE)
+    st = ftm.ft_cache_state_t(FAKE, FAKE, None)
     pol = ftm.ft_cache_policy_t(1.0, 2.0, 4, 1)
     r = ftm.ft_route_t(*[FAKE] * 8)
-    h = ftm.ft_hybrid_host_t(*[FAKE] * 6)
+    h = ftm.ft_hybrid_host_t(*[FAKE] * 7)
     args = [ctypes.byref(d), ctypes.byref(b), ctypes.byref(b), FAKE, FAKE, ctypes.byref(st),
-            ctypes.byref(pol), FAKE, 4, FAKE, FAKE, ctypes.byref(r), ctypes.byref(pl), ctypes.byref(h),
-            FAKE, 1 << 20, 0, None]
+            ctypes.byref(pol), FAKE, 4, FAKE, ctypes.byref(r), ctypes.byref(pl), ctypes.byref(h),
+            FAKE, 1 << 20, None, FAKE]
     a = list(args)
-    a[13] = ctypes.byref(ftm.ft_hybrid_host_t(FAKE, FAKE, FAKE, FAKE, FAKE, None))
+    a[12] = ctypes.byref(ftm.ft_hybrid_host_t(FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE))
     assert lib.ft_moe_step_hybrid(*a) == ftm.FT_ERR_NULL
     a = list(args)
-    a[10] = None
+    a[12] = ctypes.byref(ftm.ft_hybrid_host_t(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None))   # no task
     assert lib.ft_moe_step_hybrid(*a) == ftm.FT_ERR_NULL
     a = list(args)
-    a[10] = FAKE + 4           # misaligned CPU-partial scratch
+    a[9] = None                # no output
+    assert lib.ft_moe_step_hybrid(*a) == ftm.FT_ERR_NULL
+    a = list(args)
+    a[12] = ctypes.byref(ftm.ft_hybrid_host_t(FAKE, FAKE, FAKE, FAKE, FAKE + 4, FAKE, FAKE))   # misaligned x staging
     assert lib.ft_moe_step_hybrid(*a) == ftm.FT_ERR_SHAPE
     a = list(args)
     a[8] = 0
     assert lib.ft_moe_step_hybrid(*a) == ftm.FT_OK
+
+
+def test_cpu_pool_create_destroy():
+    """Pools start, serve a no-op call and stop; unpinned and pinned, explicit and default sizes."""
+    for n, pin in ((1, False), (3, True), (0, True)):
+        p = ftm.ft_cpu_pool_create(n, pin)
+        assert p.handle
+        ftm.ft_cpu_pool_destroy(p)
+        assert p.handle is None
 
 
 def test_library_has_no_undefined_library_symbols():

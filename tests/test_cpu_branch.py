@@ -26,8 +26,8 @@ def _pool_case(seed, wdt, gating, E, k, T, H, I):
 
 
 CASES = [
-    # seed, w_dtype, gating, E, k, T, H, I, n_threads
-    (0, workloads.DT_F32, 0, 8, 2, 5, 128, 256, 1),
+    # seed, w_dtype, gating, E, k, T, H, I, pool threads (None: the calling thread alone)
+    (0, workloads.DT_F32, 0, 8, 2, 5, 128, 256, None),
     (1, workloads.DT_BF16, 1, 16, 4, 9, 256, 128, 3),
     (2, workloads.DT_BF16, 0, 12, 3, 1, 384, 256, 0),
     (3, workloads.DT_FP8, 1, 10, 4, 6, 256, 384, 4),
@@ -49,7 +49,10 @@ def test_cpu_experts_matches_oracle(case):
     ids = torch.tensor(r["topk_ids"], dtype=torch.int32)
     w = torch.tensor(r["topk_w"], dtype=torch.float32)
     out = torch.empty(T, H, dtype=torch.float32)
-    ftm.ft_cpu_experts(desc, pool, lay.x, T, ids, w, torch.tensor(listed), out, n_threads=nt)
+    workers = None if nt is None else ftm.ft_cpu_pool_create(nt, pin=bool(seed % 2))
+    ftm.ft_cpu_experts(desc, pool, lay.x, T, ids, w, torch.tensor(listed), out, pool=workers)
+    if workers is not None:
+        ftm.ft_cpu_pool_destroy(workers)
     # oracle: a cache holding exactly the listed experts, bank row = expert id
     d2 = dict(desc, n_slots=E, shared_slot=-1)
     table = np.full(E, -1, np.int32)
@@ -62,6 +65,8 @@ def test_cpu_experts_matches_oracle(case):
 
 
 def test_cpu_experts_is_thread_count_independent():
+    """Bit-identical results on the calling thread and on pools of 1, 2 and 5 workers; one pool
+    serves several calls in a row."""
     lay, pool = _pool_case(9, workloads.DT_BF16, 0, 16, 4, 7, 256, 256)
     desc = lay.desc()
     r = oracle.route(desc, lay.logits.numpy(), lay.slot_table.numpy())
@@ -69,11 +74,15 @@ def test_cpu_experts_is_thread_count_independent():
     w = torch.tensor(r["topk_w"], dtype=torch.float32)
     listed = torch.arange(0, 16, 2, dtype=torch.int32)
     outs = []
-    for nt in (1, 2, 5):
-        out = torch.empty(7, 256, dtype=torch.float32)
-        ftm.ft_cpu_experts(desc, pool, lay.x, 7, ids, w, listed, out, n_threads=nt)
-        outs.append(out)
-    assert torch.equal(outs[0], outs[1]) and torch.equal(outs[0], outs[2])
+    for nt in (None, 1, 2, 5):
+        workers = None if nt is None else ftm.ft_cpu_pool_create(nt, pin=True)
+        for _ in range(3):
+            out = torch.empty(7, 256, dtype=torch.float32)
+            ftm.ft_cpu_experts(desc, pool, lay.x, 7, ids, w, listed, out, pool=workers)
+            outs.append(out)
+        if workers is not None:
+            ftm.ft_cpu_pool_destroy(workers)
+    assert all(torch.equal(outs[0], o) for o in outs[1:])
 
 
 def test_cpu_experts_rejects_bad_lists():

@@ -1,10 +1,12 @@
 """Cache fills and the complete hybrid layer step (GPU hits and fills + CPU branch + exact merge)
 against the oracle.
 
-Every step routes on the current cache, plans, fills the planned slots from the pinned host pool,
-evaluates hits and fills on the GPU and the rest on the CPU, and merges: the output must equal the
-oracle's output of the full MoE layer (every expert), the cache state must equal the oracle's
-plan bit for bit, and every occupied slot must hold its expert's weights bit for bit.
+Every step routes once on the current cache, plans, fills the planned slots from the pinned host
+pool, evaluates hits and fills on the GPU from the plan's rewritten slot ids and the rest on the
+CPU (a host function on a second stream, on a persistent worker pool), and merges: the output must
+equal the oracle's output of the full MoE layer (every expert), the cache state must equal the
+oracle's plan bit for bit, and every occupied slot must hold its expert's weights bit for bit.
+The same step captured in a HIP graph is checked the same way on every replay.
 """
 import numpy as np
 import pytest
@@ -27,7 +29,7 @@ def _say(msg):
 class Setup:
     """Host pool (pinned, indexed by expert), device slot banks, cache state and buffers."""
 
-    def __init__(self, seed, wdt, gating, E, R, k, T, H, I, shared, K):
+    def __init__(self, seed, wdt, gating, E, R, k, T, H, I, shared, K, clock=False):
         lay = workloads.random_layer(seed, hidden=H, inter=I, n_experts=E, top_k=k, tokens=T,
                                      gating=gating, w_dtype=wdt, n_resident=E, shared=shared)
         st = lay.slot_table.long()
@@ -58,13 +60,13 @@ class Setup:
         self.x_dtype = lay.x.dtype
         self.table = torch.full((E,), -1, dtype=torch.int32, device="cuda")
         self.state = ftm.CacheState(torch.full((n_slots,), -1, dtype=torch.int32, device="cuda"),
-                                    torch.zeros(n_slots, dtype=torch.int32, device="cuda"))
+                                    torch.zeros(n_slots, dtype=torch.int32, device="cuda"),
+                                    torch.zeros(1, dtype=torch.int32, device="cuda") if clock else None)
         self.route = ftm.RouteBuffers(T, k, E)
         self.plan = ftm.FillPlanBuffers(K, E)
         self.ws = ftm.alloc_workspace(self.desc, T)
         self.host = ftm.HybridHostBuffers(T, k, E, H, self.x_dtype)
         self.out = torch.empty(T, H, dtype=torch.float32, device="cuda")
-        self.cpu_out_dev = torch.empty(T, H, dtype=torch.float32, device="cuda")
 
     def oracle_full(self, logits, x):
         """Output of the full layer: every routed expert resident (bank row = expert id), plus the
@@ -98,6 +100,40 @@ def _logits(rng, T, E, rank):
     return (rng.standard_normal((T, E)) - 1.1 * np.log(rank)[None, :]).astype(np.float32)
 
 
+@pytest.fixture(scope="module")
+def workers():
+    p = ftm.ft_cpu_pool_create(3, pin=True)
+    yield p
+    ftm.ft_cpu_pool_destroy(p)
+
+
+class OracleCache:
+    """The oracle's cache state, advanced one step at a time on the oracle's routing."""
+
+    def __init__(self, su, bp, bh, K):
+        self.su, self.bp, self.bh, self.K = su, bp, bh, K
+        self.table = np.full(su.E, -1, np.int32)
+        self.sexp = np.full(su.desc["n_slots"], -1, np.int32)
+        self.stamp = np.zeros(su.desc["n_slots"], np.uint32)
+
+    def step_and_check(self, step, logits, x):
+        su = self.su
+        r = oracle.route(su.desc, logits, self.table)
+        plan = oracle.cache_plan(su.desc, r, self.table, self.sexp, self.stamp, self.bp, self.bh,
+                                 self.K, step)
+        self.table, self.sexp, self.stamp = plan["slot_table"], plan["slot_expert"], plan["slot_stamp"]
+        assert np.array_equal(su.table.cpu().numpy(), self.table)
+        assert np.array_equal(su.state.slot_expert.cpu().numpy(), self.sexp)
+        assert np.array_equal(su.state.slot_stamp.cpu().numpy().astype(np.uint32), self.stamp)
+        assert su.plan.counts.cpu().tolist() == [plan["q"], plan["m"] - plan["q"], plan["m"], 0]
+        su.check_banks(self.sexp)
+        ref = su.oracle_full(logits, x)
+        err = oracle.max_rel_err(su.out.cpu().numpy(), ref)
+        _say(f"   step {step}: q={plan['q']} cpu={plan['m'] - plan['q']} max_rel_err={err:.2e}")
+        assert err <= TOL[su.wdt], step
+        return plan
+
+
 CASES = [
     # seed, w_dtype, gating, E, R (routed slots), k, T, H, I, shared, K, (B_P, B_H)
     (0, workloads.DT_BF16, 0, 16, 5, 4, 3, 256, 256, False, 4, (11.8, 47.5)),
@@ -109,14 +145,12 @@ CASES = [
 
 
 @pytest.mark.parametrize("case", CASES, ids=[str(c[0]) for c in CASES])
-def test_hybrid_steps_match_full_layer(case):
+def test_hybrid_steps_match_full_layer(case, workers):
     seed, wdt, gating, E, R, k, T, H, I, shared, K, (bp, bh) = case
     su = Setup(seed, wdt, gating, E, R, k, T, H, I, shared, K)
+    oc = OracleCache(su, bp, bh, K)
     rng = np.random.default_rng(seed)
     rank = rng.permutation(E) + 1
-    table = np.full(E, -1, np.int32)
-    sexp = np.full(su.desc["n_slots"], -1, np.int32)
-    stamp = np.zeros(su.desc["n_slots"], np.uint32)
     n_cpu_steps = n_fill_steps = 0
     for step in range(1, 11):
         if step == 6:
@@ -124,24 +158,57 @@ def test_hybrid_steps_match_full_layer(case):
         logits = _logits(rng, T, E, rank)
         x = torch.randn(T, H, generator=torch.Generator().manual_seed(seed * 100 + step)).to(su.x_dtype)
         _say(f"case {seed} step {step}")
-        ftm.ft_moe_step_hybrid(su.desc, su.dev, su.pool, torch.tensor(logits, device="cuda"),
-                               su.table, su.state, bp, bh, K, step, x.cuda(), T, su.out,
-                               su.cpu_out_dev, su.route, su.plan, su.host, su.ws, n_threads=3)
+        lg, xd = torch.tensor(logits, device="cuda"), x.cuda()
+        # odd steps without a pool: the CPU branch then runs on the runtime's callback thread
+        ftm.ft_moe_step_hybrid(su.desc, su.dev, su.pool, lg, su.table, su.state, bp, bh, K, step, xd, T,
+                               su.out, su.route, su.plan, su.host, su.ws,
+                               workers if step % 2 == 0 else None)
         torch.cuda.synchronize()
-        # cache state against the oracle's plan on the same routing
-        r = oracle.route(su.desc, logits, table)
-        plan = oracle.cache_plan(su.desc, r, table, sexp, stamp, bp, bh, K, step)
-        table, sexp, stamp = plan["slot_table"], plan["slot_expert"], plan["slot_stamp"]
-        assert np.array_equal(su.table.cpu().numpy(), table)
-        assert np.array_equal(su.state.slot_expert.cpu().numpy(), sexp)
-        assert np.array_equal(su.state.slot_stamp.cpu().numpy().astype(np.uint32), stamp)
-        assert su.plan.counts.cpu().tolist() == [plan["q"], plan["m"] - plan["q"], plan["m"], 0]
+        plan = oc.step_and_check(step, logits, x)
         n_cpu_steps += plan["m"] > plan["q"]
         n_fill_steps += plan["q"] > 0
-        su.check_banks(sexp)
-        # the merged output is the full layer's
-        ref = su.oracle_full(logits, x)
-        assert oracle.max_rel_err(su.out.cpu().numpy(), ref) <= TOL[wdt], step
+    assert n_fill_steps > 0
+    if bh > bp:
+        assert n_cpu_steps > 0
+
+
+@pytest.mark.parametrize("case", [CASES[0], CASES[3]], ids=["0", "3"])
+def test_hybrid_step_graph_replays_match_full_layer(case, workers):
+    """The step captured once in a HIP graph (fixed input buffers, a device step clock) and
+    replayed step after step, with new inputs copied in eagerly between replays: every replay's
+    cache state, slot bytes and merged output match the oracle, and the captured CPU branch runs."""
+    seed, wdt, gating, E, R, k, T, H, I, shared, K, (bp, bh) = case
+    su = Setup(seed, wdt, gating, E, R, k, T, H, I, shared, K, clock=True)
+    oc = OracleCache(su, bp, bh, K)
+    lg_buf = torch.zeros(T, E, dtype=torch.float32, device="cuda")
+    x_buf = torch.zeros(T, H, dtype=su.x_dtype, device="cuda")
+    cap = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    torch.cuda.synchronize()
+    with torch.cuda.graph(graph, stream=cap, capture_error_mode="relaxed"):
+        ftm.ft_moe_step_hybrid(su.desc, su.dev, su.pool, lg_buf, su.table, su.state, bp, bh, K, 0,
+                               x_buf, T, su.out, su.route, su.plan, su.host, su.ws,
+                               workers, stream=cap)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(seed + 1000)
+    rank = rng.permutation(E) + 1
+    n_cpu_steps = n_fill_steps = 0
+    for step in range(1, 9):
+        if step == 5:
+            rank = rng.permutation(E) + 1
+        logits = _logits(rng, T, E, rank)
+        x = torch.randn(T, H, generator=torch.Generator().manual_seed(seed * 100 + step)).to(su.x_dtype)
+        lg_buf.copy_(torch.tensor(logits))
+        x_buf.copy_(x)
+        su.out.fill_(float("nan"))
+        torch.cuda.synchronize()
+        _say(f"graph case {seed} replay {step}")
+        graph.replay()
+        torch.cuda.synchronize()
+        assert int(su.state.clock[0]) == step
+        plan = oc.step_and_check(step, logits, x)
+        n_cpu_steps += plan["m"] > plan["q"]
+        n_fill_steps += plan["q"] > 0
     assert n_fill_steps > 0
     if bh > bp:
         assert n_cpu_steps > 0
