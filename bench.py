@@ -98,14 +98,15 @@ def algorithmic_work(lay, route):
                 gateup_flops=rows * 4 * H * I, u_hit=u_hit, n_hit=n_hit, rows=rows)
 
 
-def kernel_source_sha() -> str:
-    """Hash of the HIP sources the library is built from (traffic figures are tied to it)."""
-    import glob
+def kernel_source_sha(kernel: str) -> str:
+    """Hash of the sources a dominant kernel is built from (its traffic figures are tied to it):
+    the GEMM's or the GEMV's file plus the shared device and interface headers."""
     import hashlib
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(ROOT, "paper_2608_16157_amd", "csrc", "*"))):
-        with open(f, "rb") as fh:
-            h.update(os.path.basename(f).encode() + b"\0" + fh.read())
+    main = "gemm.hip" if "gemm" in kernel else "experts.hip"
+    for name in (main, "ftmoe_device.h", "ftmoe_internal.h"):
+        with open(os.path.join(ROOT, "paper_2608_16157_amd", "csrc", name), "rb") as fh:
+            h.update(name.encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
 
 
@@ -120,7 +121,7 @@ def measured_traffic(key: str):
             rec = json.load(fh).get(key)
     except (OSError, ValueError):
         return None
-    if not rec or rec.get("source_sha") != kernel_source_sha():
+    if not rec or rec.get("source_sha") != kernel_source_sha(rec.get("kernel", "")):
         return None
     return rec.get("traffic_bytes")
 
@@ -165,7 +166,7 @@ def ingest_traffic(key, kernel_match, fetch_csv, write_csv, cal_fetch_csv, cal_w
             data = json.load(fh)
     except (OSError, ValueError):
         data = {}
-    data[key] = {"kernel": kernel_match, "source_sha": kernel_source_sha(),
+    data[key] = {"kernel": kernel_match, "source_sha": kernel_source_sha(kernel_match),
                  "fetch_bytes": round(fetch), "write_bytes": round(write),
                  "traffic_bytes": round(fetch + write),
                  "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)}

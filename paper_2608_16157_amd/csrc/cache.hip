@@ -14,7 +14,9 @@
 //   2  every hit expert marks its slot as used in this step;
 //   3  every evictable slot (not hit, not the shared expert's) gets its rank by
 //      (age, slot id), age 0 for an empty slot and stamp + 1 otherwise; ranks below K are the
-//      LRU candidates.  Every missing expert gets its rank by (demand desc, id asc);
+//      LRU candidates (up to 256 slots each slot counts the slots before it; larger pools sort
+//      (age, slot id) keys with a bitonic network in LDS and take the first K).  Every missing
+//      expert gets its rank by (demand desc, id asc);
 //   4  q from m, B_P / B_H (double precision, rounded half up), K and the evictable count;
 //   5  the expert of demand rank i < q takes candidate i: fill list, slot table, slot owner,
 //      stamp and the routed pairs' slot ids are updated; the other missing experts are listed
@@ -28,12 +30,21 @@ namespace ftmoe {
 
 constexpr int kPlanThreads = 1024;
 static_assert(kMaxExperts <= kPlanThreads, "one thread per expert");
+constexpr int kPlanCountSlots = 256;   // pools up to this size rank slots by counting
+
+__host__ __device__ constexpr int pow2_at_least(int n) {
+    int p = 1;
+    while (p < n) p <<= 1;
+    return p;
+}
 
 __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
     extern __shared__ uint64_t plan_lds[];
     const int E = a.E, S = a.n_slots, K = a.K, tid = threadIdx.x;
-    uint64_t *s_key = plan_lds;                                      // [S] age key, ~0 = not evictable
-    int32_t *s_owner = reinterpret_cast<int32_t *>(s_key + S);       // [S] expert in the slot
+    const bool sorted = S > kPlanCountSlots;
+    const int SP = sorted ? pow2_at_least(S) : S;                    // key array length
+    uint64_t *s_key = plan_lds;                                      // [SP] age key, ~0 = not evictable
+    int32_t *s_owner = reinterpret_cast<int32_t *>(s_key + SP);      // [S] expert in the slot
     int32_t *s_dem = s_owner + S;                                    // [E] missed pairs, 0 = not missing
     int32_t *s_rank = s_dem + E;                                     // [E] demand rank of missing experts
     int32_t *s_cand = s_rank + E;                                    // [K] candidate slot by LRU rank
@@ -57,6 +68,7 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
                                       : (s_owner[s] < 0 ? 0ull : static_cast<uint64_t>(a.slot_stamp[s]) + 1ull);
     }
     if (has_e) s_dem[e_me] = mo1 - mo0;
+    for (int s = S + tid; s < SP; s += kPlanThreads) s_key[s] = kNotEvictable;   // sort padding
     if (tid == 0) s_misc[0] = 0;
     __syncthreads();
 
@@ -66,16 +78,41 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
 
     // ---- 3
     int nev = 0;
-    for (int s = tid; s < S; s += kPlanThreads) {
-        const uint64_t key = s_key[s];
-        if (key == kNotEvictable) continue;
-        ++nev;
-        int rank = 0;
-        for (int o = 0; o < S; ++o) {
-            const uint64_t ko = s_key[o];
-            rank += (ko < key) | ((ko == key) & (o < s));
+    if (!sorted) {
+        for (int s = tid; s < S; s += kPlanThreads) {
+            const uint64_t key = s_key[s];
+            if (key == kNotEvictable) continue;
+            ++nev;
+            int rank = 0;
+            for (int o = 0; o < S; ++o) {
+                const uint64_t ko = s_key[o];
+                rank += (ko < key) | ((ko == key) & (o < s));
+            }
+            if (rank < K) s_cand[rank] = s;
         }
-        if (rank < K) s_cand[rank] = s;
+    } else {
+        // (age, slot id) in one key: ages are at most 2^32, slot ids below 4096
+        for (int s = tid; s < S; s += kPlanThreads) {
+            const uint64_t key = s_key[s];
+            if (key == kNotEvictable) continue;
+            ++nev;
+            s_key[s] = (key << 12) | static_cast<uint64_t>(s);
+        }
+        __syncthreads();
+        for (int size = 2; size <= SP; size <<= 1)
+            for (int stride = size >> 1; stride > 0; stride >>= 1) {
+                for (int i = tid; i < SP / 2; i += kPlanThreads) {
+                    const int lo = 2 * i - (i & (stride - 1)), hi = lo + stride;
+                    const uint64_t x = s_key[lo], y = s_key[hi];
+                    if (((lo & size) == 0) == (x > y)) {
+                        s_key[lo] = y;
+                        s_key[hi] = x;
+                    }
+                }
+                __syncthreads();
+            }
+        for (int r = tid; r < K; r += kPlanThreads)
+            if (s_key[r] != kNotEvictable) s_cand[r] = static_cast<int>(s_key[r] & 0xFFF);
     }
     if (nev) atomicAdd(&s_misc[0], nev);
     for (int e = tid; e < E; e += kPlanThreads) {
@@ -138,7 +175,8 @@ __global__ __launch_bounds__(kPlanThreads) void cache_plan_kernel(PlanArgs a) {
 }
 
 hipError_t launch_cache_plan(const PlanArgs &a, hipStream_t s) {
-    const size_t lds = 8 * static_cast<size_t>(a.n_slots) + 4 * static_cast<size_t>(a.n_slots) +
+    const int sp = a.n_slots > kPlanCountSlots ? pow2_at_least(a.n_slots) : a.n_slots;
+    const size_t lds = 8 * static_cast<size_t>(sp) + 4 * static_cast<size_t>(a.n_slots) +
                        8 * static_cast<size_t>(a.E) + 4 * (kPlanMaxFill + 2);
     hipLaunchKernelGGL(cache_plan_kernel, dim3(1), dim3(kPlanThreads), lds, s, a);
     return hipGetLastError();

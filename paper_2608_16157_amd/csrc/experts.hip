@@ -433,6 +433,7 @@ __global__ __launch_bounds__(256) void zero_out(float *out, size_t n4) {
 // ascending j, then + y[T k + t] for the shared expert; tokens without any are exactly 0.
 __global__ __launch_bounds__(256) void combine_kernel(float *out, const float *y, const int32_t *topk_slot,
                                                       int T, int k, int H, int shared) {
+    constexpr int U = 8;   // pairs whose loads are issued together (no load waits on a branch)
     const int h4 = H / 4;
     const size_t n4 = static_cast<size_t>(T) * h4;
     const float4 *y4 = reinterpret_cast<const float4 *>(y);
@@ -440,14 +441,25 @@ __global__ __launch_bounds__(256) void combine_kernel(float *out, const float *y
          i += static_cast<size_t>(gridDim.x) * 256) {
         const int t = static_cast<int>(i / h4), c = static_cast<int>(i % h4);
         float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int j = 0; j < k; ++j) {
-            const int p = t * k + j;
-            if (topk_slot[p] >= 0) {
-                const float4 v = y4[static_cast<size_t>(p) * h4 + c];
-                acc.x += v.x;
-                acc.y += v.y;
-                acc.z += v.z;
-                acc.w += v.w;
+        for (int j0 = 0; j0 < k; j0 += U) {
+            int sl[U];
+            float4 v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) sl[u] = j0 + u < k ? topk_slot[t * k + j0 + u] : -1;
+            // rows of pairs not evaluated on the GPU (or past k) are read but never added
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int p = t * k + min(j0 + u, k - 1);
+                v[u] = y4[static_cast<size_t>(p) * h4 + c];
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (sl[u] >= 0) {
+                    acc.x += v[u].x;
+                    acc.y += v[u].y;
+                    acc.z += v[u].z;
+                    acc.w += v[u].w;
+                }
             }
         }
         if (shared) {

@@ -187,3 +187,23 @@ def test_cache_plan_prefill_scale():
     ref = oracle.cache_plan(desc, r, table, sexp, stamp, 52.7, 77.3, 64, 5000)
     _check_plan(dc, ref, T, k)
     assert ref["q"] > 1
+
+
+@pytest.mark.parametrize("E,n_slots,shared,K", [(300, 600, True, 64), (1024, 4096, False, 40),
+                                                (1024, 700, True, 64)])
+def test_cache_plan_large_pools(E, n_slots, shared, K):
+    """Pools above 256 slots take the bitonic sort of (age, slot id) keys; up to the 4096-slot
+    limit, with random stamps (ties included) and empty slots."""
+    rng = np.random.default_rng(E + n_slots)
+    k, T = 8, 30
+    desc = _desc(E, k, n_slots, n_slots - 1 if shared else -1)
+    table, sexp, stamp = _random_state(rng, E, n_slots, shared)
+    stamp = (stamp % 50).astype(np.uint32)          # many equal stamps
+    logits = rng.standard_normal((T, E)).astype(np.float32)
+    _say(f"large pool E={E} slots={n_slots} K={K}")
+    dc = DeviceCache(desc, T, table, sexp, stamp, K)
+    dc.step(logits, 52.7, 77.3, 9000)
+    r = oracle.route(desc, logits, table)
+    ref = oracle.cache_plan(desc, r, table, sexp, stamp, 52.7, 77.3, K, 9000)
+    _check_plan(dc, ref, T, k)
+    assert ref["q"] > 1
