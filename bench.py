@@ -140,23 +140,33 @@ def calibrate_copy(mib: int, reps: int = 5):
                       "launches": reps}), flush=True)
 
 
-def ingest_traffic(key, kernel_match, fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, cal_bytes):
+def ingest_traffic(key, kernel_match, fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, cal_bytes,
+                   per_match=None):
     """Per-launch HBM traffic of the kernel whose name contains kernel_match, from rocprofv3
     --pmc FETCH_SIZE and WRITE_SIZE counter CSVs, each scaled by the same counter's reading for
     the copy calibration kernel of cal_bytes read and cal_bytes written; merged into
-    profiles/traffic.json under key."""
+    profiles/traffic.json under key.  A stage that the library issues as several dispatches
+    (the prefill GEMMs run in chunks of workgroups) is one launch: with per_match, the name of a
+    kernel dispatched once per layer forward, the counters of kernel_match are summed and divided
+    by that kernel's dispatch count."""
     import csv
+    cal = "AUnaryFunctor<float, float, float"     # the y = 1 * x copy kernel
 
-    def per_dispatch(path, match):
+    def readings(path, match):
         vals = []
         for r in csv.DictReader(open(path)):
             if match in r["Kernel_Name"]:
                 vals.append(float(r["Counter_Value"]))
         if not vals:
             raise SystemExit(f"no dispatch of {match!r} in {path}")
-        return sum(vals) / len(vals)
+        return vals
 
-    cal = "AUnaryFunctor<float, float, float"     # the y = 1 * x copy kernel
+    def per_dispatch(path, match):
+        vals = readings(path, match)
+        if per_match is None or match == cal:
+            return sum(vals) / len(vals)
+        return sum(vals) / len(readings(path, per_match))
+
     f_scale = cal_bytes / per_dispatch(cal_fetch_csv, cal)
     w_scale = cal_bytes / per_dispatch(cal_write_csv, cal)
     fetch = per_dispatch(fetch_csv, kernel_match) * f_scale
@@ -689,14 +699,17 @@ def main():
                          "(--layers traces per workload), then exit")
     ap.add_argument("--calibrate-copy", type=int, metavar="MIB",
                     help="run only a plain copy kernel of MIB MiB (counter calibration)")
-    ap.add_argument("--ingest-traffic", nargs=7,
-                    metavar=("KEY", "KERNEL", "FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV",
-                             "CAL_WRITE_CSV", "CAL_BYTES"),
-                    help="record per-launch HBM traffic from rocprofv3 counter CSVs and exit")
+    ap.add_argument("--ingest-traffic", nargs="+",
+                    metavar="KEY KERNEL FETCH_CSV WRITE_CSV CAL_FETCH_CSV CAL_WRITE_CSV CAL_BYTES [PER_KERNEL]",
+                    help="record per-launch HBM traffic from rocprofv3 counter CSVs and exit "
+                         "(PER_KERNEL: a kernel dispatched once per layer forward, for a stage "
+                         "issued as several dispatches)")
     args = ap.parse_args()
     if args.ingest_traffic:
         a = args.ingest_traffic
-        ingest_traffic(a[0], a[1], a[2], a[3], a[4], a[5], int(a[6]))
+        if len(a) not in (7, 8):
+            ap.error("--ingest-traffic takes 7 or 8 arguments")
+        ingest_traffic(a[0], a[1], a[2], a[3], a[4], a[5], int(a[6]), a[7] if len(a) == 8 else None)
         return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
