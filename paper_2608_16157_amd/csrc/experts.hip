@@ -179,7 +179,10 @@ __device__ __forceinline__ void mfma_kblock(const u32x4_t (&av)[ALd<WT>::n], con
 }
 
 // One work item = (group, NB x 16 weight rows).  The 4 waves of the workgroup split the item's
-// K blocks into contiguous quarters and meet in LDS; rows of the group are taken 16 at a time,
+// K blocks into contiguous quarters and meet in LDS (KSP = 4), or, when the K blocks do not split
+// evenly four ways (Qwen3's down projection: 6 blocks), pairs of waves take half of the item's
+// weight blocks each and split their K blocks in halves (KSP = 2), so no wave idles; rows of the
+// group are taken 16 at a time,
 // up to MTX M tiles per pass (MTX = 1 when no group can hold more than 16 rows, which keeps the
 // register count, and so the occupancy, of few-token calls down).  Each activation load feeds
 // the NB weight blocks of the item.
@@ -191,8 +194,10 @@ template <int WT, int EPI, int MTX> constexpr int gemv_min_blocks() {
     return WT != FT_DT_BF16 ? 1 : (EPI == EPI_GATEUP && MTX > 1 && FT_GEMV_DGU_BF16 > 1 ? 2 : 4);
 }
 
-template <int WT, int EPI, int NB, int MTX>
+template <int WT, int EPI, int NB, int MTX, int KSP = kGemvWaves>
 __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) void grouped_gemv(ExpertArgs a, int tiles) {
+    static_assert(KSP == kGemvWaves || (KSP == 2 && NB % 2 == 0), "K split: 4 waves, or 2 with an even block count");
+    constexpr int NBW = NB * KSP / kGemvWaves;   // weight blocks of each wave
     // the deeper batch of the one-M-tile kernels is used where the registers allow it (not by
     // the wide fp8 items)
     constexpr int D = (MTX == 1 && (WT != FT_DT_FP8E4M3FN_B128 || NB == 2))
@@ -201,7 +206,7 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
     constexpr int NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
     constexpr int COLS = NB * 16;
     constexpr int KB = WTr<WT>::kBlock;                        // bytes of one row's K block
-    constexpr int STAGE = D * NB * 16 * KB;                   // per wave
+    constexpr int STAGE = D * NBW * 16 * KB;                  // per wave
     constexpr int REDW = 16 * (COLS + 1) * 4;                  // one wave's partial sums
     constexpr int PW = ((STAGE > REDW ? STAGE : REDW) + 255) / 256 * 256;
     // A wave writes its partial sums into its own staging area once its own K range is done (its
@@ -224,16 +229,17 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
     const int K = EPI == EPI_GATEUP ? H : I;
     const int wave = threadIdx.x / kWave, lane = lane_id();
     const int n = lane & 15, q = lane >> 4;
+    const int bw0 = (wave / KSP) * NBW, kw = wave % KSP;   // first block and K part of this wave
     const int nrows = EPI == EPI_GATEUP ? 2 * I : H;
     const int nkb = K / 128;
     // weight row of this lane's N column in block b: a gate/up block pairs 8 gate rows with the
     // 8 matching up rows, so SiLU(gate) * up of one h column stays inside the block
     const size_t row_bytes = static_cast<size_t>(nkb) * KB;
-    const float *sbase[NB];      // fp8: the row's 128 x 128 block scales
-    const uint8_t *xbase[NB];    // MXFP4: this lane's e8m0 scale of the row in K block 0
+    const float *sbase[NBW];     // fp8: the row's 128 x 128 block scales
+    const uint8_t *xbase[NBW];   // MXFP4: this lane's e8m0 scale of the row in K block 0
 #pragma unroll
-    for (int b = 0; b < NB; ++b) {
-        const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
+    for (int b = 0; b < NBW; ++b) {
+        const int col0 = (tile * NB + bw0 + b) * (EPI == EPI_GATEUP ? 8 : 16);
         const int wrow = EPI == EPI_GATEUP ? (n < 8 ? col0 + n : I + col0 + n - 8) : col0 + n;
         sbase[b] = nullptr;
         xbase[b] = nullptr;
@@ -249,24 +255,24 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
     // the chunk the swizzle puts there
     constexpr int LPR = KB / 16, RPI = 64 / LPR;
     static_assert(RPI * NL == 16, "one block is NL whole-row instructions");
-    const uint8_t *dsrc[NB][NL];
+    const uint8_t *dsrc[NBW][NL];
 #pragma unroll
-    for (int b = 0; b < NB; ++b)
+    for (int b = 0; b < NBW; ++b)
 #pragma unroll
         for (int c = 0; c < NL; ++c) {
             const int j = c * RPI + lane / LPR;
-            const int col0 = (tile * NB + b) * (EPI == EPI_GATEUP ? 8 : 16);
+            const int col0 = (tile * NB + bw0 + b) * (EPI == EPI_GATEUP ? 8 : 16);
             const int wr = EPI == EPI_GATEUP ? (j < 8 ? col0 + j : I + col0 + j - 8) : col0 + j;
             dsrc[b][c] = static_cast<const uint8_t *>(EPI == EPI_GATEUP ? a.w13 : a.w2) +
                          (static_cast<size_t>(slot) * nrows + wr) * row_bytes + wswz<KB>(j, lane % LPR) * 16;
         }
     uint8_t *wst = s_lds + wave * PW;
     const size_t a_elem = (WT == FT_DT_F32) ? 4 : 2;
-    const int per = (nkb + kGemvWaves - 1) / kGemvWaves;
-    const int kb0 = min(nkb, wave * per), kb1 = min(nkb, kb0 + per);
+    const int per = (nkb + KSP - 1) / KSP;
+    const int kb0 = min(nkb, kw * per), kb1 = min(nkb, kb0 + per);
 
     // One pass over the K blocks for MT 16-row M tiles starting at row r0 (MT chosen per pass).
-    auto pass = [&](auto mt_const, int r0, floatx4_t (&acc)[MTX][NB]) {
+    auto pass = [&](auto mt_const, int r0, floatx4_t (&acc)[MTX][NBW]) {
         constexpr int MT = decltype(mt_const)::value;
         const uint8_t *arow[MT];
 #pragma unroll
@@ -286,9 +292,9 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
         // barrier keeps the compiler from interleaving the loads with the MFMAs that use them.
         for (int kbb = kb0; kbb < kb1; kbb += D) {
             u32x4_t av[D][MT][NA];
-            u32x4_t wv[D][NB][NL];
-            float sv[D][NB];
-            uint32_t xv[D][NB];
+            u32x4_t wv[D][NBW][NL];
+            float sv[D][NBW];
+            uint32_t xv[D][NBW];
 #pragma unroll
             for (int d = 0; d < D; ++d) {
                 const int kb = min(kbb + d, kb1 - 1);
@@ -296,10 +302,10 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
                 for (int mt = 0; mt < MT; ++mt)
                     aload<WT>(av[d][mt], arow[mt] + static_cast<size_t>(kb) * 128 * a_elem, q);
 #pragma unroll
-                for (int b = 0; b < NB; ++b) {
+                for (int b = 0; b < NBW; ++b) {
 #pragma unroll
                     for (int c = 0; c < NL; ++c)
-                        gemv_dma16(dsrc[b][c] + static_cast<size_t>(kb) * KB, wst + ((d * NB + b) * 16 * KB + c * 1024));
+                        gemv_dma16(dsrc[b][c] + static_cast<size_t>(kb) * KB, wst + ((d * NBW + b) * 16 * KB + c * 1024));
                     if constexpr (WT == FT_DT_FP8E4M3FN_B128) sv[d][b] = sbase[b][kb];
                     if constexpr (WT == FT_DT_MXFP4) xv[d][b] = xbase[b][static_cast<size_t>(kb) * 4 * nrows];
                 }
@@ -312,18 +318,18 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
 #pragma unroll
                 for (int d = 0; d < D; ++d)
 #pragma unroll
-                    for (int b = 0; b < NB; ++b)
+                    for (int b = 0; b < NBW; ++b)
 #pragma unroll
                         for (int c = 0; c < NL; ++c)
                             wv[d][b][c] = *reinterpret_cast<const u32x4_t *>(
-                                wst + (d * NB + b) * 16 * KB + n * KB + wswz<KB>(n, 4 * c + q) * 16);
+                                wst + (d * NBW + b) * 16 * KB + n * KB + wswz<KB>(n, 4 * c + q) * 16);
             }
             __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int d = 0; d < D; ++d) {
                 const float keep = kbb + d < kb1 ? 1.f : 0.f;
 #pragma unroll
-                for (int b = 0; b < NB; ++b) {
+                for (int b = 0; b < NBW; ++b) {
                     u32x4_t wc[4];
                     if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
                         wc[0] = fp8x8_to_bf16x8(wv[d][b][0][0], wv[d][b][0][1]);
@@ -352,11 +358,11 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
     };
 
     for (int r0 = 0; r0 < len; r0 += 16 * MTX) {
-        floatx4_t acc[MTX][NB];
+        floatx4_t acc[MTX][NBW];
 #pragma unroll
         for (int mt = 0; mt < MTX; ++mt)
 #pragma unroll
-            for (int b = 0; b < NB; ++b) acc[mt][b] = floatx4_t{0.f, 0.f, 0.f, 0.f};
+            for (int b = 0; b < NBW; ++b) acc[mt][b] = floatx4_t{0.f, 0.f, 0.f, 0.f};
         const int nmt = min(MTX, (len - r0 + 15) / 16);
         if constexpr (MTX > 1) {
             if (nmt > 1) pass(std::integral_constant<int, MTX>{}, r0, acc);
@@ -365,18 +371,19 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
             pass(std::integral_constant<int, 1>{}, r0, acc);
         }
 
-        // lane (n, q) holds rows 4q + i of column n of every block; the 4 K quarters meet in LDS
+        // lane (n, q) holds rows 4q + i of column n of each of the wave's blocks; the KSP K parts
+        // of a block meet in LDS
         for (int mt = 0; mt < nmt; ++mt) {
             const int rt = r0 + mt * 16;
 #pragma unroll
-            for (int b = 0; b < NB; ++b)
+            for (int b = 0; b < NBW; ++b)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     float v = acc[0][b][i];
 #pragma unroll
                     for (int j = 1; j < MTX; ++j)
                         if (j == mt) v = acc[j][b][i];
-                    s_red(wave)[4 * q + i][b * 16 + n] = v;
+                    s_red(wave)[4 * q + i][(bw0 + b) * 16 + n] = v;
                 }
             __syncthreads();
             if constexpr (EPI == EPI_GATEUP) {
@@ -386,10 +393,11 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
                     const int r = rt + m;
                     if (r < len) {
                         float gs = 0.f, us = 0.f;
+                        const int w0 = (b / NBW) * KSP;   // the waves that hold block b
 #pragma unroll
-                        for (int w = 0; w < kGemvWaves; ++w) {
-                            gs += s_red(w)[m][b * 16 + c];
-                            us += s_red(w)[m][b * 16 + c + 8];
+                        for (int w = 0; w < KSP; ++w) {
+                            gs += s_red(w0 + w)[m][b * 16 + c];
+                            us += s_red(w0 + w)[m][b * 16 + c + 8];
                         }
                         const float hv = silu_f32(gs) * us;
                         const size_t o = static_cast<size_t>(beg + r) * I + (tile * NB + b) * 8 + c;
@@ -404,8 +412,9 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
                     const int r = rt + m;
                     if (r < len) {
                         float sum = 0.f;
+                        const int w0 = (c / 16 / NBW) * KSP;
 #pragma unroll
-                        for (int w = 0; w < kGemvWaves; ++w) sum += s_red(w)[m][c];
+                        for (int w = 0; w < KSP; ++w) sum += s_red(w0 + w)[m][c];
                         const float y = a.wv.row_gate[beg + r] * sum;
                         if (a.wv.ypart) {
                             const int p = a.wv.row_pair[beg + r];
@@ -478,6 +487,20 @@ static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
     auto go = [&](auto nb) {
         constexpr int NB = decltype(nb)::value;
         const int tiles = EPI == EPI_GATEUP ? a.I / (8 * NB) : a.H / (16 * NB);
+        const int nkb = (EPI == EPI_GATEUP ? a.H : a.I) / 128;
+        const bool ksp2 = nkb % kGemvWaves != 0 && nkb % 2 == 0;
+        auto run = [&](auto mtx) {
+            constexpr int MTX = decltype(mtx)::value;
+            if constexpr (NB % 2 == 0) {
+                if (ksp2) {
+                    hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB, MTX, 2>), dim3(a.max_groups * tiles),
+                                       dim3(kGemvThreads), 0, s, a, tiles);
+                    return;
+                }
+            }
+            hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB, MTX>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
+                               s, a, tiles);
+        };
         // a group holds at most T rows (the shared expert's group exactly T).  The wide fp8
         // gate/up items take four M tiles per pass above 32 tokens: a group of up to 64 rows
         // then streams its weights once, at no cost in occupancy (their register count allows
@@ -485,19 +508,16 @@ static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
         // MXFP4 gate/up items do so from 64 tokens (their occupancy halves: measured -1 % at
         // T = 48, +1 % at T = 64, +4 % at T = 128).
         if (a.T <= 16) {
-            hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB, 1>), dim3(a.max_groups * tiles), dim3(kGemvThreads), 0,
-                               s, a, tiles);
+            run(std::integral_constant<int, 1>{});
             return;
         }
         if constexpr ((WT == FT_DT_FP8E4M3FN_B128 || WT == FT_DT_MXFP4) && EPI == EPI_GATEUP && NB == 4) {
             if (a.T >= (WT == FT_DT_MXFP4 ? 64 : 33)) {
-                hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB, 4>), dim3(a.max_groups * tiles), dim3(kGemvThreads),
-                                   0, s, a, tiles);
+                run(std::integral_constant<int, 4>{});
                 return;
             }
         }
-        hipLaunchKernelGGL((grouped_gemv<WT, EPI, NB, FT_GEMV_MT_MAX>), dim3(a.max_groups * tiles),
-                           dim3(kGemvThreads), 0, s, a, tiles);
+        run(std::integral_constant<int, FT_GEMV_MT_MAX>{});
     };
     const int pairs = a.T * a.k;
     if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
