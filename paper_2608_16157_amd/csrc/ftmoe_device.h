@@ -115,6 +115,18 @@ __device__ __forceinline__ uint32_t wave_incl_scan_u32(uint32_t v) {
     return v + (row > 0 ? r0 : 0u) + (row > 1 ? r1 : 0u) + (row > 2 ? r2 : 0u);
 }
 
+// inclusive prefix maximum over the 64 lanes (lane order); 0 is the neutral value
+__device__ __forceinline__ uint32_t wave_incl_max_u32(uint32_t v) {
+    v = max(v, dpp_u32<kDppRowShr1>(v));
+    v = max(v, dpp_u32<kDppRowShr2>(v));
+    v = max(v, dpp_u32<kDppRowShr4>(v));
+    v = max(v, dpp_u32<kDppRowShr8>(v));
+    const uint32_t r0 = readlane_u32(v, 15), r1 = readlane_u32(v, 31), r2 = readlane_u32(v, 47);
+    const int row = lane_id() >> 4;
+    const uint32_t c = max(row > 0 ? r0 : 0u, max(row > 1 ? r1 : 0u, row > 2 ? r2 : 0u));
+    return max(v, c);
+}
+
 // Lanes of the wave whose `v` equals this lane's, restricted to `active`.
 __device__ __forceinline__ uint64_t match_lanes(uint32_t v, int nbits, uint64_t active) {
     uint64_t m = active;

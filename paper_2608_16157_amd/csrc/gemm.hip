@@ -218,7 +218,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     __shared__ float s_ratio[kFp8 ? kWavesN : 1][2][kFp8 ? kMaxKb : 1];
     __shared__ uint32_t s_keep[kFp8 ? kWavesN : 1][2][kFp8 ? kMaxKb : 1];
     __shared__ float s_last[kWavesN][2];
-    __shared__ int32_t s_anyzero;
+    __shared__ int32_t s_zeroblk[kWavesN];   // fp8: a column group's scales hold a 0
     __shared__ int32_t s_tok[kBM];
     __shared__ float s_gate[kBM];
     auto stA = [&](auto s) -> uint8_t * {
@@ -345,35 +345,38 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     const int nkb = K / 128;
     // fp8 block-scale tables of each wave's columns (gate half and up half of a gate/up tile; one
     // block for down), staged in LDS before the pipeline starts: a vector load inside the loop
-    // would make the compiler drain the DMA stages.  One lane per (wave, half) walks the K blocks
-    // in order: s' = the block's scale, or the previous s' when the scale is 0 (1 before the
-    // first nonzero block); the ratio of block k is s'(k-1) / s'(k) (1 for block 0).
+    // would make the compiler drain the DMA stages.  Lane kb of the waves of the first M row holds
+    // K block kb: s'(kb) = the scale of the last block at or before kb whose scale is not 0 (1
+    // before the first), found with a wave max-scan of the indices of such blocks; the ratio of
+    // block kb is s'(kb-1) / s'(kb) (1 for block 0).  One load per lane instead of a walk over
+    // the K blocks, whose dependent loads held every tile's start back by several microseconds.
     if constexpr (kFp8) {
-        if (t == 0) s_anyzero = 0;
-        __syncthreads();
-        if (t < kWavesN * 2) {
+        if (wm == 0) {
             const float *sp = static_cast<const float *>(EPI == GEMM_GATEUP ? a.s13 : a.s2);
-            const int w = t >> 1, which = t & 1;
-            int r;
-            if constexpr (EPI == GEMM_GATEUP) {
-                const int hc0 = nt * (kBN / 2) + w * (kWaveCols / 2);
-                r = which == 0 ? hc0 / 128 : (I + hc0) / 128;
-            } else {
-                r = (nt * kBN + w * kWaveCols) / 128;
+            uint64_t zero = 0;
+#pragma unroll
+            for (int which = 0; which < 2; ++which) {
+                int r;
+                if constexpr (EPI == GEMM_GATEUP) {
+                    const int hc0 = nt * (kBN / 2) + wn * (kWaveCols / 2);
+                    r = which == 0 ? hc0 / 128 : (I + hc0) / 128;
+                } else {
+                    r = (nt * kBN + wn * kWaveCols) / 128;
+                }
+                const float *row = sp + (static_cast<size_t>(slot) * (nrows / 128) + r) * nkb;
+                const float sc = lane < nkb ? row[lane] : 1.0f;
+                const bool nz = sc != 0.0f;
+                zero |= __ballot(lane < nkb && !nz);
+                const uint32_t last = wave_incl_max_u32(nz ? static_cast<uint32_t>(lane) + 1u : 0u);
+                const float cur = last ? __shfl(sc, static_cast<int>(last) - 1) : 1.0f;
+                const float prev = __shfl(cur, max(lane - 1, 0));
+                if (lane < nkb) {
+                    s_ratio[wn][which][lane] = lane == 0 ? 1.0f : prev / cur;
+                    s_keep[wn][which][lane] = nz ? 0xFFFFFFFFu : 0u;
+                }
+                if (lane == nkb - 1) s_last[wn][which] = cur;
             }
-            const float *row = sp + (static_cast<size_t>(slot) * (nrows / 128) + r) * nkb;
-            float prev = 1.0f;
-            int zero = 0;
-            for (int kb = 0; kb < nkb; ++kb) {
-                const float sc = row[kb];
-                const float cur = sc != 0.0f ? sc : prev;
-                s_ratio[w][which][kb] = kb == 0 ? 1.0f : prev / cur;
-                s_keep[w][which][kb] = sc != 0.0f ? 0xFFFFFFFFu : 0u;
-                zero |= sc == 0.0f;
-                prev = cur;
-            }
-            s_last[w][which] = prev;
-            if (zero) atomicOr(&s_anyzero, 1);
+            if (lane == 0) s_zeroblk[wn] = zero != 0;
         }
     }
     // token and gate of each row of the tile (down projection epilogue)
@@ -418,31 +421,6 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         const uint8_t *A = stA(rs);
         const uint8_t *B = stB(rs);
         const int ca = kFp8 ? 4 * (KSI / 2) + 2 * fq + (KSI % 2) : (kFp4 ? 4 * fq + KSI : 2 * KSI + fq);
-#pragma unroll
-        for (int i = 0; i < ML; ++i) {
-            const int ra = wm * kWaveRows + i * 32 + fn;
-            f.a[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, ca) << 4));
-        }
-#pragma unroll
-        for (int j = 0; j < kNJ; ++j) {
-            const int rb = wn * kWaveCols + j * 32 + fn;
-            if constexpr (kFp4) {
-                if constexpr (KSI == 0) {
-                    f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, fq) << 4));
-                    f.xb[j] = stX(rs)[xcol[j]];
-                } else {
-                    f.b[j] = prev.b[j];
-                    f.xb[j] = prev.xb[j];
-                }
-            } else if constexpr (kFp8) {
-                if constexpr (KSI % 2 == 0)
-                    f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, 2 * (KSI / 2) + fq) << 4));
-                else
-                    f.b[j] = prev.b[j];
-            } else {
-                f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, ca) << 4));
-            }
-        }
         if constexpr (kFp8) {
             if constexpr (KSI == 0) {
                 const int kb = (kt * BK) / 128;
@@ -461,6 +439,38 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
                 }
             }
         }
+#pragma unroll
+        for (int i = 0; i < ML; ++i) {
+            const int ra = wm * kWaveRows + i * 32 + fn;
+            f.a[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, ca) << 4));
+        }
+#pragma unroll
+        for (int j = 0; j < kNJ; ++j) {
+            const int rb = wn * kWaveCols + j * 32 + fn;
+            if constexpr (kFp4) {
+                if constexpr (KSI == 0) {
+                    f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, fq) << 4));
+                    f.xb[j] = stX(rs)[xcol[j]];
+                } else {
+                    f.b[j] = prev.b[j];
+                    f.xb[j] = prev.xb[j];
+                }
+            } else if constexpr (kFp8) {
+                if constexpr (KSI % 2 == 0) {
+                    f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, 2 * (KSI / 2) + fq) << 4));
+                    if constexpr (ZS) {
+                        // codes of a block with scale 0 become +0
+                        const uint32_t keep = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.keep[1] : f.keep[0];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) f.b[j][q] &= keep;
+                    }
+                } else {
+                    f.b[j] = prev.b[j];
+                }
+            } else {
+                f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, ca) << 4));
+            }
+        }
     };
     // rs: this sub-step opens a 128-wide K block (fp8: the accumulators take the block's factor)
     auto mma = [&](const Frag &f, auto ks, auto ml, auto zs, auto rs) {
@@ -473,11 +483,6 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
                 bf[j] = fp4x8_scaled_to_bf16x8(f.b[j][KSI], fp4_scale_operand(f.xb[j]));
             } else if constexpr (kFp8) {
                 bf[j] = KSI % 2 == 0 ? fp8x8_to_bf16x8(f.b[j][0], f.b[j][1]) : fp8x8_to_bf16x8(f.b[j][2], f.b[j][3]);
-                if constexpr (ZS) {
-                    const uint32_t keep = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.keep[1] : f.keep[0];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) bf[j][q] &= keep;
-                }
             } else {
                 bf[j] = f.b[j];
             }
@@ -573,6 +578,9 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     wait_vmcnt<0>();
     __syncthreads();
     static_for<0, NS>([&](auto s) { issue(min(decltype(s)::value, nk - 1), stA(s), stB(s), s); });
+    bool any_zero_scale = false;
+    if constexpr (kFp8)
+        for (int w = 0; w < kWavesN; ++w) any_zero_scale |= s_zeroblk[w] != 0;
     // one main loop per live sub-tile count (in steps of MLQ sub-tiles for tall tiles)
     constexpr int MLQ = kMI > 4 ? 2 : 1;
     const int wrows = min(max(len - m0 - wm * kWaveRows, 0), kWaveRows);   // real rows of this wave
@@ -584,7 +592,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         constexpr int ML = decltype(q)::value * MLQ;
         if (mlive == ML) {
             if constexpr (kFp8) {
-                if (s_anyzero) mainloop(ic<ML>{}, ic<1>{});
+                if (any_zero_scale) mainloop(ic<ML>{}, ic<1>{});
                 else mainloop(ic<ML>{}, ic<0>{});
             } else {
                 mainloop(ic<ML>{}, ic<0>{});
