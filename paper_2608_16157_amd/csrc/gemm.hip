@@ -487,21 +487,16 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
                 bf[j] = f.b[j];
             }
         }
-        if constexpr (kFp8 && RS) {
-#pragma unroll
-            for (int i = 0; i < ML; ++i)
-#pragma unroll
-                for (int j = 0; j < kNJ; ++j) {
-                    const float r = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.sc[1] : f.sc[0];
-                    acc[i][j] *= r;
-                }
-        }
+        // a tile's accumulators take the block factor just before its MFMA, so the multiplies of one
+        // tile can run while the previous tile's MFMA executes (see interleave)
 #pragma unroll
         for (int i = 0; i < ML; ++i)
 #pragma unroll
-            for (int j = 0; j < kNJ; ++j)
+            for (int j = 0; j < kNJ; ++j) {
+                if constexpr (kFp8 && RS) acc[i][j] *= (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.sc[1] : f.sc[0];
                 acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(f.a[i]), as_bf16x8(bf[j]), acc[i][j], 0,
                                                                      0, 0);
+            }
     };
 
     // Software pipeline.  The ring holds NS stages; the DMA of stage kt + NS goes into the slot of
@@ -516,20 +511,32 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     // Order of one sub-step's instructions: its MFMAs with the next sub-step's operand reads
     // (sub-step ks2 of the same or the next stage) threaded between them, one read after each
     // MFMA.  Measured 2-4 % faster than issuing all the reads first behind an explicit wait.
-    auto interleave = [&](auto ks2, auto ml, auto zs) {
+    // In a sub-step that opens an fp8 K block (rsv) each MFMA is preceded by the 16 multiplies of
+    // its tile's block factor (the first also by the widening of the sub-step's weight operands).
+    auto interleave = [&](auto ks2, auto ml, auto zs, auto rsv) {
         constexpr int K2 = decltype(ks2)::value, ML = decltype(ml)::value;
-        constexpr bool ZS = decltype(zs)::value;
+        constexpr bool ZS = decltype(zs)::value, RSV = decltype(rsv)::value;
         constexpr bool kReadsB = kFp4 ? K2 == 0 : (kFp8 ? K2 % 2 == 0 : true);
         constexpr int kReads = ML + (kReadsB ? kNJ : 0) + (kFp4 && K2 == 0 ? kNJ : 0) +
                                (kFp8 && K2 == 0 ? (ZS ? 4 : 2) : 0);
         constexpr int kMfma = ML * kNJ;
         constexpr int kPairs = kReads < kMfma ? kReads : kMfma;
-        static_for<0, kPairs>([&](auto) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
-        });
-        if constexpr (kMfma > kPairs) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kPairs, 0);
-        if constexpr (kReads > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kPairs, 0);
+        if constexpr (RSV) {
+            static_for<0, kMfma>([&](auto q) {
+                constexpr int Q = decltype(q)::value;
+                __builtin_amdgcn_sched_group_barrier(0x002, Q == 0 ? 16 + 4 * kNJ : 16, 0);   // VALU
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // one MFMA
+                if constexpr (Q < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
+            });
+            if constexpr (kReads > kMfma) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kMfma, 0);
+        } else {
+            static_for<0, kPairs>([&](auto) {
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+            });
+            if constexpr (kMfma > kPairs) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kPairs, 0);
+            if constexpr (kReads > kPairs) __builtin_amdgcn_sched_group_barrier(0x100, kReads - kPairs, 0);
+        }
     };
     auto mainloop = [&](auto ml, auto zs) {
         Frag cur, nxt;
@@ -549,12 +556,13 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
                     issue(min(kt + NS, nk - 1), stA(s), stB(s), s);
                 }
                 __builtin_amdgcn_sched_barrier(0);
-                mma(cur, ks, ml, zs, ic<(kOpens && KSI == 0) ? 1 : 0>{});
+                constexpr int kRescale = (kOpens && KSI == 0) ? 1 : 0;
+                mma(cur, ks, ml, zs, ic<kRescale>{});
                 if constexpr (KSI + 1 < KS)
                     load_frag(s, ic<KSI + 1>{}, ml, zs, nxt, cur, kt);
                 else
                     load_frag(ic<(S + 1) % NS>{}, ic<0>{}, ml, zs, nxt, cur, min(kt + 1, nk - 1));
-                interleave(ic<(KSI + 1) % KS>{}, ml, zs);
+                interleave(ic<(KSI + 1) % KS>{}, ml, zs, ic<kRescale>{});
                 __builtin_amdgcn_sched_barrier(0);
                 cur = nxt;
             });
