@@ -28,6 +28,11 @@ routes each token to k of them).  The readings taken here:
 * expert FFN (SwiGLU): FFN(x) = W2 (silu(W1 x) * (W3 x)), silu(z) = z / (1 + exp(-z)).
 * output: out[t] = sum over hit pairs of g_tj FFN_e(x_t) (+ FFN_shared(x_t), weight 1, when a
   shared expert is configured); a token without hits and without shared expert gets 0.
+* fp8 activations (optional mode ACT_FP8_1X128_POW2, not the paper's exact method): the expert
+  inputs x and the intermediate h are quantised per token and 128-channel block to e4m3fn with
+  a power-of-two scale, the smallest 2^e with 448 * 2^e >= the block's largest magnitude, and
+  rounded to nearest, ties to even; h is first rounded to bfloat16 (round half to even).  Then
+  FFN(x) = W2 Q(bf16(silu(W1 Q(x)) * (W3 Q(x)))).  The exact mode (ACT_EXACT) is the default.
 """
 from __future__ import annotations
 
@@ -39,6 +44,9 @@ DT_F32 = 0
 DT_BF16 = 1
 DT_FP8 = 2
 DT_MXFP4 = 3
+
+ACT_EXACT = 0
+ACT_FP8_1X128_POW2 = 1
 
 STATUS_SLOT_RANGE = 1     # a slot outside [-1, n_slots)
 STATUS_SLOT_DUP = 2       # two experts share one slot
@@ -240,6 +248,51 @@ def expert_ffn(x: np.ndarray, w1: np.ndarray, w3: np.ndarray, w2: np.ndarray) ->
     return (silu(x @ w1.T) * (x @ w3.T)) @ w2.T
 
 
+# ----------------------------------------------------------------------------------------
+# fp8 activations (optional mode): per-token, per-128-channel e4m3fn with power-of-two scales
+# ----------------------------------------------------------------------------------------
+
+def round_bf16(v: np.ndarray) -> np.ndarray:
+    """Nearest bfloat16 value (8 significant bits, round half to even), as float64.  Normal
+    range only (no value here comes near bfloat16's subnormals or its overflow)."""
+    v = np.asarray(v, dtype=np.float64)
+    m, p = np.frexp(v)                      # v = m 2^p, 0.5 <= |m| < 1
+    return np.ldexp(np.rint(np.ldexp(m, 8)), p - 8)
+
+
+def round_e4m3fn(v: np.ndarray) -> np.ndarray:
+    """Nearest e4m3fn value, ties to even, for |v| <= 448 (no saturation needed), as float64.
+    Normal values 2^-6 .. 448 have 3 mantissa bits (spacing 2^(p-4) in [2^(p-1), 2^p)); below
+    2^-6 the subnormals are multiples of 2^-9."""
+    v = np.asarray(v, dtype=np.float64)
+    _, p = np.frexp(v)
+    spacing = np.ldexp(1.0, np.maximum(p - 4, -9))
+    return np.rint(v / spacing) * spacing
+
+
+def act_quant_fp8(v: np.ndarray):
+    """Quantise-dequantise rows of v [n][D] (D a multiple of 128) in 128-wide blocks: scale
+    2^e with e the smallest integer such that 448 * 2^e >= the block's largest magnitude (0 for
+    a block of zeros), values rounded to e4m3fn.  Returns (dequantised float64 [n][D], e [n][D/128])."""
+    v = np.asarray(v, dtype=np.float64)
+    n, D = v.shape
+    blocks = v.reshape(n, D // 128, 128)
+    amax = np.abs(blocks).max(axis=2)
+    m, p = np.frexp(amax)                   # amax = m 2^p; 448 = 0.875 2^9
+    e = np.where(amax > 0, p - 9 + (m > 0.875), 0).astype(np.int64)
+    scale = np.ldexp(1.0, e)[..., None]
+    q = round_e4m3fn(blocks / scale) * scale
+    return q.reshape(n, D), e
+
+
+def expert_ffn_fp8_act(x: np.ndarray, w1: np.ndarray, w3: np.ndarray, w2: np.ndarray) -> np.ndarray:
+    """SwiGLU expert with fp8 activations: [n][H] -> [n][H], float64 arithmetic."""
+    xq, _ = act_quant_fp8(x)
+    h = silu(xq @ w1.T) * (xq @ w3.T)
+    hq, _ = act_quant_fp8(round_bf16(h))
+    return hq @ w2.T
+
+
 def expert_weights(banks: dict, desc: dict, slot: int):
     """Decoded (W1, W3, W2) of the expert stored in bank row ``slot``."""
     I = desc["inter"]
@@ -260,7 +313,8 @@ def decode_x(x: np.ndarray, x_dtype: int) -> np.ndarray:
 def moe_partial(desc: dict, banks: dict, logits, slot_table, x, tokens=None):
     """Partial MoE output over cache-resident experts.
 
-    desc   : hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot
+    desc   : hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot,
+             optionally act_quant (ACT_EXACT when absent)
     banks  : w13 [n_slots][2I][H], w2 [n_slots][H][I] (float32 arrays, bf16 bit patterns as
              uint16, fp8 codes as uint8, or MXFP4 code pairs as uint8 [..][K/2]) and for fp8 s13, s2
              float32 block scales, for MXFP4 uint8 E8M0 scales [..][K/32][rows]
@@ -273,6 +327,7 @@ def moe_partial(desc: dict, banks: dict, logits, slot_table, x, tokens=None):
     T = np.asarray(logits).shape[0]
     H, k = desc["hidden"], desc["top_k"]
     want = np.ones(T, dtype=bool) if tokens is None else np.isin(np.arange(T), tokens)
+    ffn = expert_ffn_fp8_act if desc.get("act_quant", ACT_EXACT) == ACT_FP8_1X128_POW2 else expert_ffn
     acc = np.zeros((T, H), dtype=np.float64)
     # group the wanted hit pairs by expert and run each expert once over its tokens
     for e in range(desc["n_experts"]):
@@ -284,14 +339,14 @@ def moe_partial(desc: dict, banks: dict, logits, slot_table, x, tokens=None):
             continue
         ts = [p // k for p in ps]
         w1, w3, w2 = expert_weights(banks, desc, int(r["eff_slot"][e]))
-        y = expert_ffn(decode_x(x[ts], desc["x_dtype"]), w1, w3, w2)
+        y = ffn(decode_x(x[ts], desc["x_dtype"]), w1, w3, w2)
         for i, p in enumerate(ps):
             acc[p // k] += r["topk_w"][p // k, p % k] * y[i]
     if desc["shared_slot"] >= 0:
         ts = [t for t in range(T) if want[t]]
         if ts:
             w1, w3, w2 = expert_weights(banks, desc, desc["shared_slot"])
-            acc[ts] += expert_ffn(decode_x(x[ts], desc["x_dtype"]), w1, w3, w2)
+            acc[ts] += ffn(decode_x(x[ts], desc["x_dtype"]), w1, w3, w2)
     return acc.astype(np.float32), r
 
 

@@ -655,3 +655,105 @@ def test_replay_lru_top1_inclusion(seed):
          for C in range(1, E + 1)]
     assert all(a >= b for a, b in zip(m, m[1:])), m
     assert m[-1] == 0
+
+
+# ---------------------------------------------------------------------------------------------
+# fp8 activations (optional mode): the roundings against torch's own casts, the scale rule
+# against its closed form, and the expert FFN against a torch-cast reimplementation
+# ---------------------------------------------------------------------------------------------
+
+def _e4m3_grid():
+    v = oracle.E4M3FN_TABLE[:127]                      # codes 0 .. 126: +0 .. 448
+    return np.unique(v)
+
+
+def test_round_e4m3fn_matches_torch_cast():
+    grid = _e4m3_grid()
+    mids = (grid[:-1] + grid[1:]) / 2                  # every tie, float32-exact
+    rng = np.random.default_rng(11)
+    rand = rng.uniform(-448, 448, 20000)
+    tiny = rng.uniform(-2.0 ** -5, 2.0 ** -5, 5000)     # the subnormal range
+    v = np.concatenate([grid, -grid, mids, -mids, rand, tiny]).astype(np.float32).astype(np.float64)
+    ref = torch.from_numpy(v.astype(np.float32)).to(torch.float8_e4m3fn).to(torch.float64).numpy()
+    got = oracle.round_e4m3fn(v)
+    assert np.array_equal(got, ref)
+    # ties went to the even code: every midpoint landed on a grid value whose code is even
+    codes = np.searchsorted(grid, oracle.round_e4m3fn(mids))
+    assert np.all(codes % 2 == 0)
+
+
+def test_round_bf16_matches_torch_cast():
+    rng = np.random.default_rng(12)
+    v = np.concatenate([rng.standard_normal(20000) * 10.0 ** rng.integers(-6, 6, 20000),
+                        [0.0, 1.0, -1.0, 1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8]]).astype(np.float32)
+    ref = torch.from_numpy(v).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(oracle.round_bf16(v.astype(np.float64)), ref)
+
+
+def test_act_quant_scale_rule_closed_form():
+    # a block whose largest magnitude is exactly 448 * 2^k takes 2^k; a hair above takes 2^(k+1)
+    rows = []
+    expect = []
+    for k in (-12, -3, 0, 5):
+        b = np.zeros(128)
+        b[7] = -448.0 * 2.0 ** k
+        b[9] = 1.5 * 2.0 ** k
+        rows.append(b)
+        expect.append(k)
+        c = b.copy()
+        c[7] = -np.nextafter(448.0 * 2.0 ** k, np.inf)
+        rows.append(c)
+        expect.append(k + 1)
+    rows.append(np.zeros(128))
+    expect.append(0)
+    x = np.stack(rows)
+    q, e = oracle.act_quant_fp8(x)
+    assert e[:, 0].tolist() == expect
+    assert np.all(q[-1] == 0)
+    # e is the smallest integer with 448 * 2^e >= amax, by brute force
+    rng = np.random.default_rng(13)
+    y = rng.standard_normal((64, 512)) * 10.0 ** rng.integers(-4, 4, (64, 1))
+    _, e = oracle.act_quant_fp8(y)
+    amax = np.abs(y.reshape(64, 4, 128)).max(axis=2)
+    assert np.all(448.0 * 2.0 ** e >= amax) and np.all(448.0 * 2.0 ** (e - 1) < amax)
+
+
+def test_act_quant_is_idempotent_and_within_half_a_step():
+    rng = np.random.default_rng(14)
+    x = rng.standard_normal((32, 256)) * 3
+    q, e = oracle.act_quant_fp8(x)
+    q2, _ = oracle.act_quant_fp8(q)     # the values are fixed points (a block whose largest value
+    assert np.array_equal(q, q2)        # rounded down may take the next smaller scale, exactly)
+    scale = np.repeat(2.0 ** e, 128, axis=1)
+    scaled = np.abs(x) / scale
+    _, p = np.frexp(scaled)
+    step = np.ldexp(1.0, np.maximum(p - 4, -9)) * scale
+    assert np.all(np.abs(q - x) <= step / 2)
+
+
+def test_expert_ffn_fp8_act_matches_torch_cast_reimplementation():
+    """The composition Q(x) -> SwiGLU -> bf16 -> Q(h) -> W2, with torch's float8 and bfloat16
+    casts doing the roundings and the scale taken from log2 with a one-step correction."""
+    rng = np.random.default_rng(15)
+    H, I, n = 256, 384, 9
+    x = oracle.bf16_bits_to_f64((rng.standard_normal((n, H)).astype(np.float32).view(np.uint32) >> 16)
+                                .astype(np.uint16))
+    w1, w3 = rng.standard_normal((I, H)) / 16, rng.standard_normal((I, H)) / 16
+    w2 = rng.standard_normal((H, I)) / 20
+
+    def q_torch(v):
+        t = torch.from_numpy(v).reshape(v.shape[0], -1, 128)
+        amax = t.abs().amax(dim=2, keepdim=True)
+        e = torch.ceil(torch.log2(amax / 448.0))
+        e = torch.where(448.0 * torch.exp2(e - 1) >= amax, e - 1, e)   # log2 rounding slack
+        e = torch.where(amax > 0, e, torch.zeros_like(e))
+        s = torch.exp2(e)
+        return ((t / s).to(torch.float32).to(torch.float8_e4m3fn).to(torch.float64) * s).reshape(v.shape).numpy()
+
+    xq = q_torch(x)
+    z = xq @ w1.T
+    h = (z / (1 + np.exp(-z))) * (xq @ w3.T)
+    hb = torch.from_numpy(h).to(torch.bfloat16).to(torch.float64).numpy()
+    ref = q_torch(hb) @ w2.T
+    got = oracle.expert_ffn_fp8_act(x, w1, w3, w2)
+    assert np.allclose(got, ref, rtol=1e-12, atol=1e-12)
