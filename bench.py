@@ -563,18 +563,20 @@ def cpu_baseline(lay, tokens):
                       f"{t_one:.1f} s on one thread"}
 
 
-def measure_forward(config, T, n_layers, steps, warmup, hip, combine=0):
+def measure_forward(config, T, n_layers, steps, warmup, hip, combine=0, act_quant=0, layers=None):
     """Time ``steps`` back-to-back ft_moe_forward calls over ``n_layers`` rotating instances of
     ``config`` at T tokens (inputs resident in HBM), then the same steps with stage events.
     Returns the throughput, the per-stage times and the dominant kernel's roofline, and the
-    layer instances (for the CPU baseline)."""
+    layer instances (for the CPU baseline).  act_quant selects the optional fp8-activation mode;
+    ``layers`` reuses instances built by an earlier call."""
     import torch
     import paper_2608_16157_amd as ftm
     import workloads
     cfg = workloads.CONFIGS[config]
-    print(f"# building {n_layers} layer instances of {config} T={T}", file=sys.stderr, flush=True)
-    layers = [workloads.make_layer(config, T, layer=i, device="cuda") for i in range(n_layers)]
-    desc = dict(layers[0].desc(), combine=combine)
+    if layers is None:
+        print(f"# building {n_layers} layer instances of {config} T={T}", file=sys.stderr, flush=True)
+        layers = [workloads.make_layer(config, T, layer=i, device="cuda") for i in range(n_layers)]
+    desc = dict(layers[0].desc(), combine=combine, act_quant=act_quant)
     ws = ftm.alloc_workspace(desc, T)
     routes = [ftm.RouteBuffers(T, cfg.top_k, cfg.n_experts) for _ in layers]
     out = torch.empty(T, cfg.hidden, dtype=torch.float32, device="cuda")
@@ -634,8 +636,16 @@ def measure_forward(config, T, n_layers, steps, warmup, hip, combine=0):
     gu_flops = sum(w["gateup_flops"] for w in step_work) / K
     stage_avg = [sum(s[j] for s in stage_ms) / K for j in range(ftm.FT_PROF_STAGES)]
     mfma_path = T >= 256      # the library's many-token (MFMA GEMM) path
-    traffic = measured_traffic(f"{config}:T{T}")
-    if mfma_path:
+    traffic = measured_traffic(f"{config}:T{T}") if not act_quant else None
+    if mfma_path and act_quant:
+        # fp8 activations: fp8 x fp8 products on the matrix cores, against the fp8 dense peak
+        achieved = gu_flops / (gu_ms / 1e3) / 1e12
+        roof = {"kernel": "grouped gate/up GEMM, fp8 x fp8 + SiLU-mul (grouped_gemm<fp8 activations, gate/up>)",
+                "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_PEAK_TFLOPS["fp8"],
+                "unit": "TFLOP/s", "frac": round(achieved / MFMA_PEAK_TFLOPS["fp8"], 4),
+                "traffic": None, "flops_per_launch": round(gu_flops),
+                "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
+    elif mfma_path:
         # fp8 and MXFP4 weights are widened to bf16 in registers, so every contraction runs on
         # bf16 MFMA
         achieved = gu_flops / (gu_ms / 1e3) / 1e12
@@ -652,6 +662,9 @@ def measure_forward(config, T, n_layers, steps, warmup, hip, combine=0):
                 "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
     wdt = {0: "f32", 1: "bf16", 2: "fp8 e4m3 + 128x128 float32 block scales, widened exactly to bf16",
            3: "MXFP4, widened exactly to bf16"}[cfg.w_dtype]
+    if act_quant:
+        wdt = ("fp8 e4m3 + 128x128 float32 block scales, activations quantised to fp8 e4m3 per token "
+               "and 128 channels with power-of-two scales (optional mode, not the exact method)")
     res = {
         "value": round(T * K / (total_ms / 1e3), 1),
         "ms_per_step": round(ms_step, 5),
@@ -661,7 +674,8 @@ def measure_forward(config, T, n_layers, steps, warmup, hip, combine=0):
         "layer_hbm_gbps": round(layer_bytes / (ms_step / 1e3) / 1e9, 1),
         "layer_hbm_frac": round(layer_bytes / (ms_step / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
         "layer_tflops": round(layer_flops / (ms_step / 1e3) / 1e12, 2),
-        "layer_mfma_frac": round(layer_flops / (ms_step / 1e3) / 1e12 / MFMA_PEAK_TFLOPS["bf16"], 4),
+        "layer_mfma_frac": round(layer_flops / (ms_step / 1e3) / 1e12 /
+                                 MFMA_PEAK_TFLOPS["fp8" if act_quant and mfma_path else "bf16"], 4),
         "stage_ms": {"route": round(stage_avg[0], 5), "gate_up": round(stage_avg[1], 5),
                      "down": round(stage_avg[2], 5), "combine": round(stage_avg[3], 5)},
         "roofline": roof,
@@ -681,6 +695,11 @@ def main():
     ap.add_argument("--decode-extras", default="qwen3_decode:32,dsv3_decode:64",
                     help="decode points (config:T, comma-separated) timed after the headline in the "
                          "same run, reported under 'decode'; '' for none")
+    ap.add_argument("--act-quant", type=int, default=0,
+                    help="1: the optional fp8-activation mode (FT_ACT_FP8_1x128_POW2) for --config")
+    ap.add_argument("--fp8-act-extra", type=int, default=1,
+                    help="with an fp8 many-token headline, also time the fp8-activation mode on the same "
+                         "instances, reported under 'fp8_act' (0: skip)")
     ap.add_argument("--measure-bandwidths", action="store_true",
                     help="measure B_P (fills over PCIe) and B_H (CPU branch) for --config, then exit")
     ap.add_argument("--hybrid", action="store_true",
@@ -746,7 +765,8 @@ def main():
     ftm.load()
     hip = HipEvents()
     T = args.tokens
-    res, layers = measure_forward(args.config, T, args.layers, args.steps, args.warmup, hip)
+    res, layers = measure_forward(args.config, T, args.layers, args.steps, args.warmup, hip,
+                                  act_quant=args.act_quant)
     cfg = workloads.CONFIGS[args.config]
     line = {
         "metric": METRIC,
@@ -773,6 +793,14 @@ def main():
         else:   # eight tokens from each eighth of the chunk (every hot-set segment of dsv3_prefill)
             toks = sorted({i * (T // 8) + j for i in range(8) for j in range(min(8, T // 8))})
         line["cpu_baseline"] = cpu_baseline(layers[0], toks)
+    if args.fp8_act_extra and not args.act_quant and cfg.w_dtype == workloads.DT_FP8 and T >= 256:
+        # the optional fp8-activation mode on the same layer instances (not the headline: the
+        # exact mode is the paper's method)
+        ra, _ = measure_forward(args.config, T, args.layers, args.steps, args.warmup, hip,
+                                act_quant=ftm.FT_ACT_FP8_1x128_POW2, layers=layers)
+        line["fp8_act"] = {k: ra[k] for k in ("value", "ms_per_step", "workload", "layer_tflops",
+                                               "layer_mfma_frac", "stage_ms", "roofline")}
+        line["fp8_act"]["unit"] = "tokens/s"
     del layers
     torch.cuda.empty_cache()
     # decode points of the metric's other half (achieved HBM bandwidth), timed in the same run

@@ -60,6 +60,17 @@ enum { FT_GATE_SOFTMAX_TOPK_RENORM = 0, FT_GATE_SIGMOID_TOPK_RENORM = 1 };
  * (T >= 256) always adds atomically. */
 enum { FT_COMBINE_ORDERED = 0, FT_COMBINE_ATOMIC = 1 };
 
+/* Activation precision of the expert evaluation (ft_moe_desc_t.act_quant).  EXACT: the paper's
+ * weight-only dequantisation, activations in bf16.  FP8_1x128_POW2 (fp8 weights only; not the
+ * paper's exact method, a mode for the fp8 matrix cores): the expert inputs x and the SwiGLU
+ * activation h (first rounded to bf16) are quantised per token and 128-channel block to e4m3fn,
+ * with the scale 2^e, e the smallest integer such that 448 * 2^e >= the block's largest
+ * magnitude (clamped to [-127, 127]), values rounded to nearest, ties to even.  The many-token
+ * path then multiplies fp8 by fp8 on the matrix cores (activation scales in the MFMA's
+ * per-row scale operand, weight block scales on the float32 partial sums); the few-token path
+ * widens the quantised values to bf16. */
+enum { FT_ACT_EXACT = 0, FT_ACT_FP8_1x128_POW2 = 1 };
+
 enum {
     FT_DT_F32 = 0,              /* IEEE float32 */
     FT_DT_BF16 = 1,             /* bfloat16 */
@@ -94,9 +105,14 @@ enum {
  *   shared_slot: bank row of an always-resident shared expert with gate 1 for every token,
  *                or -1 for none.
  *   combine: FT_COMBINE_* (0, the ordered combine, for a zero-initialised struct).
+ *   act_quant: FT_ACT_* (0, exact, for a zero-initialised struct).  FT_ACT_FP8_1x128_POW2
+ *              requires w_dtype FT_DT_FP8E4M3FN_B128 (FT_ERR_DTYPE otherwise) and is accepted by
+ *              ft_moe_forward, ft_moe_forward_noalloc and ft_prefill_layers; ft_cpu_experts and
+ *              ft_moe_step_hybrid, whose CPU branch evaluates exactly, return FT_ERR_DTYPE.
  */
 typedef struct {
-    int32_t hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot, combine;
+    int32_t hidden, inter, n_experts, top_k, gating, w_dtype, x_dtype, n_slots, shared_slot, combine,
+        act_quant;
 } ft_moe_desc_t;
 
 /*

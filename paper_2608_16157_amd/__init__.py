@@ -39,6 +39,7 @@ LIB_PATH = os.path.join(HERE, "libftmoe.so")
 FT_OK, FT_ERR_NULL, FT_ERR_SHAPE, FT_ERR_DTYPE, FT_ERR_CAPACITY, FT_ERR_HIP = range(6)
 FT_GATE_SOFTMAX_TOPK_RENORM, FT_GATE_SIGMOID_TOPK_RENORM = 0, 1
 FT_COMBINE_ORDERED, FT_COMBINE_ATOMIC = 0, 1
+FT_ACT_EXACT, FT_ACT_FP8_1x128_POW2 = 0, 1
 FT_DT_F32, FT_DT_BF16, FT_DT_FP8E4M3FN_B128, FT_DT_MXFP4 = 0, 1, 2, 3
 FT_SLOT_MISS = -1
 FT_DEV_SLOT_RANGE, FT_DEV_SLOT_DUP, FT_DEV_SLOT_SHARED = 1, 2, 4
@@ -60,7 +61,7 @@ class FtError(RuntimeError):
 class ft_moe_desc_t(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("hidden", "inter", "n_experts", "top_k", "gating",
                                               "w_dtype", "x_dtype", "n_slots", "shared_slot",
-                                              "combine")]
+                                              "combine", "act_quant")]
 
 
 class ft_banks_t(ctypes.Structure):
@@ -279,8 +280,10 @@ def _stream(stream) -> Optional[int]:
 
 
 def make_desc(d: dict) -> ft_moe_desc_t:
-    """ft_moe_desc_t from a dict; ``combine`` defaults to FT_COMBINE_ORDERED."""
-    return ft_moe_desc_t(**{f: int(d.get(f, 0) if f == "combine" else d[f]) for f, _ in ft_moe_desc_t._fields_})
+    """ft_moe_desc_t from a dict; ``combine`` defaults to FT_COMBINE_ORDERED and ``act_quant`` to
+    FT_ACT_EXACT."""
+    return ft_moe_desc_t(**{f: int(d.get(f, 0) if f in ("combine", "act_quant") else d[f])
+                            for f, _ in ft_moe_desc_t._fields_})
 
 
 class RouteBuffers:

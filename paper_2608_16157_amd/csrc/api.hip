@@ -22,12 +22,15 @@ bool desc_ok(const ft_moe_desc_t *d) {
     if (d->n_slots < 0) return false;
     if (d->shared_slot < -1 || d->shared_slot >= d->n_slots) return false;
     if (d->combine != FT_COMBINE_ORDERED && d->combine != FT_COMBINE_ATOMIC) return false;
+    if (d->act_quant != FT_ACT_EXACT && d->act_quant != FT_ACT_FP8_1x128_POW2) return false;
     return true;
 }
 
 ft_status_t dtype_status(const ft_moe_desc_t *d) {
     if (d->gating != FT_GATE_SOFTMAX_TOPK_RENORM && d->gating != FT_GATE_SIGMOID_TOPK_RENORM)
         return FT_ERR_DTYPE;
+    if (d->act_quant == FT_ACT_FP8_1x128_POW2)
+        return d->w_dtype == FT_DT_FP8E4M3FN_B128 && d->x_dtype == FT_DT_BF16 ? FT_OK : FT_ERR_DTYPE;
     if (d->w_dtype == FT_DT_F32 && d->x_dtype == FT_DT_F32) return FT_OK;
     if ((d->w_dtype == FT_DT_BF16 || d->w_dtype == FT_DT_FP8E4M3FN_B128 || d->w_dtype == FT_DT_MXFP4) &&
         d->x_dtype == FT_DT_BF16)
@@ -51,7 +54,7 @@ ft_status_t check_common(const ft_moe_desc_t *desc, const float *logits, const i
 }
 
 WsView carve(const ft_moe_desc_t *d, int T, void *ws) {
-    const WsLayout L = ws_layout(d->n_experts, d->hidden, d->inter, d->top_k, d->w_dtype, d->combine, T);
+    const WsLayout L = ws_layout(d->n_experts, d->hidden, d->inter, d->top_k, d->w_dtype, d->combine, d->act_quant, T);
     uint8_t *b = static_cast<uint8_t *>(ws);
     WsView v;
     v.eff_slot = reinterpret_cast<int32_t *>(b + L.eff_slot);
@@ -67,6 +70,13 @@ WsView carve(const ft_moe_desc_t *d, int T, void *ws) {
     v.row_pair = reinterpret_cast<int32_t *>(b + L.row_pair);
     v.h = b + L.h;
     v.ypart = L.ypart_bytes ? reinterpret_cast<float *>(b + L.ypart) : nullptr;
+    const bool aq = d->act_quant == FT_ACT_FP8_1x128_POW2;
+    const bool gemm = gemm_shape(T, d->hidden, d->inter, d->w_dtype);
+    v.xq = aq && gemm ? b + L.xq : nullptr;
+    v.xs = aq && gemm ? b + L.xs : nullptr;
+    v.hq = aq && gemm ? b + L.hq : nullptr;
+    v.hs = aq && gemm ? b + L.hs : nullptr;
+    v.xd = aq && !gemm ? reinterpret_cast<uint16_t *>(b + L.xd) : nullptr;
     return v;
 }
 
@@ -126,7 +136,9 @@ extern "C" {
 size_t ft_moe_workspace_bytes(const ft_moe_desc_t *desc, int32_t max_tokens) {
     if (!desc_ok(desc) || max_tokens < 0) return 0;
     const int T = max_tokens > 0 ? max_tokens : 1;
-    return ws_layout(desc->n_experts, desc->hidden, desc->inter, desc->top_k, desc->w_dtype, desc->combine, T).total;
+    return ws_layout(desc->n_experts, desc->hidden, desc->inter, desc->top_k, desc->w_dtype, desc->combine,
+                     desc->act_quant, T)
+        .total;
 }
 
 ft_status_t ft_route_only(const ft_moe_desc_t *desc, const float *logits, const int32_t *slot_table,
@@ -190,6 +202,7 @@ hipError_t enqueue_experts(const ft_moe_desc_t *desc, const ft_banks_t *banks, c
     ea.w_dtype = desc->w_dtype;
     ea.n_slots = desc->n_slots;
     ea.shared = desc->shared_slot >= 0 ? 1 : 0;
+    ea.act_quant = desc->act_quant;
     const long routed_slots = desc->n_slots - ea.shared;
     long mg = desc->n_experts;
     if (routed_slots < mg) mg = routed_slots;
@@ -333,6 +346,7 @@ ft_status_t check_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_
     if (!desc || !host_pool) return FT_ERR_NULL;
     if (!desc_ok(desc)) return FT_ERR_SHAPE;
     if (ft_status_t st = dtype_status(desc); st != FT_OK) return st;
+    if (desc->act_quant != FT_ACT_EXACT) return FT_ERR_DTYPE;   // the CPU branch evaluates exactly
     if (T < 0 || n_list < 0 || n_list > desc->n_experts) return FT_ERR_SHAPE;
     if (n_list > 0 && (!host_pool->w13 || !host_pool->w2)) return FT_ERR_NULL;
     if (n_list > 0 && has_scales(desc->w_dtype) && (!host_pool->s13 || !host_pool->s2)) return FT_ERR_NULL;

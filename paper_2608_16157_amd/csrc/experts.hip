@@ -545,8 +545,16 @@ static hipError_t launch_stream_path(const ExpertArgs &a, hipStream_t s, const P
     const size_t n4 = static_cast<size_t>(a.T) * a.H / 4;
     const unsigned blocks = static_cast<unsigned>(std::min<size_t>(2048, (n4 + 255) / 256));
     if (!prof.mark(1)) return hipErrorUnknown;
-    if (a.max_groups > 0) launch_gemv<WT, EPI_GATEUP>(a, s);
+    // fp8 activations: the GEMVs read x and h quantised and widened back to bf16
+    ExpertArgs ag = a;
+    if (a.act_quant && a.max_groups > 0) {
+        if (hipError_t e = launch_act_quant_x(a, s); e != hipSuccess) return e;
+        ag.x = a.wv.xd;
+    }
+    if (a.max_groups > 0) launch_gemv<WT, EPI_GATEUP>(ag, s);
     else if (!a.wv.ypart) hipLaunchKernelGGL(zero_out, dim3(blocks), dim3(256), 0, s, a.out, n4);
+    if (a.act_quant && a.max_groups > 0)
+        if (hipError_t e = launch_act_quant_h(a, s); e != hipSuccess) return e;
     if (!prof.mark(2)) return hipErrorUnknown;
     if (a.max_groups > 0) launch_gemv<WT, EPI_DOWN>(a, s);
     if (!prof.mark(3)) return hipErrorUnknown;

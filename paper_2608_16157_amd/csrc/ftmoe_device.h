@@ -66,6 +66,37 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t v) {
     return __builtin_bit_cast(bf16x8_t, v);
 }
 
+// fp8 activations (FT_ACT_FP8_1x128_POW2).  The scale exponent of a 128-value block with largest
+// magnitude amax: the smallest e with 448 * 2^e >= amax (448 = 0.875 * 2^9), 0 for amax = 0,
+// clamped to the e8m0 range [-127, 127].
+__device__ __forceinline__ int act_scale_exp(float amax) {
+    int ex;
+    const float m = frexpf(amax, &ex);   // amax = m 2^ex, 0.5 <= m < 1
+    const int e = amax > 0.0f ? ex - 9 + (m > 0.875f ? 1 : 0) : 0;
+    return min(max(e, -127), 127);
+}
+
+// e4m3fn code nearest to v, ties to even, for |v| <= 448.  Below 2^-6 the values are the
+// multiples of 2^-9 (subnormal codes 0..7; 8 is the smallest normal, 2^-6); above, 3 mantissa
+// bits rounded from float32's 23.
+__device__ __forceinline__ uint32_t e4m3_rne(float v) {
+    const uint32_t bits = __float_as_uint(v), sign = (bits >> 24) & 0x80u;
+    const float a = fabsf(v);
+    if (a < 0.015625f) return sign | static_cast<uint32_t>(__builtin_rintf(a * 512.0f));
+    const uint32_t ab = bits & 0x7FFFFFFFu, m = ab & 0x7FFFFFu;
+    uint32_t q = m >> 20;
+    const uint32_t rem = m & 0xFFFFFu;
+    q += (rem > 0x80000u || (rem == 0x80000u && (q & 1u))) ? 1u : 0u;
+    return sign | ((((ab >> 23) - 120u) << 3) + q);   // exponent field e + 7; q = 8 carries
+}
+
+// value of an e4m3fn code (no NaN codes reach it)
+__device__ __forceinline__ float e4m3_value(uint32_t c) {
+    const uint32_t e = (c >> 3) & 15u, m = c & 7u;
+    const float v = e ? __uint_as_float(((e + 120u) << 23) | (m << 20)) : static_cast<float>(m) * 0.001953125f;
+    return (c & 0x80u) ? -v : v;
+}
+
 // ---------------------------------------------------------------- wave utilities
 // Cross-lane steps use DPP row rotations/shifts (within 16-lane rows) plus v_readlane of the
 // four row results, so no reduction goes through the LDS crossbar (ds_bpermute).

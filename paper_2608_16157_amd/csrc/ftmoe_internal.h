@@ -68,6 +68,14 @@ struct WsView {
     void *h;             // [T*k + T][I] SwiGLU activations (bf16, or f32 for f32 weights)
     float *ypart;        // streaming path: [T*k + T][H] gate-weighted expert outputs by pair
                          // index, summed per token in a fixed order by the combine (else null)
+    // fp8 activations (FT_ACT_FP8_1x128_POW2), else null.  Matrix-core path: x and h as e4m3fn
+    // codes with one e8m0 exponent byte (e + 127) per token (row) and 128-channel block.
+    // Streaming path: x quantised and widened back to bf16 (h is quantised in place).
+    uint8_t *xq;         // [T][H]
+    uint8_t *xs;         // [T][H/128]
+    uint8_t *hq;         // [T*k + T][I]
+    uint8_t *hs;         // [T*k + T][I/128]
+    uint16_t *xd;        // [T][H] bf16
 };
 
 struct RouteArgs {
@@ -86,6 +94,7 @@ struct ExpertArgs {
     const void *x;
     float *out;
     int T, H, I, k, w_dtype, n_slots, shared;
+    int act_quant;    // FT_ACT_*
     int max_groups;   // upper bound on groups, known on the host
     RouteOut ro;
     WsView wv;
@@ -93,7 +102,7 @@ struct ExpertArgs {
 
 struct WsLayout {
     size_t eff_slot, blk_hist, grp_meta, grp_slot, grp_beg, grp_len, grp_mt_off, mt_group, row_tok,
-        row_gate, row_pair, h, ypart, ypart_bytes, total;
+        row_gate, row_pair, h, ypart, ypart_bytes, xq, xs, hq, hs, xd, total;
 };
 
 // Whether a call of T tokens runs the matrix-core GEMM path (many tokens, shapes that tile);
@@ -113,7 +122,7 @@ inline size_t gemm_max_mtiles(int T, int k, int E) {
     return (rows + kGemmBM - 1) / kGemmBM + E + 1;
 }
 
-inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int combine, int T) {
+inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int combine, int act_quant, int T) {
     WsLayout L{};
     size_t o = 0;
     auto take = [&](size_t bytes) {
@@ -137,6 +146,12 @@ inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int combine, 
     L.h = take(rows * I * (w_dtype == FT_DT_F32 ? 4u : 2u));
     L.ypart_bytes = (gemm_shape(T, H, I, w_dtype) || combine != FT_COMBINE_ORDERED) ? 0 : rows * H * 4u;
     L.ypart = take(L.ypart_bytes);
+    const bool aq = act_quant == FT_ACT_FP8_1x128_POW2, gemm = gemm_shape(T, H, I, w_dtype);
+    L.xq = take(aq && gemm ? static_cast<size_t>(T) * H : 0);
+    L.xs = take(aq && gemm ? static_cast<size_t>(T) * (H / 128) : 0);
+    L.hq = take(aq && gemm ? rows * I : 0);
+    L.hs = take(aq && gemm ? rows * (I / 128) : 0);
+    L.xd = take(aq && !gemm ? static_cast<size_t>(T) * H * 2 : 0);
 
     L.total = o;
     return L;
@@ -285,5 +300,9 @@ hipError_t launch_route(const RouteArgs &a, hipStream_t s);
 hipError_t launch_cache_plan(const PlanArgs &a, hipStream_t s);
 hipError_t launch_experts(const ExpertArgs &a, hipStream_t s, const Prof &prof);
 hipError_t launch_gemm(const ExpertArgs &a, hipStream_t s, const Prof &prof);
+// fp8 activations (quant.hip): x into codes and exponents (matrix-core path) or into quantised
+// bf16 (streaming path); h quantised in place (streaming path)
+hipError_t launch_act_quant_x(const ExpertArgs &a, hipStream_t s);
+hipError_t launch_act_quant_h(const ExpertArgs &a, hipStream_t s);
 
 }  // namespace ftmoe

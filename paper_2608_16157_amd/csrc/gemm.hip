@@ -96,6 +96,9 @@ enum { GEMM_GATEUP = 0, GEMM_DOWN = 1 };
 #ifndef FT_GEMM_FP8_NS
 #define FT_GEMM_FP8_NS 2
 #endif
+// Internal weight-format code of fp8 weights with fp8 activations (FT_ACT_FP8_1x128_POW2): fp8 x
+// fp8 products on the scaled 32x32x64 MFMA.
+constexpr int kWtFp8Act = 16;
 template <int WT> struct GTr;
 // CHUNK_GU, CHUNK_DN: workgroups per launch of the gate/up and the down GEMM (see launch_tiles).
 // SKIP_PAD_GU: gate/up tiles skip the MFMAs of 32-row sub-tiles that hold only padding rows.  The
@@ -103,20 +106,42 @@ template <int WT> struct GTr;
 // (measured 2.58 against 2.70 ms at DeepSeek-V3 prefill; the other kernels lost 2-5 % without it).
 template <> struct GTr<FT_DT_BF16> {
     static constexpr int BK = FT_GEMM_BF16_BK, NS = FT_GEMM_BF16_NS, BRB = 2 * BK;
+    static constexpr int OCC_GU = kGemmOcc, OCC_DN = kGemmOcc, NS_GU = NS, NS_DN = NS;
     static constexpr long CHUNK_GU = 768, CHUNK_DN = 1024;
-    static constexpr bool SKIP_PAD_GU = true;
+    static constexpr bool SKIP_PAD_GU = true, SKIP_PAD_DN = true;
 };
 template <> struct GTr<FT_DT_FP8E4M3FN_B128> {
     static constexpr int BK = FT_GEMM_FP8_BK, NS = FT_GEMM_FP8_NS, BRB = BK;
+    static constexpr int OCC_GU = kGemmOcc, OCC_DN = kGemmOcc, NS_GU = NS, NS_DN = NS;
     static constexpr long CHUNK_GU = 512, CHUNK_DN = 1536;
-    static constexpr bool SKIP_PAD_GU = false;
+    static constexpr bool SKIP_PAD_GU = false, SKIP_PAD_DN = true;
+};
+// fp8 weights and fp8 activations: 64 K values per stage (one 32x32x64 MFMA step); one workgroup
+// per CU, whose 512 registers a lane hold the 32-byte operands of two steps beside the
+// accumulators, with a four-stage ring
+#ifndef FT_GEMM_AQ_OCC_GU
+#define FT_GEMM_AQ_OCC_GU 2
+#endif
+#ifndef FT_GEMM_AQ_OCC_DN
+#define FT_GEMM_AQ_OCC_DN 2
+#endif
+#ifndef FT_GEMM_AQ_SKIP_DN
+#define FT_GEMM_AQ_SKIP_DN false
+#endif
+template <> struct GTr<kWtFp8Act> {
+    static constexpr int BK = 64, BRB = BK;
+    static constexpr int OCC_GU = FT_GEMM_AQ_OCC_GU, OCC_DN = FT_GEMM_AQ_OCC_DN;
+    static constexpr int NS_GU = OCC_GU == 2 ? 2 : 4, NS_DN = OCC_DN == 2 ? 2 : 4;
+    static constexpr long CHUNK_GU = 256 * OCC_GU, CHUNK_DN = 768 * OCC_DN;
+    static constexpr bool SKIP_PAD_GU = false, SKIP_PAD_DN = FT_GEMM_AQ_SKIP_DN;
 };
 // MXFP4: 64 K values (32 code bytes) per weight row and stage, so that one lane's 16-byte chunk
 // of a row is a whole 32-value scale run
 template <> struct GTr<FT_DT_MXFP4> {
     static constexpr int BK = 64, NS = 3, BRB = BK / 2;
+    static constexpr int OCC_GU = kGemmOcc, OCC_DN = kGemmOcc, NS_GU = NS, NS_DN = NS;
     static constexpr long CHUNK_GU = 512, CHUNK_DN = 1536;
-    static constexpr bool SKIP_PAD_GU = true;
+    static constexpr bool SKIP_PAD_GU = true, SKIP_PAD_DN = true;
 };
 
 template <int V> using ic = std::integral_constant<int, V>;
@@ -172,6 +197,12 @@ __device__ __forceinline__ int swz(int r, int c) {
     else return c ^ ((r >> 3) & 1);
 }
 
+typedef int i32x8_t __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ i32x8_t cat_u32x8(u32x4_t lo, u32x4_t hi) {
+    return i32x8_t{static_cast<int>(lo[0]), static_cast<int>(lo[1]), static_cast<int>(lo[2]), static_cast<int>(lo[3]),
+                   static_cast<int>(hi[0]), static_cast<int>(hi[1]), static_cast<int>(hi[2]), static_cast<int>(hi[3])};
+}
+
 __device__ __forceinline__ void dma16(const void *g, uint8_t *lds_block) {
     __builtin_amdgcn_global_load_lds(g, (lds_void_t *)(lds_block), 16, 0, 0);
 }
@@ -182,11 +213,14 @@ __device__ __forceinline__ void dma4(const void *g, uint8_t *lds_block) {
 }
 
 template <int WT, int EPI>
-__global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArgs a, int ntn, int base) {
-    constexpr bool kFp8 = WT == FT_DT_FP8E4M3FN_B128;
+__global__ __launch_bounds__(kGemmThreads, EPI == GEMM_GATEUP ? GTr<WT>::OCC_GU : GTr<WT>::OCC_DN) void grouped_gemm(
+    ExpertArgs a, int ntn, int base) {
+    constexpr bool kAq = WT == kWtFp8Act;                          // fp8 activations (fp8 x fp8 MFMA)
+    constexpr bool kFp8 = WT == FT_DT_FP8E4M3FN_B128 || kAq;        // fp8 weights with block scales
+    constexpr bool kWiden8 = WT == FT_DT_FP8E4M3FN_B128;            // fp8 weights widened to bf16
     constexpr bool kFp4 = WT == FT_DT_MXFP4;
-    constexpr int BK = GTr<WT>::BK, NS = GTr<WT>::NS;
-    constexpr int ARB = BK * 2;                      // A row bytes per stage (bf16)
+    constexpr int BK = GTr<WT>::BK, NS = EPI == GEMM_GATEUP ? GTr<WT>::NS_GU : GTr<WT>::NS_DN;
+    constexpr int ARB = kAq ? BK : BK * 2;           // A row bytes per stage (bf16, or fp8 codes)
     constexpr int BRB = GTr<WT>::BRB;                // B row bytes per stage
     constexpr int ASTAGE = kBM * ARB, BSTAGE = kBN * BRB;
     constexpr int A_INSTR = ASTAGE / 1024 / kGemmWaves;   // 1 KB DMA instructions per wave
@@ -198,6 +232,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     static_assert(NS >= 2 && NS <= 4, "ring depth");
     static_assert(NS * PER_STAGE < 64, "vmcnt range");
     static_assert(!kFp8 || 128 % BK == 0, "an fp8 K stage lies in one scale block");
+    static_assert(!kAq || (BK % 64 == 0 && kWavesM == 1), "fp8 activations: 64-K MFMA steps, 4 waves");
     // stages unrolled per main-loop turn: whole ring turns and, for fp8, whole 128-wide K blocks
     constexpr int kStagesPerKb = kFp8 ? 128 / BK : 1;
     constexpr int kUnit = NS / gcd_c(NS, kStagesPerKb) * kStagesPerKb;   // lcm
@@ -221,6 +256,11 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     __shared__ int32_t s_zeroblk[kWavesN];   // fp8: a column group's scales hold a 0
     __shared__ int32_t s_tok[kBM];
     __shared__ float s_gate[kBM];
+    // fp8 activations: e8m0 scale byte of each tile row and K block, and (gate/up epilogue) the
+    // per-wave largest |h| of each row and the rows' h exponents
+    __shared__ uint8_t s_ascale[kAq ? kBM * kMaxKb : 1];
+    __shared__ float s_hmax[kAq ? kWavesN : 1][kAq ? kBM : 1];
+    __shared__ int32_t s_hexp[kAq ? kBM : 1];
     auto stA = [&](auto s) -> uint8_t * {
         constexpr int S = decltype(s)::value;
         if constexpr (S == 0) return sA0;
@@ -282,10 +322,12 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         const int row = (wave * A_INSTR + ii) * A_ROWS + lane / A_CHUNKS;
         const int r = min(len - 1, m0 + row);      // padding rows repeat the last row; never stored
         const uint8_t *rowp;
+        constexpr size_t EB = kAq ? 1 : 2;   // bytes per activation element
         if constexpr (EPI == GEMM_GATEUP)
-            rowp = static_cast<const uint8_t *>(a.x) + static_cast<size_t>(a.wv.row_tok[beg + r]) * H * 2;
+            rowp = (kAq ? a.wv.xq : static_cast<const uint8_t *>(a.x)) +
+                   static_cast<size_t>(a.wv.row_tok[beg + r]) * H * EB;
         else
-            rowp = static_cast<const uint8_t *>(a.wv.h) + static_cast<size_t>(beg + r) * I * 2;
+            rowp = (kAq ? a.wv.hq : static_cast<const uint8_t *>(a.wv.h)) + static_cast<size_t>(beg + r) * I * EB;
         asrc[ii] = rowp + (swz<ARB>(row, lane % A_CHUNKS) << 4);
     }
     // B tile row -> weight row.  gate/up: wave n's 64 rows are the 32 gate rows of h columns
@@ -379,6 +421,17 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
             if (lane == 0) s_zeroblk[wn] = zero != 0;
         }
     }
+    // fp8 activations: each tile row's exponent byte of every K block (rows of x by token, rows
+    // of h by position), staged like the weight scales before the pipeline starts
+    if constexpr (kAq) {
+        const uint8_t *src = EPI == GEMM_GATEUP ? a.wv.xs : a.wv.hs;
+        for (int idx = t; idx < kBM * nkb; idx += kGemmThreads) {
+            const int r = idx / nkb, kb = idx - r * nkb;
+            const int rr = min(len - 1, m0 + r);
+            const size_t srow = EPI == GEMM_GATEUP ? static_cast<size_t>(a.wv.row_tok[beg + rr]) : static_cast<size_t>(beg + rr);
+            s_ascale[r * kMaxKb + kb] = src[srow * nkb + kb];
+        }
+    }
     // token and gate of each row of the tile (down projection epilogue)
     if constexpr (EPI == GEMM_DOWN) {
         for (int i = t; i < kBM; i += kGemmThreads) {
@@ -397,7 +450,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         for (int j = 0; j < kNJ; ++j) acc[i][j] = floatx16_t{};
 
     const int nk = K / BK;
-    constexpr int KS = BK / 16;   // MFMA sub-steps per K stage
+    constexpr int KS = kAq ? BK / 64 : BK / 16;   // MFMA sub-steps per K stage
     // Operands of one 32x32x16 MFMA sub-step.  The lane (r = lane % 32, kg = lane / 32) holds 8 K
     // values of row r for each operand; which 8 is free as long as A and B agree.  bf16 weights:
     // sub-step ks takes K [16 ks + 8 kg, +8), i.e. 16-byte chunk 2 ks + kg of both rows.  fp8
@@ -407,9 +460,15 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     // K values under one scale, for all four sub-steps, so sub-step ks takes K [32 kg + 8 ks, +8):
     // word ks of the chunk, activation chunk 4 kg + ks.  Weight chunks and scales are carried
     // over from the sub-step that read them.
+    // fp8 activations: lane (r, kg) holds bytes [32 kg, 32 kg + 32) of the stage's 64-byte row r
+    // for both operands (chunks 2 kg and 2 kg + 1; the MFMA pairs the same byte slots of A and
+    // B), and its row's exponent byte for the K block.
     struct Frag {
         u32x4_t a[kMI];
         u32x4_t b[kNJ];
+        u32x4_t a2[kAq ? kMI : 1];   // fp8 activations: second 16 bytes of each operand
+        u32x4_t b2[kAq ? kNJ : 1];
+        uint32_t as[kAq ? kMI : 1];  // fp8 activations: e8m0 scale byte of the lane's row
         uint32_t xb[kNJ];   // MXFP4 e8m0 scale byte of each column tile
         float sc[2];        // fp8: accumulator factor of this K block, gate (or down) and up half
         uint32_t keep[2];   // fp8: code mask of this K block (0 for a block with scale 0)
@@ -420,7 +479,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         constexpr bool ZS = decltype(zs)::value;
         const uint8_t *A = stA(rs);
         const uint8_t *B = stB(rs);
-        const int ca = kFp8 ? 4 * (KSI / 2) + 2 * fq + (KSI % 2) : (kFp4 ? 4 * fq + KSI : 2 * KSI + fq);
+        const int ca = kWiden8 ? 4 * (KSI / 2) + 2 * fq + (KSI % 2) : (kFp4 ? 4 * fq + KSI : 2 * KSI + fq);
         if constexpr (kFp8) {
             if constexpr (KSI == 0) {
                 const int kb = (kt * BK) / 128;
@@ -442,7 +501,14 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
 #pragma unroll
         for (int i = 0; i < ML; ++i) {
             const int ra = wm * kWaveRows + i * 32 + fn;
-            f.a[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, ca) << 4));
+            if constexpr (kAq) {
+                f.a[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, 4 * KSI + 2 * fq) << 4));
+                f.a2[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, 4 * KSI + 2 * fq + 1) << 4));
+                if constexpr (KSI == 0) f.as[i] = s_ascale[ra * kMaxKb + (kt * BK) / 128];
+                else f.as[i] = prev.as[i];
+            } else {
+                f.a[i] = *reinterpret_cast<const u32x4_t *>(A + ra * ARB + (swz<ARB>(ra, ca) << 4));
+            }
         }
 #pragma unroll
         for (int j = 0; j < kNJ; ++j) {
@@ -454,6 +520,17 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
                 } else {
                     f.b[j] = prev.b[j];
                     f.xb[j] = prev.xb[j];
+                }
+            } else if constexpr (kAq) {
+                f.b[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, 4 * KSI + 2 * fq) << 4));
+                f.b2[j] = *reinterpret_cast<const u32x4_t *>(B + rb * BRB + (swz<BRB>(rb, 4 * KSI + 2 * fq + 1) << 4));
+                if constexpr (ZS) {
+                    const uint32_t keep = (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.keep[1] : f.keep[0];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        f.b[j][q] &= keep;
+                        f.b2[j][q] &= keep;
+                    }
                 }
             } else if constexpr (kFp8) {
                 if constexpr (KSI % 2 == 0) {
@@ -481,7 +558,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
         for (int j = 0; j < kNJ; ++j) {
             if constexpr (kFp4) {
                 bf[j] = fp4x8_scaled_to_bf16x8(f.b[j][KSI], fp4_scale_operand(f.xb[j]));
-            } else if constexpr (kFp8) {
+            } else if constexpr (kWiden8) {
                 bf[j] = KSI % 2 == 0 ? fp8x8_to_bf16x8(f.b[j][0], f.b[j][1]) : fp8x8_to_bf16x8(f.b[j][2], f.b[j][3]);
             } else {
                 bf[j] = f.b[j];
@@ -494,8 +571,13 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
 #pragma unroll
             for (int j = 0; j < kNJ; ++j) {
                 if constexpr (kFp8 && RS) acc[i][j] *= (EPI == GEMM_GATEUP && j >= kNJ / 2) ? f.sc[1] : f.sc[0];
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(f.a[i]), as_bf16x8(bf[j]), acc[i][j], 0,
-                                                                     0, 0);
+                if constexpr (kAq)   // formats 0 (fp8 e4m3) for both; B's scale byte 127 (1.0)
+                    acc[i][j] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                        cat_u32x8(f.a[i], f.a2[i]), cat_u32x8(f.b[j], f.b2[j]), acc[i][j], 0, 0, 0,
+                        static_cast<int>(f.as[i]), 0, 127);
+                else
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(f.a[i]), as_bf16x8(bf[j]),
+                                                                         acc[i][j], 0, 0, 0);
             }
     };
 
@@ -516,15 +598,15 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     auto interleave = [&](auto ks2, auto ml, auto zs, auto rsv) {
         constexpr int K2 = decltype(ks2)::value, ML = decltype(ml)::value;
         constexpr bool ZS = decltype(zs)::value, RSV = decltype(rsv)::value;
-        constexpr bool kReadsB = kFp4 ? K2 == 0 : (kFp8 ? K2 % 2 == 0 : true);
-        constexpr int kReads = ML + (kReadsB ? kNJ : 0) + (kFp4 && K2 == 0 ? kNJ : 0) +
-                               (kFp8 && K2 == 0 ? (ZS ? 4 : 2) : 0);
+        constexpr bool kReadsB = kFp4 ? K2 == 0 : (kWiden8 ? K2 % 2 == 0 : true);
+        constexpr int kReads = (kAq ? (K2 == 0 ? 3 : 2) * ML : ML) + (kReadsB ? (kAq ? 2 : 1) * kNJ : 0) +
+                               (kFp4 && K2 == 0 ? kNJ : 0) + (kFp8 && K2 == 0 ? (ZS ? 4 : 2) : 0);
         constexpr int kMfma = ML * kNJ;
         constexpr int kPairs = kReads < kMfma ? kReads : kMfma;
         if constexpr (RSV) {
             static_for<0, kMfma>([&](auto q) {
                 constexpr int Q = decltype(q)::value;
-                __builtin_amdgcn_sched_group_barrier(0x002, Q == 0 ? 16 + 4 * kNJ : 16, 0);   // VALU
+                __builtin_amdgcn_sched_group_barrier(0x002, Q == 0 && kWiden8 ? 16 + 4 * kNJ : 16, 0);   // VALU
                 __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                           // one MFMA
                 if constexpr (Q < kReads) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // one LDS read
             });
@@ -592,7 +674,7 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
     // one main loop per live sub-tile count (in steps of MLQ sub-tiles for tall tiles)
     constexpr int MLQ = kMI > 4 ? 2 : 1;
     const int wrows = min(max(len - m0 - wm * kWaveRows, 0), kWaveRows);   // real rows of this wave
-    constexpr bool kSkipPad = EPI == GEMM_DOWN || GTr<WT>::SKIP_PAD_GU;
+    constexpr bool kSkipPad = EPI == GEMM_DOWN ? GTr<WT>::SKIP_PAD_DN : GTr<WT>::SKIP_PAD_GU;
     const int mlive = kSkipPad ? __builtin_amdgcn_readfirstlane((wrows + 32 * MLQ - 1) / (32 * MLQ) * MLQ)
                                : (wrows > 0 || kWavesM == 1 ? kMI : 0);
     // (a wave of a tall tile may hold no real rows; it still moves its share of the stages)
@@ -619,7 +701,48 @@ __global__ __launch_bounds__(kGemmThreads, kGemmOcc) void grouped_gemm(ExpertArg
 
     // ---- epilogue: element e of a 32 x 32 tile in lane (fn, fq) is row 8 (e / 4) + 4 fq + e % 4,
     // column fn
-    if constexpr (EPI == GEMM_GATEUP) {
+    if constexpr (EPI == GEMM_GATEUP && kAq) {
+        // fp8 activations: h = silu(gate) * up rounded to bf16, then quantised per row over the
+        // tile's 128 h columns (one 128-channel block): the row's largest |h| over the 4 waves'
+        // 32 columns each, its exponent, e4m3fn codes into hq and the exponent byte into hs.
+        // A lane holds column fn of rows 8 (e / 4) + 4 fq + e % 4 of each 32-row sub-tile i.
+        const int nbh = I / 128;
+#pragma unroll
+        for (int i = 0; i < kMI; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const float hv = bf16_to_f32(f32_to_bf16(silu_f32(acc[i][0][e]) * acc[i][1][e]));
+                acc[i][0][e] = hv;
+                // largest |h| of the row over the 32 lanes of this half-wave
+                uint32_t m = __float_as_uint(fabsf(hv));
+                m = max(m, dpp_u32<kDppRowRor1>(m));
+                m = max(m, dpp_u32<kDppRowRor2>(m));
+                m = max(m, dpp_u32<kDppRowRor4>(m));
+                m = max(m, dpp_u32<kDppRowRor8>(m));
+                m = max(m, static_cast<uint32_t>(__shfl_xor(static_cast<int>(m), 16)));
+                if (fn == 0) s_hmax[wn][i * 32 + (e >> 2) * 8 + 4 * fq + (e & 3)] = __uint_as_float(m);
+            }
+        __syncthreads();
+        if (t < kBM) {
+            float m = s_hmax[0][t];
+#pragma unroll
+            for (int w = 1; w < kWavesN; ++w) m = fmaxf(m, s_hmax[w][t]);
+            const int ex = act_scale_exp(m);
+            s_hexp[t] = ex;
+            if (m0 + t < len) a.wv.hs[static_cast<size_t>(beg + m0 + t) * nbh + nt] = static_cast<uint8_t>(ex + 127);
+        }
+        __syncthreads();
+        const int col0 = nt * (kBN / 2) + wn * (kWaveCols / 2) + fn;
+#pragma unroll
+        for (int i = 0; i < kMI; ++i)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int rl = i * 32 + (e >> 2) * 8 + 4 * fq + (e & 3);
+                if (m0 + rl < len)
+                    a.wv.hq[static_cast<size_t>(beg + m0 + rl) * I + col0] =
+                        static_cast<uint8_t>(e4m3_rne(ldexpf(acc[i][0][e], -s_hexp[rl])));
+            }
+    } else if constexpr (EPI == GEMM_GATEUP) {
         uint16_t *hout = static_cast<uint16_t *>(a.wv.h);
         const int col0 = nt * (kBN / 2) + wn * (kWaveCols / 2) + fn;
 #pragma unroll
@@ -679,6 +802,8 @@ template <int WT>
 static hipError_t launch_gemm_wt(const ExpertArgs &a, hipStream_t s, const Prof &prof) {
     const long mtiles = max_mtiles(a);
     if (!prof.mark(1)) return hipErrorUnknown;
+    if constexpr (WT == kWtFp8Act)   // x into e4m3fn codes and exponents
+        if (hipError_t e = launch_act_quant_x(a, s); e != hipSuccess) return e;
     const int ntn_gu = a.I / (kBN / 2);
     launch_tiles<WT, GEMM_GATEUP>(a, s, mtiles * ntn_gu, ntn_gu);
     if (!prof.mark(2)) return hipErrorUnknown;
@@ -689,6 +814,7 @@ static hipError_t launch_gemm_wt(const ExpertArgs &a, hipStream_t s, const Prof 
 }
 
 hipError_t launch_gemm(const ExpertArgs &a, hipStream_t s, const Prof &prof) {
+    if (a.act_quant) return launch_gemm_wt<kWtFp8Act>(a, s, prof);
     if (a.w_dtype == FT_DT_BF16) return launch_gemm_wt<FT_DT_BF16>(a, s, prof);
     if (a.w_dtype == FT_DT_MXFP4) return launch_gemm_wt<FT_DT_MXFP4>(a, s, prof);
     return launch_gemm_wt<FT_DT_FP8E4M3FN_B128>(a, s, prof);

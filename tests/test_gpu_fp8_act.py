@@ -1,0 +1,146 @@
+"""GPU parity of the optional fp8-activation mode (FT_ACT_FP8_1x128_POW2) against the oracle's
+same mode: x and h quantised per token and 128-channel block to e4m3fn with power-of-two scales.
+The streaming path (T < 256) widens the quantised values to bf16, the matrix-core path multiplies
+fp8 by fp8.  Lists bit-exact.
+
+Outputs: quantisation turns small arithmetic differences into whole-step differences.  The fp8
+matrix cores add the 64 products of one instruction in a narrower adder than float32: measured
+on the probe sum 256 + 63 * 2^-6, they return 256.875 for 256.984 (4e-4 relative), whereas the
+oracle works in float64.  Where the two values of h lie on either side of a bfloat16 or e4m3fn
+rounding boundary, that element of the quantised h differs by one e4m3fn step (measured: 0.16 %
+of the h elements of a 300-token layer).  Each such step moves its token's output by a fraction of
+a percent of the row's RMS.  The bound: every element within 1e-1 (row-RMS floor), every row
+within 3e-2 normwise, and at least 90 % of the rows within 1e-2 elementwise.  The streaming path
+(bf16 matrix cores, float32 accumulation) meets 1e-4 in practice."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2608_16157_amd as ftm
+import workloads
+from tests._util import oracle_inputs
+from tests.test_gpu_parity import check_route, tile_covering_tokens
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def check_output_aq(out, ref, rows=None):
+    got = out.cpu().numpy()
+    if rows is not None:
+        got, ref = got[rows], ref[rows]
+    assert np.isfinite(got).all()
+    zero = ~ref.any(axis=1)
+    assert not got[zero].any(), "rows without hits must be exactly zero"
+    floor = np.sqrt((ref.astype(np.float64) ** 2).mean(axis=1, keepdims=True))
+    el = np.abs(got - ref) / np.maximum(np.abs(ref), floor)
+    el[zero] = 0
+    nz = ~zero
+    norm = np.zeros(len(ref))
+    norm[nz] = np.linalg.norm(got[nz] - ref[nz], axis=1) / np.linalg.norm(ref[nz], axis=1)
+    row_max = el.max(axis=1)
+    frac = np.mean(row_max[nz] <= 1e-2) if nz.any() else 1.0
+    _say(f"   max_rel_err={el.max():.3e} median={np.median(el[nz]) if nz.any() else 0:.1e} "
+         f"worst row normwise={norm.max():.3e} rows within 1e-2={frac:.4f}")
+    assert el.max() <= 1e-1
+    assert norm.max() <= 3e-2
+    assert frac >= 0.90
+
+
+def run_forward_aq(lay, T=None):
+    T = lay.tokens if T is None else T
+    desc = dict(lay.desc(), act_quant=ftm.FT_ACT_FP8_1x128_POW2)
+    ws = ftm.alloc_workspace(desc, T)
+    route = ftm.RouteBuffers(T, lay.top_k, lay.n_experts)
+    out = torch.full((T, lay.hidden), float("nan"), dtype=torch.float32, device="cuda")
+    ftm.ft_moe_forward(desc, ftm.banks_of(lay), lay.logits, lay.slot_table, lay.x, T, out, route, ws)
+    torch.cuda.synchronize()
+    return out, route
+
+
+def oracle_aq(lay, tokens=None):
+    inp = list(oracle_inputs(lay))
+    inp[0] = dict(inp[0], act_quant=oracle.ACT_FP8_1X128_POW2)
+    return oracle.moe_partial(*inp, tokens=tokens)
+
+
+CASES = [
+    # seed, gating, E, k, T, n_res, shared, H, I, zipf
+    (0, 1, 32, 8, 1, 9, True, 384, 256, 0.0),       # streaming, one token
+    (1, 0, 12, 3, 20, 12, False, 256, 384, 0.0),    # streaming, narrow items
+    (2, 1, 8, 4, 60, 8, True, 256, 256, 0.0),       # streaming, wide gate/up items
+    (3, 0, 16, 4, 130, 10, True, 512, 384, 0.5),    # streaming, several M tiles a pass
+    (4, 1, 24, 6, 300, 10, True, 256, 256, 1.0),    # matrix cores, ragged groups
+    (5, 0, 32, 8, 520, 13, True, 512, 384, 2.0),    # matrix cores, skewed
+    (6, 1, 16, 4, 2900, 12, True, 256, 256, 3.0),   # matrix cores, groups over 1024 rows
+    (7, 0, 16, 4, 400, 0, False, 256, 256, 0.0),    # nothing resident: output exactly zero
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[str(c[0]) for c in CASES])
+def test_fp8_act_random_shapes(case):
+    seed, gating, E, k, T, n_res, shared, H, I, zipf = case
+    _say(f"fp8 activations {case}")
+    lay = workloads.random_layer(100 + seed, hidden=H, inter=I, n_experts=E, top_k=k, tokens=T,
+                                 gating=gating, w_dtype=workloads.DT_FP8, n_resident=n_res,
+                                 shared=shared, zipf_s=zipf, device="cuda")
+    out, route = run_forward_aq(lay)
+    ref, r = oracle_aq(lay)
+    check_route(route, r, T, k)
+    check_output_aq(out, ref)
+    if n_res == 0 and not shared:
+        assert not out.any()
+
+
+@pytest.mark.parametrize("T", [20, 300])
+def test_fp8_act_zero_block_scales(T):
+    lay = workloads.random_layer(150 + T, hidden=512, inter=384, n_experts=8, top_k=3, tokens=T,
+                                 w_dtype=workloads.DT_FP8, gating=1, n_resident=8, shared=True,
+                                 device="cuda")
+    lay.s13[0, :, 0] = 0
+    lay.s13[3] = 0
+    lay.s2[4, 2, :] = 0
+    _say(f"fp8 activations, zero block scales, T={T}")
+    out, route = run_forward_aq(lay)
+    ref, r = oracle_aq(lay)
+    check_route(route, r, T, lay.top_k)
+    check_output_aq(out, ref)
+
+
+@pytest.mark.parametrize("name,T", [("dsv3_decode", 16), ("dsv3_decode", 64)])
+def test_fp8_act_decode_configs_full(name, T):
+    _say(f"fp8 activations {name} T={T}")
+    lay = workloads.make_layer(name, T, device="cuda")
+    out, route = run_forward_aq(lay)
+    ref, r = oracle_aq(lay)
+    check_route(route, r, T, lay.top_k)
+    check_output_aq(out, ref)
+
+
+def test_fp8_act_prefill_tile_covering():
+    name, T = "dsv3_prefill", 8192
+    lay = workloads.make_layer(name, T, device="cuda")
+    out, route = run_forward_aq(lay)
+    inp = oracle_inputs(lay)
+    r = oracle.route(inp[0], inp[2], inp[3])
+    rows = tile_covering_tokens(r, T, lay.top_k, lay.shared_slot >= 0)
+    _say(f"fp8 activations {name} T={T}: {len(rows)} tile-covering rows")
+    ref, r2 = oracle_aq(lay, tokens=rows)
+    check_route(route, r2, T, lay.top_k)
+    check_output_aq(out, ref, rows=rows)
+
+
+def test_fp8_act_rejected_without_fp8_weights():
+    lay = workloads.random_layer(7, hidden=128, inter=128, n_experts=8, top_k=2, tokens=4,
+                                 w_dtype=workloads.DT_BF16, n_resident=4, device="cuda")
+    desc = dict(lay.desc(), act_quant=ftm.FT_ACT_FP8_1x128_POW2)
+    assert ftm.load().ft_moe_workspace_bytes(ftm.make_desc(desc), 4) > 0
+    ws = torch.zeros(1 << 20, dtype=torch.uint8, device="cuda")
+    route = ftm.RouteBuffers(4, 2, 8)
+    out = torch.zeros(4, 128, device="cuda")
+    with pytest.raises(ftm.FtError):
+        ftm.ft_moe_forward(desc, ftm.banks_of(lay), lay.logits, lay.slot_table, lay.x, 4, out, route, ws)
