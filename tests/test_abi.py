@@ -275,3 +275,23 @@ def test_binding_rejects_host_tensors_and_bad_sizes_before_the_call():
                            torch.zeros(T, H))
     assert ftm.expert_bank_bytes(dict(d, w_dtype=ftm.FT_DT_FP8E4M3FN_B128, hidden=256, inter=128)) == \
         (2 * 128 * 256, 256 * 128, 2 * 2 * 4, 2 * 1 * 4)
+
+
+def test_act_quant_validation():
+    """The fp8-activation mode: unknown values make the description invalid, non-fp8 weights
+    are refused as a dtype error, the CPU branch (which evaluates exactly) refuses the mode, and
+    the matrix-core path's workspace grows by the codes and exponents of x and h."""
+    lib = ftm.load()
+    fp8 = _desc(w_dtype=2, x_dtype=1, hidden=256, inter=256)
+    assert lib.ft_moe_workspace_bytes(ctypes.byref(ftm.make_desc(dict(fp8, act_quant=2))), 8) == 0
+    for T in (8, 300):
+        exact = lib.ft_moe_workspace_bytes(ctypes.byref(ftm.make_desc(fp8)), T)
+        aq = lib.ft_moe_workspace_bytes(ctypes.byref(ftm.make_desc(dict(fp8, act_quant=1))), T)
+        assert aq > exact
+    d = ftm.make_desc(dict(fp8, act_quant=1))
+    pool = ftm.ft_banks_t(FAKE, FAKE, FAKE, FAKE)
+    assert lib.ft_cpu_experts(ctypes.byref(d), ctypes.byref(pool), FAKE, 1, FAKE, FAKE, FAKE, 1, FAKE,
+                              None) == ftm.FT_ERR_DTYPE
+    bf = ftm.make_desc(_desc(w_dtype=1, x_dtype=1, act_quant=1))
+    r = ftm.ft_route_t(*[FAKE] * 8)
+    assert lib.ft_route_only(ctypes.byref(bf), FAKE, FAKE, 4, ctypes.byref(r), FAKE, 1 << 30, None) == ftm.FT_ERR_DTYPE
