@@ -217,9 +217,10 @@ ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, c
  * GPU holds from the library's load until the process ends; the call itself allocates and frees
  * nothing.  Every argument and every result is as for ft_moe_forward.
  *   Returns FT_ERR_CAPACITY, before enqueuing anything, when ft_moe_workspace_bytes(desc, T)
- *   exceeds FT_NOALLOC_SCRATCH_BYTES (e.g. 64 MiB holds a Qwen3-30B-A3B-shaped layer up to 4096
- *   tokens, and a DeepSeek-V3-shaped one up to 1811 tokens except 228..255 with the ordered
- *   combine, whose per-pair outputs take T*(k+1)*H*4 bytes).  FT_ERR_HIP if the array's device address
+ *   exceeds FT_NOALLOC_SCRATCH_BYTES (e.g. 64 MiB holds a Qwen3-30B-A3B-shaped layer up to 4805
+ *   tokens, and a DeepSeek-V3-shaped one up to 1811 tokens, 2583 with FT_ACT_FP8_1x128_POW2,
+ *   except 228..255, 217..255 with FT_ACT_FP8_1x128_POW2, under the ordered combine, whose
+ *   per-pair outputs take T*(k+1)*H*4 bytes).  FT_ERR_HIP if the array's device address
  *   cannot be found: it is looked up on the first call on each device (make that first call, a
  *   T = 0 call will do, before capturing a graph).
  *   All calls on one GPU share its array and nothing in it is kept between calls: calls that may

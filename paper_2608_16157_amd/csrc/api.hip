@@ -68,10 +68,10 @@ WsView carve(const ft_moe_desc_t *d, int T, void *ws) {
     v.row_tok = reinterpret_cast<int32_t *>(b + L.row_tok);
     v.row_gate = reinterpret_cast<float *>(b + L.row_gate);
     v.row_pair = reinterpret_cast<int32_t *>(b + L.row_pair);
-    v.h = b + L.h;
-    v.ypart = L.ypart_bytes ? reinterpret_cast<float *>(b + L.ypart) : nullptr;
     const bool aq = d->act_quant == FT_ACT_FP8_1x128_POW2;
     const bool gemm = gemm_shape(T, d->hidden, d->inter, d->w_dtype);
+    v.h = aq && gemm ? nullptr : b + L.h;
+    v.ypart = L.ypart_bytes ? reinterpret_cast<float *>(b + L.ypart) : nullptr;
     v.xq = aq && gemm ? b + L.xq : nullptr;
     v.xs = aq && gemm ? b + L.xs : nullptr;
     v.hq = aq && gemm ? b + L.hq : nullptr;

@@ -143,10 +143,11 @@ inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int combine, 
     L.row_tok = take(4u * rows);
     L.row_gate = take(4u * rows);
     L.row_pair = take(4u * rows);
-    L.h = take(rows * I * (w_dtype == FT_DT_F32 ? 4u : 2u));
-    L.ypart_bytes = (gemm_shape(T, H, I, w_dtype) || combine != FT_COMBINE_ORDERED) ? 0 : rows * H * 4u;
-    L.ypart = take(L.ypart_bytes);
     const bool aq = act_quant == FT_ACT_FP8_1x128_POW2, gemm = gemm_shape(T, H, I, w_dtype);
+    // the fp8-activation matrix-core path keeps h only as codes (hq, hs)
+    L.h = take(aq && gemm ? 0 : rows * I * (w_dtype == FT_DT_F32 ? 4u : 2u));
+    L.ypart_bytes = (gemm || combine != FT_COMBINE_ORDERED) ? 0 : rows * H * 4u;
+    L.ypart = take(L.ypart_bytes);
     L.xq = take(aq && gemm ? static_cast<size_t>(T) * H : 0);
     L.xs = take(aq && gemm ? static_cast<size_t>(T) * (H / 128) : 0);
     L.hq = take(aq && gemm ? rows * I : 0);

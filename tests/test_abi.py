@@ -280,14 +280,20 @@ def test_binding_rejects_host_tensors_and_bad_sizes_before_the_call():
 def test_act_quant_validation():
     """The fp8-activation mode: unknown values make the description invalid, non-fp8 weights
     are refused as a dtype error, the CPU branch (which evaluates exactly) refuses the mode, and
-    the matrix-core path's workspace grows by the codes and exponents of x and h."""
+    the workspace follows the mode: the streaming path adds a bf16 copy of the quantised x, the
+    matrix-core path holds x and h as codes and exponents in place of the bf16 h."""
     lib = ftm.load()
-    fp8 = _desc(w_dtype=2, x_dtype=1, hidden=256, inter=256)
+    H, I, k = 256, 256, 2
+    fp8 = _desc(w_dtype=2, x_dtype=1, hidden=H, inter=I, top_k=k)
     assert lib.ft_moe_workspace_bytes(ctypes.byref(ftm.make_desc(dict(fp8, act_quant=2))), 8) == 0
-    for T in (8, 300):
-        exact = lib.ft_moe_workspace_bytes(ctypes.byref(ftm.make_desc(fp8)), T)
-        aq = lib.ft_moe_workspace_bytes(ctypes.byref(ftm.make_desc(dict(fp8, act_quant=1))), T)
-        assert aq > exact
+    ws = lambda d, T: lib.ft_moe_workspace_bytes(ctypes.byref(ftm.make_desc(d)), T)
+    T = 8   # streaming path (ordered combine)
+    assert ws(dict(fp8, act_quant=1), T) - ws(fp8, T) in range(T * H * 2, T * H * 2 + 256)
+    T = 300
+    rows = T * (k + 1)   # evaluation rows are sized for a shared expert in every case
+    codes = T * H + T * H // 128 + rows * I + rows * I // 128
+    diff = ws(dict(fp8, act_quant=1), T) - ws(fp8, T)
+    assert abs(diff - (codes - rows * I * 2)) < 5 * 256
     d = ftm.make_desc(dict(fp8, act_quant=1))
     pool = ftm.ft_banks_t(FAKE, FAKE, FAKE, FAKE)
     assert lib.ft_cpu_experts(ctypes.byref(d), ctypes.byref(pool), FAKE, 1, FAKE, FAKE, FAKE, 1, FAKE,
