@@ -636,14 +636,14 @@ def measure_forward(config, T, n_layers, steps, warmup, hip, combine=0, act_quan
     gu_flops = sum(w["gateup_flops"] for w in step_work) / K
     stage_avg = [sum(s[j] for s in stage_ms) / K for j in range(ftm.FT_PROF_STAGES)]
     mfma_path = T >= 256      # the library's many-token (MFMA GEMM) path
-    traffic = measured_traffic(f"{config}:T{T}") if not act_quant else None
+    traffic = measured_traffic(f"{config}:T{T}" + (":fp8act" if act_quant else ""))
     if mfma_path and act_quant:
         # fp8 activations: fp8 x fp8 products on the matrix cores, against the fp8 dense peak
         achieved = gu_flops / (gu_ms / 1e3) / 1e12
         roof = {"kernel": "grouped gate/up GEMM, fp8 x fp8 + SiLU-mul (grouped_gemm<fp8 activations, gate/up>)",
                 "bound": "mfma", "achieved": round(achieved, 1), "peak": MFMA_PEAK_TFLOPS["fp8"],
                 "unit": "TFLOP/s", "frac": round(achieved / MFMA_PEAK_TFLOPS["fp8"], 4),
-                "traffic": None, "flops_per_launch": round(gu_flops),
+                "traffic": traffic, "flops_per_launch": round(gu_flops),
                 "bytes_per_launch": round(gu_bytes), "ms_per_launch": round(gu_ms, 5)}
     elif mfma_path:
         # fp8 and MXFP4 weights are widened to bf16 in registers, so every contraction runs on

@@ -114,12 +114,17 @@ __device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int l) {
     return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), l));
 }
 
-// max over the 64 lanes, result uniform
-__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+// max over the 16 lanes of this lane's row, in every lane of the row
+__device__ __forceinline__ uint32_t row_max_u32(uint32_t v) {
     v = max(v, dpp_u32<kDppRowRor1>(v));
     v = max(v, dpp_u32<kDppRowRor2>(v));
     v = max(v, dpp_u32<kDppRowRor4>(v));
-    v = max(v, dpp_u32<kDppRowRor8>(v));
+    return max(v, dpp_u32<kDppRowRor8>(v));
+}
+
+// max over the 64 lanes, result uniform
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+    v = row_max_u32(v);
     return max(max(readlane_u32(v, 0), readlane_u32(v, 16)), max(readlane_u32(v, 32), readlane_u32(v, 48)));
 }
 
