@@ -78,8 +78,10 @@ def expert_bytes(lay):
     return w13 + H * I * wb + s2, w13
 
 
-def algorithmic_work(lay, route):
-    """Bytes the layer must move and flops it must do, from the realised routing."""
+def algorithmic_work(lay, route, act_quant=0):
+    """Bytes the layer must move and flops it must do, from the realised routing.  With fp8
+    activations on the matrix-core path the gate/up GEMM reads x and writes h as one-byte codes
+    plus one exponent byte per 128 values."""
     import numpy as np
     T, H, I, E, k = lay.tokens, lay.hidden, lay.inter, lay.n_experts, lay.top_k
     xb = 4 if lay.x_dtype == 0 else 2
@@ -93,6 +95,8 @@ def algorithmic_work(lay, route):
     rows = n_hit + shared * T
     hb = 4 if lay.w_dtype == 0 else 2
     gateup_bytes = (u_hit + shared) * S13 + T * H * xb + rows * I * hb
+    if act_quant and T >= 256:
+        gateup_bytes = (u_hit + shared) * S13 + (T * H + rows * I) * 129 // 128
     flops = rows * 6 * H * I
     return dict(layer_bytes=layer_bytes, gateup_bytes=gateup_bytes, flops=flops,
                 gateup_flops=rows * 4 * H * I, u_hit=u_hit, n_hit=n_hit, rows=rows)
@@ -596,7 +600,7 @@ def measure_forward(config, T, n_layers, steps, warmup, hip, combine=0, act_quan
     for i in range(warmup):
         step(i)
     torch.cuda.synchronize()
-    work = [algorithmic_work(l, r) for l, r in zip(layers, routes)]
+    work = [algorithmic_work(l, r, act_quant) for l, r in zip(layers, routes)]
     K = steps
     stream = torch.cuda.current_stream().cuda_stream
     start, stop = hip.create(), hip.create()
