@@ -298,6 +298,18 @@ def test_act_quant_validation():
     pool = ftm.ft_banks_t(FAKE, FAKE, FAKE, FAKE)
     assert lib.ft_cpu_experts(ctypes.byref(d), ctypes.byref(pool), FAKE, 1, FAKE, FAKE, FAKE, 1, FAKE,
                               None) == ftm.FT_ERR_DTYPE
+    # the hybrid step merges with the CPU branch's exact partial: the mode is refused there too
+    fb = ftm.ft_banks_t(FAKE, FAKE, FAKE, FAKE)
+    pl = ftm.ft_fill_plan_t(*[FAKE] * 5)
+    st = ftm.ft_cache_state_t(FAKE, FAKE, None)
+    pol = ftm.ft_cache_policy_t(1.0, 2.0, 4, 1)
+    hh = ftm.ft_hybrid_host_t(*[FAKE] * 7)
+    rr = ftm.ft_route_t(*[FAKE] * 8)
+    hyb = lambda desc: lib.ft_moe_step_hybrid(
+        ctypes.byref(desc), ctypes.byref(fb), ctypes.byref(fb), FAKE, FAKE, ctypes.byref(st), ctypes.byref(pol),
+        FAKE, 4, FAKE, ctypes.byref(rr), ctypes.byref(pl), ctypes.byref(hh), FAKE, 1 << 30, None, FAKE)
+    assert hyb(d) == ftm.FT_ERR_DTYPE
+    assert hyb(ftm.make_desc(fp8)) == ftm.FT_ERR_SHAPE   # exact: passes to the staging lookup, which fails
     bf = ftm.make_desc(_desc(w_dtype=1, x_dtype=1, act_quant=1))
     r = ftm.ft_route_t(*[FAKE] * 8)
     assert lib.ft_route_only(ctypes.byref(bf), FAKE, FAKE, 4, ctypes.byref(r), FAKE, 1 << 30, None) == ftm.FT_ERR_DTYPE

@@ -37,6 +37,7 @@ def check_output_aq(out, ref, rows=None):
     zero = ~ref.any(axis=1)
     assert not got[zero].any(), "rows without hits must be exactly zero"
     floor = np.sqrt((ref.astype(np.float64) ** 2).mean(axis=1, keepdims=True))
+    floor[zero] = 1.0   # rows the oracle makes zero are checked for exact zeros above
     el = np.abs(got - ref) / np.maximum(np.abs(ref), floor)
     el[zero] = 0
     nz = ~zero
@@ -132,6 +133,22 @@ def test_fp8_act_prefill_tile_covering():
     ref, r2 = oracle_aq(lay, tokens=rows)
     check_route(route, r2, T, lay.top_k)
     check_output_aq(out, ref, rows=rows)
+
+
+@pytest.mark.parametrize("T", [40, 260])
+def test_fp8_act_prefill_layers(T):
+    """ft_prefill_layers in the mode: every layer against the oracle's full layer in the same
+    mode, on the streaming (T = 40) and matrix-core (T = 260) paths, with a shared expert."""
+    from tests.test_gpu_prefill import _desc, _oracle, _pool_in_id_order, _run
+    lays = [workloads.random_layer(170 + T + l, hidden=384, inter=256, n_experts=12, top_k=3, tokens=T,
+                                   gating=1, w_dtype=workloads.DT_FP8, n_resident=12, shared=True).to("cuda")
+            for l in range(3)]
+    desc = dict(_desc(lays[0]), act_quant=ftm.FT_ACT_FP8_1x128_POW2)
+    pools = [_pool_in_id_order(l) for l in lays]
+    _say(f"fp8 activations, prefill layers T={T}")
+    outs, _ = _run(desc, pools, lays, T, True)
+    for l in range(len(lays)):
+        check_output_aq(outs[l], _oracle(desc, pools[l], lays[l].logits, lays[l].x))
 
 
 def test_fp8_act_rejected_without_fp8_weights():
