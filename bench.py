@@ -104,11 +104,12 @@ def algorithmic_work(lay, route, act_quant=0):
 
 def kernel_source_sha(kernel: str) -> str:
     """Hash of the sources a dominant kernel is built from (its traffic figures are tied to it):
-    the GEMM's or the GEMV's file plus the shared device and interface headers."""
+    the GEMM's or the GEMV's file plus the shared device and interface headers, and for the GEMM
+    the router, whose tile map orders its tiles."""
     import hashlib
     h = hashlib.sha256()
-    main = "gemm.hip" if "gemm" in kernel else "experts.hip"
-    for name in (main, "ftmoe_device.h", "ftmoe_internal.h"):
+    files = ("gemm.hip", "route.hip") if "gemm" in kernel else ("experts.hip",)
+    for name in (*files, "ftmoe_device.h", "ftmoe_internal.h"):
         with open(os.path.join(ROOT, "paper_2608_16157_amd", "csrc", name), "rb") as fh:
             h.update(name.encode() + b"\0" + fh.read())
     return h.hexdigest()[:16]
