@@ -31,9 +31,14 @@ namespace ftmoe {
 #define FT_GEMV_NB 2
 #endif
 // fp8 and MXFP4 take items of 2 or 4 blocks: the narrow ones spread few-token calls (few groups)
-// over more workgroups; the fp8 down projection always takes the narrow ones
+// over more workgroups
 #ifndef FT_GEMV_NB_FP8
 #define FT_GEMV_NB_FP8 4
+#endif
+// the fp8 down projection takes the wide items, two K blocks a batch, above this many tokens
+// (measured at dsv3 T = 64: down 160 -> 152 us; at 1 and 16 tokens the narrow ones are faster)
+#ifndef FT_GEMV_FP8_DN_WIDE_TOKENS
+#define FT_GEMV_FP8_DN_WIDE_TOKENS 32
 #endif
 #ifndef FT_GEMV_NB_FP4
 #define FT_GEMV_NB_FP4 4
@@ -202,7 +207,9 @@ __global__ __launch_bounds__(kGemvThreads, (gemv_min_blocks<WT, EPI, MTX>())) vo
     // the wide fp8 items)
     constexpr int D = (MTX == 1 && (WT != FT_DT_FP8E4M3FN_B128 || NB == 2))
                           ? WTr<WT>::kBatch1
-                          : (MTX > 1 && EPI == EPI_GATEUP ? WTr<WT>::kBatchGU : WTr<WT>::kBatch);
+                          : (MTX > 1 && EPI == EPI_GATEUP
+                                 ? WTr<WT>::kBatchGU
+                                 : (WT == FT_DT_FP8E4M3FN_B128 && EPI == EPI_DOWN && NB == 4 ? 2 : WTr<WT>::kBatch));
     constexpr int NL = WTr<WT>::kLoads, NA = ALd<WT>::n;
     constexpr int COLS = NB * 16;
     constexpr int KB = WTr<WT>::kBlock;                        // bytes of one row's K block
@@ -521,7 +528,10 @@ static void launch_gemv(const ExpertArgs &a, hipStream_t s) {
     };
     const int pairs = a.T * a.k;
     if constexpr (WT == FT_DT_FP8E4M3FN_B128) {
-        if constexpr (EPI == EPI_DOWN) go(std::integral_constant<int, 2>{});
+        if constexpr (EPI == EPI_DOWN) {
+            if (a.T > FT_GEMV_FP8_DN_WIDE_TOKENS) go(std::integral_constant<int, 4>{});
+            else go(std::integral_constant<int, 2>{});
+        }
         else if (pairs <= FT_GEMV_FP8_NARROW_PAIRS) go(std::integral_constant<int, 2>{});
         else go(std::integral_constant<int, FT_GEMV_NB_FP8>{});
     } else if constexpr (WT == FT_DT_MXFP4) {

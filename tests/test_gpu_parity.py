@@ -231,13 +231,15 @@ RANDOM_FWD = [
     (20, workloads.DT_MXFP4, 0, 32, 8, 520, 13, False, 512, 384, 2.0),
     # every streaming-kernel variant the launcher picks: T <= 16 takes the one-M-tile kernels;
     # fp8 items are wide above 128 pairs, MXFP4 items above 12; the wide gate/up items take four M
-    # tiles a pass above 32 tokens (fp8) or from 64 (MXFP4)
+    # tiles a pass above 32 tokens (fp8) or from 64 (MXFP4); fp8 down items are wide, two K blocks
+    # a batch, above 32 tokens
     (21, workloads.DT_FP8, 1, 32, 12, 16, 20, True, 256, 256, 0.0),    # fp8, one tile, wide
     (22, workloads.DT_FP8, 0, 16, 4, 20, 10, False, 256, 384, 0.0),    # fp8, two tiles, narrow
     (23, workloads.DT_MXFP4, 1, 16, 4, 16, 12, True, 256, 256, 0.0),   # MXFP4, one tile, wide
     (24, workloads.DT_BF16, 0, 16, 4, 16, 16, True, 384, 256, 0.0),    # bf16, T = 16 exactly
     (25, workloads.DT_FP8, 1, 8, 4, 60, 8, True, 256, 256, 0.0),       # fp8 wide gate/up, 4 M tiles a pass
     (26, workloads.DT_MXFP4, 0, 16, 4, 100, 12, True, 256, 256, 0.7),  # MXFP4 wide gate/up, 4 M tiles a pass
+    (30, workloads.DT_FP8, 0, 16, 4, 48, 10, True, 512, 640, 0.5),     # fp8 wide down, 5 K blocks (tail batch)
     # groups above 1024 rows (more than one band of 8 M tiles, the last band short): strong skew
     # puts most tokens on the top experts, and the shared expert's 2900 rows make 23 M tiles
     (27, workloads.DT_BF16, 0, 16, 4, 2900, 12, True, 256, 256, 3.0),
