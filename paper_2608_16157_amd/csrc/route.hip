@@ -4,12 +4,21 @@
 //
 // Three variants:
 //  * route_wave: one wave does everything (one or two tokens, T*k <= 64 pairs).
-//  * route_fused: one 1024-thread workgroup does everything in LDS (decode).
+//  * route_fused: one 1024-thread workgroup does everything in LDS (decode), for the larger
+//    decode batches after route_topk has selected every token's experts on many CUs.
 //  * route_tokens -> route_scan -> route_scatter: many tokens (prefill chunks).
 // All produce bit-identical outputs: the permutation is a counting sort whose within-expert
 // order is the pair index, computed with wave ballots, never with order-dependent atomics.
 #include "ftmoe_device.h"
 #include "ftmoe_internal.h"
+
+// logits (T * E) from which the decode router takes its top-k in a kernel of its own: measured
+// at 16 tokens x 256 experts and beyond, the launch the split adds costs less than the selection
+// rounds it moves off the fused router's one CU (Qwen3 T = 64: routing 14.9 -> 9.8 us, dsv3
+// T = 64: 20.3 -> 10.6 us); at 16 x 128 and below it does not
+#ifndef FT_ROUTE_SPLIT_LOGITS
+#define FT_ROUTE_SPLIT_LOGITS 4096
+#endif
 
 namespace ftmoe {
 
@@ -329,8 +338,9 @@ __device__ void scan_experts(int E, int T, int k, int shared_slot, const int32_t
 }
 
 // ---------------------------------------------------------------------------------------
-// Fused single-workgroup routing for T*k <= kFusedMaxPairs (few tokens: decode).  Four
-// barriers separate five phases:
+// Fused single-workgroup routing for T*k <= kFusedMaxPairs (few tokens: decode).  For the
+// larger of these batches the top-k runs ahead in route_topk, and phase B only loads it (PRE).
+// Four barriers separate five phases:
 //   A  slot-table entry per thread, zeroed counters, logits of each wave's first token batch;
 //   B  experts per slot counted; top-k per token (a wave per token, kTopkBatch tokens per wave
 //      with their logits loaded together);
@@ -356,7 +366,8 @@ constexpr int kFusedWaves = kFusedThreads / kWave;
 constexpr int kTopkBatch = 4;
 constexpr int kFusedPairsPerThread = kFusedMaxPairs / kFusedThreads;
 
-template <int NPL>
+// PRE: the top-k was computed by route_topk (topk_ids, topk_w hold it); phase B only loads it.
+template <int NPL, bool PRE>
 __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     extern __shared__ int32_t lds[];
     // tokens per wave batch, within the 128 registers a 1024-thread workgroup leaves a lane
@@ -379,9 +390,20 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     // tokens of this wave: wave, wave + 16, ...; the first NBT are loaded here
     const int nmine = T > wave ? (T - wave + kFusedWaves - 1) / kFusedWaves : 0;
     uint32_t key0[NBT][NPL];
+    int pre_id[kFusedPairsPerThread];
+    float pre_w[kFusedPairsPerThread];
+    if constexpr (PRE) {
 #pragma unroll
-    for (int b = 0; b < NBT; ++b)
-        topk_load<NPL>(a.logits + static_cast<size_t>(min(wave + b * kFusedWaves, T - 1)) * E, E, key0[b]);
+        for (int i = 0; i < kFusedPairsPerThread; ++i) {
+            const int p = min(tid + i * kFusedThreads, P - 1);
+            pre_id[i] = a.ro.topk_ids[p];
+            pre_w[i] = a.ro.topk_w[p];
+        }
+    } else {
+#pragma unroll
+        for (int b = 0; b < NBT; ++b)
+            topk_load<NPL>(a.logits + static_cast<size_t>(min(wave + b * kFusedWaves, T - 1)) * E, E, key0[b]);
+    }
     for (int i = tid; i < nch * E; i += kFusedThreads) s_wh[i] = 0;
     for (int i = tid; i < ncnt; i += kFusedThreads) s_cnt[i] = 0;
     if (tid == 0) *s_status = 0;
@@ -429,14 +451,25 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
         topk_select<NPL>(key[0], k, a.gating, id[0], w[0]);
         put(tb, id[0], w[0]);
     };
-    if (nmine > 0) select_batch(key0, wave, min(nmine, NBT));
-    for (int b0 = NBT; b0 < nmine; b0 += NBT) {
-        uint32_t key[NBT][NPL];
-        const int tb = wave + b0 * kFusedWaves;
+    if constexpr (PRE) {
 #pragma unroll
-        for (int b = 0; b < NBT; ++b)
-            topk_load<NPL>(a.logits + static_cast<size_t>(min(tb + b * kFusedWaves, T - 1)) * E, E, key[b]);
-        select_batch(key, tb, min(nmine - b0, NBT));
+        for (int i = 0; i < kFusedPairsPerThread; ++i) {
+            const int p = tid + i * kFusedThreads;
+            if (p < P) {
+                s_ids[p] = pre_id[i];
+                s_w[p] = pre_w[i];
+            }
+        }
+    } else {
+        if (nmine > 0) select_batch(key0, wave, min(nmine, NBT));
+        for (int b0 = NBT; b0 < nmine; b0 += NBT) {
+            uint32_t key[NBT][NPL];
+            const int tb = wave + b0 * kFusedWaves;
+#pragma unroll
+            for (int b = 0; b < NBT; ++b)
+                topk_load<NPL>(a.logits + static_cast<size_t>(min(tb + b * kFusedWaves, T - 1)) * E, E, key[b]);
+            select_batch(key, tb, min(nmine - b0, NBT));
+        }
     }
     lds_barrier();
 
@@ -600,8 +633,10 @@ __global__ __launch_bounds__(kFusedThreads) void route_fused(RouteArgs a) {
     for (int i = tid; i < P; i += kFusedThreads) {
         if (i >= nh) a.ro.hit_pairs[i] = -1;
         if (i >= nm) a.ro.miss_pairs[i] = -1;
-        a.ro.topk_ids[i] = s_ids[i];
-        a.ro.topk_w[i] = s_w[i];
+        if constexpr (!PRE) {
+            a.ro.topk_ids[i] = s_ids[i];
+            a.ro.topk_w[i] = s_w[i];
+        }
     }
     if (a.shared_slot >= 0) {
         for (int t = tid; t < T; t += kFusedThreads) {
@@ -902,6 +937,21 @@ __global__ __launch_bounds__(64) void route_scatter(RouteArgs a) {
 }
 
 // ---------------------------------------------------------------------------------------
+// Top-k ahead of route_fused<NPL, true> for the larger decode batches: one wave per token, four
+// tokens per workgroup, so the k selection rounds of all tokens run on many CUs at once instead
+// of in turn on the 16 waves of the fused router.
+template <int NPL>
+__global__ __launch_bounds__(256) void route_topk(RouteArgs a) {
+    const int t = blockIdx.x * 4 + threadIdx.x / kWave, lane = lane_id();
+    if (t >= a.T) return;
+    int id;
+    float w;
+    wave_topk<NPL>(a.logits + static_cast<size_t>(t) * a.E, a.E, a.k, a.gating, id, w);
+    if (lane < a.k) {
+        a.ro.topk_ids[t * a.k + lane] = id;
+        a.ro.topk_w[t * a.k + lane] = w;
+    }
+}
 
 template <int NPL>
 static hipError_t launch_route_npl(RouteArgs a, hipStream_t s) {
@@ -916,7 +966,12 @@ static hipError_t launch_route_npl(RouteArgs a, hipStream_t s) {
         }
     }
     if (P <= kFusedMaxPairs && fused_lds <= kFusedMaxLds) {
-        hipLaunchKernelGGL(route_fused<NPL>, dim3(1), dim3(kFusedThreads), fused_lds, s, a);
+        if (a.T * a.E >= FT_ROUTE_SPLIT_LOGITS) {
+            hipLaunchKernelGGL(route_topk<NPL>, dim3((a.T + 3) / 4), dim3(256), 0, s, a);
+            hipLaunchKernelGGL((route_fused<NPL, true>), dim3(1), dim3(kFusedThreads), fused_lds, s, a);
+        } else {
+            hipLaunchKernelGGL((route_fused<NPL, false>), dim3(1), dim3(kFusedThreads), fused_lds, s, a);
+        }
         return hipGetLastError();
     }
     const int nblk = (a.T + kTokPerBlk - 1) / kTokPerBlk;

@@ -95,10 +95,15 @@ def test_route_bit_exact_configs(name, T):
     check_route(route, oracle.route(desc, logits, st), T, lay.top_k)
 
 
+# Decode batches of T * E >= 4096 logits take their top-k in a kernel ahead of the fused router:
+# cases on both sides of that edge, for 1, 2, 4, 8 and 16 experts per lane.
 @pytest.mark.parametrize("seed,E,k,T,ties", [(0, 8, 8, 5, True), (1, 1024, 64, 3, False),
                                              (2, 1000, 7, 33, True), (3, 64, 1, 2500, False),
                                              (4, 256, 8, 257, True), (5, 130, 13, 4099, True),
-                                             (6, 1024, 8, 600, False), (7, 2, 2, 1, True)])
+                                             (6, 1024, 8, 600, False), (7, 2, 2, 1, True),
+                                             (8, 128, 8, 31, True), (9, 128, 8, 32, True),
+                                             (10, 256, 8, 16, False), (11, 64, 4, 64, True),
+                                             (12, 512, 8, 8, True), (13, 130, 13, 40, True)])
 def test_route_bit_exact_random(seed, E, k, T, ties):
     _say(f"route random seed={seed} E={E} k={k} T={T}")
     lay = workloads.random_layer(seed, hidden=128, inter=128, n_experts=E, top_k=k, tokens=T,
@@ -264,6 +269,29 @@ def test_forward_random_shapes(case):
     if T >= 2000:
         sizes = np.diff(r["hit_off"])
         assert sizes.max() > 8 * GEMM_BM, "a group must span more than one band of M tiles"
+
+
+@pytest.mark.parametrize("wdt", [workloads.DT_BF16, workloads.DT_FP8, workloads.DT_MXFP4])
+def test_gemm_tile_classes(wdt):
+    """Groups sized at the edges of the router's GEMM tile classes (1, 32, 33, 64, 65, 96, 97, 128,
+    129 and 300 rows, one routed expert per token, plus a shared expert): every class, the class
+    boundaries and groups of one and of several M tiles in one call, checked on every row."""
+    sizes = [32, 33, 64, 65, 96, 97, 128, 129, 1, 300]
+    E, T = 12, sum(sizes)
+    lay = workloads.random_layer(77, hidden=256, inter=256, n_experts=E, top_k=1, tokens=T,
+                                 w_dtype=wdt, gating=0, n_resident=E, shared=True)
+    owner = np.repeat(np.arange(len(sizes)), sizes)
+    np.random.default_rng(5).shuffle(owner)      # tokens of one expert scattered over the batch
+    logits = np.random.default_rng(6).normal(size=(T, E)).astype(np.float32)
+    logits[np.arange(T), owner] += 20.0
+    lay.logits = torch.from_numpy(logits)
+    lay = lay.to("cuda")
+    _say(f"GEMM tile classes, dtype {wdt}")
+    out, route = run_forward(lay)
+    ref, r = oracle.moe_partial(*oracle_inputs(lay))
+    assert sorted(np.diff(r["hit_off"])[np.diff(r["hit_off"]) > 0].tolist()) == sorted(sizes)
+    check_route(route, r, T, 1)
+    check_output(out, ref, wdt)
 
 
 @pytest.mark.parametrize("T", [20, 300])
