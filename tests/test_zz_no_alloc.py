@@ -31,8 +31,8 @@ def _layer(kind, T):
     return workloads.make_layer(kind, T, device="cuda")
 
 
-def _both(lay, T):
-    desc = lay.desc()
+def _both(lay, T, act_quant=0):
+    desc = dict(lay.desc(), act_quant=act_quant)
     banks = ftm.banks_of(lay)
     ra, rb = (ftm.RouteBuffers(T, lay.top_k, lay.n_experts) for _ in range(2))
     oa = torch.full((T, lay.hidden), float("nan"), device="cuda")
@@ -60,6 +60,24 @@ def test_noalloc_matches_forward_twice(kind, T1, T2):
         assert oracle.max_rel_err(b, a) <= tol
         ref, _ = oracle.moe_partial(*oracle_inputs(lay))
         assert oracle.max_rel_err(b, ref) <= tol
+
+
+@pytest.mark.parametrize("kind,T1,T2", [("gemm", 700, 300), ("dsv3_decode", 64, 16)])
+def test_noalloc_fp8_activations_twice(kind, T1, T2):
+    """The optional fp8-activation mode through the array: the matrix-core path (codes of x and
+    h in the array) and the streaming path (the widened x in the array)."""
+    for T in (T1, T2):
+        print(f"noalloc fp8 activations {kind} T={T}", flush=True)
+        lay = _layer(kind, T)
+        oa, ra, ob, rb = _both(lay, T, ftm.FT_ACT_FP8_1x128_POW2)
+        for n in ROUTE_FIELDS:
+            assert torch.equal(getattr(ra, n), getattr(rb, n)), n
+        a, b = oa.cpu().numpy(), ob.cpu().numpy()
+        assert np.isfinite(b).all()
+        assert np.array_equal(~a.any(axis=1), ~b.any(axis=1))
+        # the same kernels on the same inputs: only the order of the float32 atomic adds of the
+        # matrix-core down projection may differ
+        assert oracle.max_rel_err(b, a) <= 1e-4
 
 
 def test_noalloc_rejects_a_workspace_beyond_the_array():
