@@ -3,13 +3,15 @@
 // addressed as bank + slot * expert_stride with no relayout), and the gate-weighted combine.
 //
 // Streaming (GEMV-like) path, any token count and any weight dtype:
-//   grouped_gemv<GATEUP>: h[r] = silu(W1 x_tok(r)) * (W3 x_tok(r))       per group, 8 h-columns/WG
-//   grouped_gemv<DOWN>  : y[pair(r)] = gate(r) * W2 h[r]                 per group, 16 columns/WG
+//   grouped_gemv<GATEUP>: h[r] = silu(W1 x_tok(r)) * (W3 x_tok(r))       per (group, 8 NB h columns)
+//   grouped_gemv<DOWN>  : y[pair(r)] = gate(r) * W2 h[r]                 per (group, 16 NB columns)
 //   combine             : out[t] = sum_j y[t k + j] over the pairs evaluated on the GPU, in
 //                         j order, then the shared expert's row: every output element is summed
 //                         in one fixed order, so the layer output is bit-reproducible
 // With the atomic combine the down projection adds gate(r) * W2 h[r] into out[tok(r)] with
-// float32 atomics instead (the gate/up kernel zeroes out first): one launch less.
+// float32 atomics instead (the gate/up kernel zeroes out first): one launch less.  In the
+// optional fp8-activation mode x and h are quantised (quant.hip) and widened back to bf16 before
+// the projections read them.
 // The weights stream from HBM once per (group, column tile).  Tokens of a group are the MFMA M
 // dimension (16-row tiles), weight rows the N dimension; the contraction (hidden or intermediate
 // dimension) is split over the 4 waves of a workgroup in contiguous runs of 128-wide blocks (the

@@ -1,5 +1,5 @@
-// Grouped expert GEMM on MFMA tiles for many-token chunks (prefill): bf16 or fp8 weights,
-// bf16 activations, float32 accumulation.
+// Grouped expert GEMM on MFMA tiles for many-token chunks (prefill): bf16, fp8 or MXFP4 weights,
+// bf16 activations (fp8 ones in the optional FT_ACT_FP8_1x128_POW2 mode), float32 accumulation.
 //
 // The same two projections as the streaming path (Section 3.2, grouped evaluation of the GPU
 // execution set; weights addressed through the slot, Section 4.2), shaped for matrix-core reuse:
@@ -24,7 +24,10 @@
 // the M tile fastest, through the per-M-tile group map the router writes, so the tiles that
 // share a weight tile and those that share activation rows run at the same time; the block ->
 // tile map keeps consecutive tiles on one XCD (workgroups are dealt to the 8 XCDs round-robin)
-// to share its L2.
+// to share its L2.  The router numbers the groups in cost classes (the shared expert, groups of
+// several M tiles, then one-tile groups by their live 32-row sub-tiles), and tiles skip the
+// MFMAs of sub-tiles that hold only padding rows (all but the fp8-activation kernels, whose
+// registers do not allow the extra loop variants), so the tiles of one launch cost about the same.
 //
 // Data movement.  A (activation rows, gathered through row_tok for gate/up) and B (weight rows,
 // kept in their storage format) go straight from global memory into LDS with global_load_lds
