@@ -25,7 +25,10 @@ routes each token to k of them).  The readings taken here:
   else is a miss (Section 4.1 rewrites routed ids into slot ids or a CPU flag).
 * permutation: hit pairs p = t*k + j sorted stably by expert id (so, within one expert, by
   ascending p); misses likewise.  Offsets are exclusive prefix sums of per-expert counts.
-* expert FFN (SwiGLU): FFN(x) = W2 (silu(W1 x) * (W3 x)), silu(z) = z / (1 + exp(-z)).
+* expert FFN (SwiGLU): FFN(x) = W2 (silu(W1 x) * (W3 x)), silu(z) = z / (1 + exp(-z)).  For
+  layers with bf16, fp8 or MXFP4 weights the activation between the two projections is a
+  bfloat16 tensor, as in a model served in BF16 (Section 5.1): h = bf16(silu(W1 x) * (W3 x)),
+  rounded to nearest, ties to even; float32 layers keep h exact.
 * output: out[t] = sum over hit pairs of g_tj FFN_e(x_t) (+ FFN_shared(x_t), weight 1, when a
   shared expert is configured); a token without hits and without shared expert gets 0.
 * fp8 activations (optional mode ACT_FP8_1X128_POW2, not the paper's exact method): the expert
@@ -243,9 +246,14 @@ def silu(z: np.ndarray) -> np.ndarray:
     return z / (1.0 + np.exp(-z))
 
 
-def expert_ffn(x: np.ndarray, w1: np.ndarray, w3: np.ndarray, w2: np.ndarray) -> np.ndarray:
-    """SwiGLU expert on rows of x: [n][H] -> [n][H], all float64."""
-    return (silu(x @ w1.T) * (x @ w3.T)) @ w2.T
+def expert_ffn(x: np.ndarray, w1: np.ndarray, w3: np.ndarray, w2: np.ndarray,
+               h_bf16: bool = False) -> np.ndarray:
+    """SwiGLU expert on rows of x: [n][H] -> [n][H], float64 arithmetic; with h_bf16 the
+    intermediate activation is rounded to bfloat16 before the down projection."""
+    h = silu(x @ w1.T) * (x @ w3.T)
+    if h_bf16:
+        h = round_bf16(h)
+    return h @ w2.T
 
 
 # ----------------------------------------------------------------------------------------
@@ -254,7 +262,7 @@ def expert_ffn(x: np.ndarray, w1: np.ndarray, w3: np.ndarray, w2: np.ndarray) ->
 
 def round_bf16(v: np.ndarray) -> np.ndarray:
     """Nearest bfloat16 value (8 significant bits, round half to even), as float64.  Normal
-    range only (no value here comes near bfloat16's subnormals or its overflow)."""
+    range and zero only (no value here comes near bfloat16's subnormals or its overflow)."""
     v = np.asarray(v, dtype=np.float64)
     m, p = np.frexp(v)                      # v = m 2^p, 0.5 <= |m| < 1
     return np.ldexp(np.rint(np.ldexp(m, 8)), p - 8)
@@ -327,7 +335,11 @@ def moe_partial(desc: dict, banks: dict, logits, slot_table, x, tokens=None):
     T = np.asarray(logits).shape[0]
     H, k = desc["hidden"], desc["top_k"]
     want = np.ones(T, dtype=bool) if tokens is None else np.isin(np.arange(T), tokens)
-    ffn = expert_ffn_fp8_act if desc.get("act_quant", ACT_EXACT) == ACT_FP8_1X128_POW2 else expert_ffn
+    if desc.get("act_quant", ACT_EXACT) == ACT_FP8_1X128_POW2:
+        ffn = expert_ffn_fp8_act
+    else:
+        h_bf16 = desc["w_dtype"] != DT_F32
+        ffn = lambda xr, w1, w3, w2: expert_ffn(xr, w1, w3, w2, h_bf16)
     acc = np.zeros((T, H), dtype=np.float64)
     # group the wanted hit pairs by expert and run each expert once over its tokens
     for e in range(desc["n_experts"]):

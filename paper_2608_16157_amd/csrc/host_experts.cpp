@@ -14,7 +14,8 @@
 //            so every output element is summed in a fixed order (the result does not depend on
 //            the thread count or timing).
 // Weights are decoded exactly (bf16 by widening, fp8 e4m3fn and MXFP4 e2m1 from the format
-// definitions times their scales) and every product accumulates in float32.  All code in this file is
+// definitions times their scales) and every product accumulates in float32.  As on the GPU, h is
+// held as bfloat16 values (rounded to nearest even) for all but float32 layers.  All code in this file is
 // compiled for AVX2 + FMA; the entry point checks the CPU supports them before calling in.
 #include <pthread.h>
 #include <sched.h>
@@ -83,6 +84,16 @@ float e8m0_to_float(uint8_t s) { return s == 255 ? NAN : std::ldexp(1.0f, static
 float bf16_to_float(uint16_t b) {
     const uint32_t u = static_cast<uint32_t>(b) << 16;
     float f;
+    std::memcpy(&f, &u, 4);
+    return f;
+}
+
+// Nearest bfloat16 value of a finite float (round half to even on the dropped 16 bits).
+float round_to_bf16(float f) {
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    u &= 0xFFFF0000u;
     std::memcpy(&f, &u, 4);
     return f;
 }
@@ -338,7 +349,8 @@ void cpu_experts(const CpuExpertArgs &a) {
             for (size_t n = 0; n < toks[li].size(); ++n) {
                 const float *xv = xf.data() + static_cast<size_t>(toks[li][n]) * H;
                 const float gs = dot(g, xv, H), us = dot(u, xv, H);
-                h[li][n * I + r] = gs / (1.0f + std::exp(-gs)) * us;
+                const float hv = gs / (1.0f + std::exp(-gs)) * us;
+                h[li][n * I + r] = a.w_dtype == FT_DT_F32 ? hv : round_to_bf16(hv);
             }
         }
     });

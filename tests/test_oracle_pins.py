@@ -250,7 +250,11 @@ def test_swiglu_identity_weights():
 
 def _dense_reference(lay, resident_mask):
     """Dense masked MoE in torch float64: every expert on every token, gate zero unless the
-    expert is among the token's top-k AND resident.  Independent of the oracle's grouping."""
+    expert is among the token's top-k AND resident.  Independent of the oracle's grouping.  For
+    bf16, fp8 and MXFP4 layers the activation between the projections goes through torch's own
+    bfloat16 cast."""
+    def hcast(h):
+        return h if lay.w_dtype == 0 else h.to(torch.bfloat16).double()
     T, E, H, I, k = lay.tokens, lay.n_experts, lay.hidden, lay.inter, lay.top_k
     l = lay.logits.double()
     score = torch.softmax(l, dim=1) if lay.gating == 0 else torch.sigmoid(l)
@@ -268,13 +272,13 @@ def _dense_reference(lay, resident_mask):
         w2 = decode_bank_torch(lay.w2[slot], lay.w_dtype, None if lay.s2 is None else lay.s2[slot])
         a = torch.einsum("th,ih->ti", xd, w13[:I])
         b = torch.einsum("th,ih->ti", xd, w13[I:])
-        y = torch.einsum("ti,hi->th", torch.nn.functional.silu(a) * b, w2)
+        y = torch.einsum("ti,hi->th", hcast(torch.nn.functional.silu(a) * b), w2)
         out += gate[:, e:e + 1] * y
     if lay.shared_slot >= 0:
         s = lay.shared_slot
         w13 = decode_bank_torch(lay.w13[s], lay.w_dtype, None if lay.s13 is None else lay.s13[s])
         w2 = decode_bank_torch(lay.w2[s], lay.w_dtype, None if lay.s2 is None else lay.s2[s])
-        h = torch.nn.functional.silu(xd @ w13[:I].T) * (xd @ w13[I:].T)
+        h = hcast(torch.nn.functional.silu(xd @ w13[:I].T) * (xd @ w13[I:].T))
         out += h @ w2.T
     return out.numpy()
 
