@@ -271,6 +271,36 @@ def test_forward_random_shapes(case):
         assert sizes.max() > 8 * GEMM_BM, "a group must span more than one band of M tiles"
 
 
+def _sweep_cases(seed, n):
+    rng = np.random.default_rng(seed)
+    for _ in range(n):
+        wdt = int(rng.choice([workloads.DT_BF16, workloads.DT_FP8, workloads.DT_MXFP4]))
+        E = int(rng.choice([8, 16, 24, 40, 64, 130]))
+        k = int(rng.integers(1, min(E, 9)))
+        T = int(rng.choice([int(rng.integers(3, 120)), int(rng.integers(256, 2400))]))
+        yield dict(seed=int(rng.integers(0, 1 << 30)), w_dtype=wdt, n_experts=E, top_k=k, tokens=T,
+                   hidden=int(rng.choice([256, 512])), inter=int(rng.choice([128, 256, 384])),
+                   shared=bool(rng.integers(0, 2)), n_resident=int(rng.integers(0, E + 1)),
+                   zipf_s=float(rng.choice([0.0, 1.0, 2.5])), gating=int(rng.integers(0, 2)))
+
+
+@pytest.mark.parametrize("chunk", range(4))
+def test_forward_random_sweep(chunk):
+    """A seeded sweep of 40 random layers over every weight format, both paths (3-119 and
+    256-2399 tokens), residency from none to full, skew and the shared expert, every row
+    checked."""
+    for i, c in enumerate(_sweep_cases(2024, 40)):
+        if i % 4 != chunk:
+            continue
+        _say(f"sweep {i}: {c}")
+        seed = c.pop("seed")
+        lay = workloads.random_layer(seed, device="cuda", **c)
+        out, route = run_forward(lay)
+        ref, r = oracle.moe_partial(*oracle_inputs(lay))
+        check_route(route, r, c["tokens"], c["top_k"])
+        check_output(out, ref, c["w_dtype"])
+
+
 @pytest.mark.parametrize("wdt", [workloads.DT_BF16, workloads.DT_FP8, workloads.DT_MXFP4])
 def test_gemm_tile_classes(wdt):
     """Groups sized at the edges of the router's GEMM tile classes (1, 32, 33, 64, 65, 96, 97, 128,
