@@ -26,8 +26,8 @@
 // tile map keeps consecutive tiles on one XCD (workgroups are dealt to the 8 XCDs round-robin)
 // to share its L2.  The router numbers the groups in cost classes (the shared expert, groups of
 // several M tiles, then one-tile groups by their live 32-row sub-tiles), and tiles skip the
-// MFMAs of sub-tiles that hold only padding rows (all but the fp8-activation kernels, whose
-// registers do not allow the extra loop variants), so the tiles of one launch cost about the same.
+// MFMAs of sub-tiles that hold only padding rows (the fp8-activation kernels in steps of two
+// sub-tiles), so the tiles of one launch cost about the same.
 //
 // Data movement.  A (activation rows, gathered through row_tok for gate/up) and B (weight rows,
 // kept in their storage format) go straight from global memory into LDS with global_load_lds
@@ -127,8 +127,8 @@ template <> struct GTr<FT_DT_FP8E4M3FN_B128> {
 };
 // fp8 weights and fp8 activations: 64 K values per stage (one 32x32x64 MFMA step).  Two
 // workgroups per CU with a two-stage ring (one workgroup with four stages was slower: 5.1 ms
-// against 3.4 ms for the DeepSeek-V3 prefill layer); the down projection runs every 32-row
-// sub-tile, since its padding-skipping variants spilled registers.
+// against 3.4 ms for the DeepSeek-V3 prefill layer); both projections skip padding in steps of
+// two 32-row sub-tiles (layer 3.32 -> 3.27 ms).
 #ifndef FT_GEMM_AQ_OCC_GU
 #define FT_GEMM_AQ_OCC_GU 2
 #endif
@@ -141,15 +141,12 @@ template <> struct GTr<FT_DT_FP8E4M3FN_B128> {
 #ifndef FT_GEMM_AQ_CHUNK_DN
 #define FT_GEMM_AQ_CHUNK_DN 2560   // as for the exact fp8 down GEMM (1536: down 1.40 against 1.25 ms)
 #endif
-#ifndef FT_GEMM_AQ_SKIP_DN
-#define FT_GEMM_AQ_SKIP_DN false
-#endif
 template <> struct GTr<kWtFp8Act> {
     static constexpr int BK = 64, BRB = BK;
     static constexpr int OCC_GU = FT_GEMM_AQ_OCC_GU, OCC_DN = FT_GEMM_AQ_OCC_DN;
     static constexpr int NS_GU = OCC_GU == 2 ? 2 : 4, NS_DN = OCC_DN == 2 ? 2 : 4;
     static constexpr long CHUNK_GU = FT_GEMM_AQ_CHUNK_GU, CHUNK_DN = FT_GEMM_AQ_CHUNK_DN;
-    static constexpr bool SKIP_PAD_GU = false, SKIP_PAD_DN = FT_GEMM_AQ_SKIP_DN;
+    static constexpr bool SKIP_PAD_GU = true, SKIP_PAD_DN = true;
 };
 // MXFP4: 64 K values (32 code bytes) per weight row and stage, so that one lane's 16-byte chunk
 // of a row is a whole 32-value scale run
@@ -687,8 +684,11 @@ __global__ __launch_bounds__(kGemmThreads, EPI == GEMM_GATEUP ? GTr<WT>::OCC_GU 
     bool any_zero_scale = false;
     if constexpr (kFp8)
         for (int w = 0; w < kWavesN; ++w) any_zero_scale |= s_zeroblk[w] != 0;
-    // one main loop per live sub-tile count (in steps of MLQ sub-tiles for tall tiles)
-    constexpr int MLQ = kMI > 4 ? 2 : 1;
+    // one main loop per live sub-tile count, in steps of MLQ sub-tiles for tall tiles and for the
+    // fp8-activation kernels (with steps of one their registers spilled in the common main loop;
+    // with steps of two only the loop for zero block scales, which real weights rarely take,
+    // spills)
+    constexpr int MLQ = kMI > 4 || kAq ? 2 : 1;
     const int wrows = min(max(len - m0 - wm * kWaveRows, 0), kWaveRows);   // real rows of this wave
     constexpr bool kSkipPad = EPI == GEMM_DOWN ? GTr<WT>::SKIP_PAD_DN : GTr<WT>::SKIP_PAD_GU;
     const int mlive = kSkipPad ? __builtin_amdgcn_readfirstlane((wrows + 32 * MLQ - 1) / (32 * MLQ) * MLQ)
