@@ -110,7 +110,7 @@ template <int WT> struct GTr;
 template <> struct GTr<FT_DT_BF16> {
     static constexpr int BK = FT_GEMM_BF16_BK, NS = FT_GEMM_BF16_NS, BRB = 2 * BK;
     static constexpr int OCC_GU = kGemmOcc, OCC_DN = kGemmOcc, NS_GU = NS, NS_DN = NS;
-    static constexpr long CHUNK_GU = 768, CHUNK_DN = 1024;
+    static constexpr long CHUNK_GU = 768, CHUNK_DN = 2048;   // down 1024 before the tile classes
     static constexpr bool SKIP_PAD_GU = true, SKIP_PAD_DN = true;
 };
 #ifndef FT_GEMM_FP8_CHUNK_GU
