@@ -141,6 +141,8 @@ CASES = [
     (2, workloads.DT_F32, 0, 8, 3, 2, 4, 128, 128, False, 2, (6.0, 5.0)),
     (3, workloads.DT_BF16, 1, 24, 8, 6, 5, 384, 256, True, 8, (25.1, 63.2)),
     (4, workloads.DT_MXFP4, 1, 20, 6, 4, 3, 256, 384, False, 4, (55.5, 44.9)),
+    # a prefill-sized step: the evaluation groups of G = H u F drive the matrix-core GEMM
+    (5, workloads.DT_FP8, 1, 16, 6, 4, 300, 256, 256, True, 4, (54.1, 137.2)),
 ]
 
 
