@@ -355,7 +355,9 @@ void ft_cpu_pool_destroy(ft_cpu_pool_t *pool);
  *   experts     n_list distinct expert ids to evaluate (e.g. ft_fill_plan_t.cpu_expert)
  *   out         [T][H] float32, overwritten: out[t] = sum over (t, j) with topk_ids[t][j] in
  *               experts of topk_w[t][j] * FFN_e(x_t), every product accumulated in float32 and
- *               every element summed in a fixed order (independent of the pool)
+ *               every element summed in a fixed order (independent of the pool); the SwiGLU
+ *               activation between the two projections is rounded to bf16 (float32 for f32
+ *               layers), as on the GPU
  * Returns FT_ERR_DTYPE if the host CPU lacks AVX2 and FMA.
  */
 ft_status_t ft_cpu_experts(const ft_moe_desc_t *desc, const ft_banks_t *host_pool, const void *x,
