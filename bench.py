@@ -108,7 +108,7 @@ def kernel_source_sha(kernel: str) -> str:
     the router, whose tile map orders its tiles."""
     import hashlib
     h = hashlib.sha256()
-    files = ("gemm.hip", "route.hip") if "gemm" in kernel else ("experts.hip",)
+    files = ("gemm.hip", "route.hip", "route_wave.h") if "gemm" in kernel else ("experts.hip", "route_wave.h")
     for name in (*files, "ftmoe_device.h", "ftmoe_internal.h"):
         with open(os.path.join(ROOT, "paper_2608_16157_amd", "csrc", name), "rb") as fh:
             h.update(name.encode() + b"\0" + fh.read())

@@ -8,6 +8,7 @@
 #include <vector>
 
 #include "ftmoe_internal.h"
+#include "route_wave.h"
 
 using namespace ftmoe;
 
@@ -159,7 +160,7 @@ namespace {
 
 hipError_t enqueue_experts(const ft_moe_desc_t *desc, const ft_banks_t *banks, const void *x, int32_t T,
                            float *out_partial, const ft_route_t *route, const WsView &wv, hipStream_t s,
-                           const Prof &prof);
+                           const Prof &prof, const RouteArgs *self_route = nullptr);
 
 ft_status_t forward_impl(const ft_moe_desc_t *desc, const ft_banks_t *banks, const float *logits,
                          const int32_t *slot_table, const void *x, int32_t T, float *out_partial,
@@ -174,8 +175,13 @@ ft_status_t forward_impl(const ft_moe_desc_t *desc, const ft_banks_t *banks, con
     const WsView wv = carve(desc, T, ws);
     const RouteArgs ra = route_args(desc, logits, slot_table, T, route, wv);
     if (!prof.mark(0)) return FT_ERR_HIP;
-    if (launch_route(ra, s) != hipSuccess) return FT_ERR_HIP;
-    if (enqueue_experts(desc, banks, x, T, out_partial, route, wv, s, prof) != hipSuccess) return FT_ERR_HIP;
+    // one or two tokens on the streaming path: the gate/up kernel routes the call itself (no
+    // router launch); otherwise the router kernels run first
+    const bool self_route = desc->n_slots > 0 && self_route_ok(T, desc->n_experts, desc->top_k, desc->n_slots);
+    if (!self_route && launch_route(ra, s) != hipSuccess) return FT_ERR_HIP;
+    if (enqueue_experts(desc, banks, x, T, out_partial, route, wv, s, prof, self_route ? &ra : nullptr) !=
+        hipSuccess)
+        return FT_ERR_HIP;
     if (!prof.mark(FT_PROF_STAGES)) return FT_ERR_HIP;
     return FT_OK;
 }
@@ -187,8 +193,16 @@ namespace {
 // The grouped expert FFN and the combine over the groups the workspace holds.
 hipError_t enqueue_experts(const ft_moe_desc_t *desc, const ft_banks_t *banks, const void *x, int32_t T,
                            float *out_partial, const ft_route_t *route, const WsView &wv, hipStream_t s,
-                           const Prof &prof) {
+                           const Prof &prof, const RouteArgs *self_route) {
     ExpertArgs ea{};
+    if (self_route) {
+        ea.logits = self_route->logits;
+        ea.slot_table = self_route->slot_table;
+        ea.E = self_route->E;
+        ea.gating = self_route->gating;
+        ea.shared_slot = self_route->shared_slot;
+        ea.nbits = self_route->nbits;
+    }
     ea.w13 = banks->w13;
     ea.w2 = banks->w2;
     ea.s13 = banks->s13;

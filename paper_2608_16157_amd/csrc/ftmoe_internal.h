@@ -96,6 +96,11 @@ struct ExpertArgs {
     int T, H, I, k, w_dtype, n_slots, shared;
     int act_quant;    // FT_ACT_*
     int max_groups;   // upper bound on groups, known on the host
+    // routing of a one- or two-token call done by the gate/up kernel itself (logits != nullptr;
+    // otherwise the router ran before and the workspace holds its groups)
+    const float *logits;
+    const int32_t *slot_table;
+    int E, gating, shared_slot, nbits;
     RouteOut ro;
     WsView wv;
 };

@@ -175,6 +175,46 @@ def test_forward_configs_full(name, T):
     check_output(out, ref, lay.w_dtype)
 
 
+# One- and two-token calls with 65 to 256 experts are routed inside the gate/up kernel (each
+# workgroup routes with one wave; workgroup 0 writes the routing's outputs).  Its edges through
+# the whole layer: two and four experts per router lane, an expert count that is not a multiple
+# of 64, 64 pairs (every lane holds one), the shared expert's rows after the hit rows, every
+# weight dtype, sigmoid gating, no resident expert, and a faulty slot table.
+@pytest.mark.parametrize("seed,E,k,T,gating,shared,wdt,n_res", [
+    (40, 128, 8, 2, workloads.GATE_SOFTMAX, False, workloads.DT_BF16, None),
+    (41, 200, 3, 1, workloads.GATE_SIGMOID, True, workloads.DT_FP8, None),
+    (42, 65, 32, 2, workloads.GATE_SOFTMAX, True, workloads.DT_MXFP4, None),
+    (43, 256, 6, 2, workloads.GATE_SIGMOID, False, workloads.DT_F32, None),
+    (44, 256, 8, 1, workloads.GATE_SOFTMAX, True, workloads.DT_BF16, 256),
+    (45, 129, 4, 2, workloads.GATE_SOFTMAX, True, workloads.DT_FP8, 0),
+    (46, 192, 16, 2, workloads.GATE_SOFTMAX, False, workloads.DT_BF16, 0)])
+def test_forward_self_routed(seed, E, k, T, gating, shared, wdt, n_res):
+    _say(f"forward self-routed seed={seed} E={E} k={k} T={T} dtype={wdt} shared={shared} resident={n_res}")
+    lay = workloads.random_layer(seed, hidden=256, inter=256, n_experts=E, top_k=k, tokens=T, gating=gating,
+                                 w_dtype=wdt, n_resident=n_res, shared=shared, zipf_s=1.0, device="cuda")
+    out, route = run_forward(lay)
+    ref, r = oracle.moe_partial(*oracle_inputs(lay))
+    check_route(route, r, T, k)
+    check_output(out, ref, lay.w_dtype)
+
+
+def test_forward_self_routed_invalid_slot_table():
+    lay = workloads.random_layer(47, hidden=256, inter=256, n_experts=128, top_k=8, tokens=2,
+                                 n_resident=40, shared=True, device="cuda")
+    st = lay.slot_table.clone()
+    res = (st >= 0).nonzero().flatten().tolist()
+    st[res[0]] = st[res[1]]                  # duplicate
+    st[res[2]] = lay.n_slots + 5             # out of range
+    st[res[3]] = lay.shared_slot             # points at the shared expert
+    lay.slot_table = st
+    _say(f"forward self-routed, invalid slot table: {st.tolist()}")
+    out, route = run_forward(lay)
+    ref, r = oracle.moe_partial(*oracle_inputs(lay))
+    assert r["status"] == 7
+    check_route(route, r, 2, lay.top_k)
+    check_output(out, ref, lay.w_dtype)
+
+
 GEMM_BM = 128      # token rows of one M tile of the many-token (matrix-core) path
 
 
