@@ -217,7 +217,7 @@ ft_status_t ft_moe_forward(const ft_moe_desc_t *desc, const ft_banks_t *banks, c
  * GPU holds from the library's load until the process ends; the call itself allocates and frees
  * nothing.  Every argument and every result is as for ft_moe_forward.
  *   Returns FT_ERR_CAPACITY, before enqueuing anything, when ft_moe_workspace_bytes(desc, T)
- *   exceeds FT_NOALLOC_SCRATCH_BYTES (e.g. 64 MiB holds a Qwen3-30B-A3B-shaped layer up to 4805
+ *   exceeds FT_NOALLOC_SCRATCH_BYTES (e.g. 64 MiB holds a Qwen3-30B-A3B-shaped layer up to 4804
  *   tokens, and a DeepSeek-V3-shaped one up to 1811 tokens, 2583 with FT_ACT_FP8_1x128_POW2,
  *   except 228..255, 217..255 with FT_ACT_FP8_1x128_POW2, under the ordered combine, whose
  *   per-pair outputs take T*(k+1)*H*4 bytes).  FT_ERR_HIP if the array's device address

@@ -19,6 +19,7 @@ namespace ftmoe {
 constexpr int kMaxExperts = 1024;
 constexpr int kMaxTopK = 64;
 constexpr int kTokPerBlk = 16;          // tokens per workgroup in the multi-block router
+constexpr int kBlkPerPart = 16;         // router blocks per part of its scan (the part table)
 constexpr int kFusedMaxPairs = 2048;    // T*k handled by the single-workgroup router
 constexpr int kFusedMaxLds = 64 * 1024;
 #ifndef FT_GEMM_BM
@@ -55,7 +56,7 @@ struct RouteOut {
 //  reads the weights of bank row grp_slot[g].
 struct WsView {
     int32_t *eff_slot;   // [E]
-    int32_t *blk_hist;   // [nblk][E]
+    int32_t *blk_hist;   // [nblk][E] per-block expert counts, then [ceil(nblk / kBlkPerPart)][E] part sums
     int32_t *grp_meta;   // [8]: G (groups incl. shared), U (hit groups), n_hit, T, M-tiles
     int32_t *grp_slot;   // [E+1]
     int32_t *grp_beg;    // [E+1]
@@ -138,7 +139,8 @@ inline WsLayout ws_layout(int E, int H, int I, int k, int w_dtype, int combine, 
     const size_t nblk = (static_cast<size_t>(T) + kTokPerBlk - 1) / kTokPerBlk;
     const size_t rows = static_cast<size_t>(T) * k + T;
     L.eff_slot = take(4u * E);
-    L.blk_hist = take(4u * nblk * E);
+    const size_t nparts = (nblk + kBlkPerPart - 1) / kBlkPerPart;
+    L.blk_hist = take(4u * (nblk + nparts) * E);
     L.grp_meta = take(32);
     L.grp_slot = take(4u * (E + 1));
     L.grp_beg = take(4u * (E + 1));

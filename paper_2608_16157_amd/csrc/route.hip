@@ -8,7 +8,7 @@
 //    instead (route_wave.h, experts.hip): every workgroup routes for itself, one writes the outputs.
 //  * route_fused: one 1024-thread workgroup does everything in LDS (decode), for the larger
 //    decode batches after route_topk has selected every token's experts on many CUs.
-//  * route_tokens -> route_scan -> route_scatter: many tokens (prefill chunks).
+//  * route_tokens -> route_partscan -> route_scan -> route_scatter: many tokens (prefill chunks).
 // All produce bit-identical outputs: the permutation is a counting sort whose within-expert
 // order is the pair index, computed with wave ballots, never with order-dependent atomics.
 #include "ftmoe_device.h"
@@ -195,18 +195,8 @@ __device__ void scan_experts(int E, int T, int k, int shared_slot, const int32_t
         }
     }
     // list tails and the shared expert's rows
-    const int nh = s_hoff[E], nm = s_moff[E];
-    for (int i = threadIdx.x; i < T * k; i += blockDim.x) {
-        if (i >= nh) ro.hit_pairs[i] = -1;
-        if (i >= nm) ro.miss_pairs[i] = -1;
-    }
-    if (shared_slot >= 0) {
-        for (int t = threadIdx.x; t < T; t += blockDim.x) {
-            wv.row_tok[nh + t] = t;
-            wv.row_pair[nh + t] = T * k + t;
-            wv.row_gate[nh + t] = 1.0f;
-        }
-    }
+    // the list tails and the shared expert's rows are written by route_scatter, spread over its
+    // workgroups
 }
 
 // ---------------------------------------------------------------------------------------
@@ -551,9 +541,37 @@ __global__ __launch_bounds__(256) void route_tokens(RouteArgs a) {
     for (int e = threadIdx.x; e < E; e += blockDim.x) hist[e] = s_hist[e];
 }
 
+// Per part of kBlkPerPart router blocks (grid: parts x ceil(E / 256)): each block's per-expert
+// counts become the counts of the part's earlier blocks (in place), and the part's totals go to
+// the part table after the nblk block rows.  Spreads the scan's memory rounds over many CUs: the
+// one-workgroup route_scan then only scans the part table (measured at DeepSeek-V3 prefill,
+// 8192 tokens: route_scan 35 us when it scanned all 512 block rows itself).
+__global__ __launch_bounds__(256) void route_partscan(RouteArgs a, int nblk) {
+    const int E = a.E, e = blockIdx.y * 256 + threadIdx.x;
+    if (e >= E) return;
+    const int b0 = blockIdx.x * kBlkPerPart, b1 = min(nblk, b0 + kBlkPerPart);
+    int32_t *col = a.wv.blk_hist + e;
+    int v[kBlkPerPart];
+    // clamped, unconditional loads, all in flight together
+#pragma unroll
+    for (int i = 0; i < kBlkPerPart; ++i) v[i] = col[static_cast<size_t>(min(b0 + i, b1 - 1)) * E];
+    int run = 0;
+#pragma unroll
+    for (int i = 0; i < kBlkPerPart; ++i) {
+        if (b0 + i < b1) {
+            col[static_cast<size_t>(b0 + i) * E] = run;
+            run += v[i];
+        }
+    }
+    col[(static_cast<size_t>(nblk) + blockIdx.x) * E] = run;
+}
+
 __global__ __launch_bounds__(1024) void route_scan(RouteArgs a, int nblk) {
     extern __shared__ int32_t lds[];
     const int E = a.E;
+    // the part table (route_partscan): one row of per-expert counts per part of kBlkPerPart blocks
+    const int nparts = (nblk + kBlkPerPart - 1) / kBlkPerPart;
+    int32_t *ptab = a.wv.blk_hist + static_cast<size_t>(nblk) * E;
     int32_t *s_raw = lds, *s_eff = s_raw + E, *s_tot = s_eff + E, *s_hoff = s_tot + E;
     int32_t *s_moff = s_hoff + E + 1, *s_gidx = s_moff + E + 1;
     int *s_status = s_gidx + E;
@@ -562,11 +580,11 @@ __global__ __launch_bounds__(1024) void route_scan(RouteArgs a, int nblk) {
     const int raw = threadIdx.x < E ? a.slot_table[threadIdx.x] : -1;
     if (threadIdx.x == 0) *s_status = 0;
     validate_slots(raw, E, a.n_slots, a.shared_slot, s_raw, s_cnt, s_eff, s_status);
-    // `parts` threads per expert, each over a contiguous range of the blocks
+    // `parts` threads per expert, each over a contiguous range of the part rows
     const int parts = a.scan_parts;
     const int e = threadIdx.x % E, part = threadIdx.x / E;
-    const int per = (nblk + parts - 1) / parts;
-    const int b0 = min(nblk, part * per), b1 = min(nblk, b0 + per);
+    const int per = (nparts + parts - 1) / parts;
+    const int b0 = min(nparts, part * per), b1 = min(nparts, b0 + per);
     const bool active = part < parts;
     // each thread's column range is read kScanBatch entries at a time, all in flight together
     // (one workgroup does the whole scan, so its memory latency is the scan's cost)
@@ -577,7 +595,7 @@ __global__ __launch_bounds__(1024) void route_scan(RouteArgs a, int nblk) {
             int buf[kScanBatch];
             // clamped, unconditional loads; entries past the range count 0
 #pragma unroll
-            for (int i = 0; i < kScanBatch; ++i) buf[i] = a.wv.blk_hist[static_cast<size_t>(min(b + i, b1 - 1)) * E + e];
+            for (int i = 0; i < kScanBatch; ++i) buf[i] = ptab[static_cast<size_t>(min(b + i, b1 - 1)) * E + e];
 #pragma unroll
             for (int i = 0; i < kScanBatch; ++i) sum += b + i < b1 ? buf[i] : 0;
         }
@@ -604,7 +622,7 @@ __global__ __launch_bounds__(1024) void route_scan(RouteArgs a, int nblk) {
             // two loads would make each wait cover the store too)
             int buf[kScanBatch];
 #pragma unroll
-            for (int i = 0; i < kScanBatch; ++i) buf[i] = a.wv.blk_hist[static_cast<size_t>(min(b + i, b1 - 1)) * E + e];
+            for (int i = 0; i < kScanBatch; ++i) buf[i] = ptab[static_cast<size_t>(min(b + i, b1 - 1)) * E + e];
             int off[kScanBatch];
 #pragma unroll
             for (int i = 0; i < kScanBatch; ++i) {
@@ -613,24 +631,41 @@ __global__ __launch_bounds__(1024) void route_scan(RouteArgs a, int nblk) {
             }
 #pragma unroll
             for (int i = 0; i < kScanBatch; ++i)
-                if (b + i < b1) a.wv.blk_hist[static_cast<size_t>(b + i) * E + e] = off[i];
+                if (b + i < b1) ptab[static_cast<size_t>(b + i) * E + e] = off[i];
         }
     }
 }
 
+// Block b's first list position per expert = its part's entry of the part table (the expert's
+// offset plus the counts of the earlier parts) + its own entry of the block table (the counts of
+// the part's earlier blocks).  Besides its pairs, block b writes the list tails in its pair range
+// and the shared expert's rows of its tokens.
 __global__ __launch_bounds__(64) void route_scatter(RouteArgs a) {
     __shared__ int32_t s_eff[kMaxExperts];
     __shared__ int32_t s_run[kMaxExperts];
-    const int E = a.E, k = a.k, T = a.T;
+    const int E = a.E, k = a.k, T = a.T, nblk = gridDim.x;
     const int32_t *off = a.wv.blk_hist + static_cast<size_t>(blockIdx.x) * E;
+    const int32_t *base = a.wv.blk_hist + (static_cast<size_t>(nblk) + blockIdx.x / kBlkPerPart) * E;
     for (int e = threadIdx.x; e < E; e += blockDim.x) {
         s_eff[e] = a.wv.eff_slot[e];
-        s_run[e] = off[e];
+        s_run[e] = base[e] + off[e];
     }
+    const int nh = a.ro.hit_off[E], nm = a.ro.miss_off[E];
     __syncthreads();
-    const int p0 = blockIdx.x * kTokPerBlk * k;
-    const int p1 = min(T, (blockIdx.x + 1) * kTokPerBlk) * k;
+    const int t0 = blockIdx.x * kTokPerBlk, t1 = min(T, t0 + kTokPerBlk);
+    const int p0 = t0 * k, p1 = t1 * k;
     scatter_run(p0, p1, k, a.nbits, a.ro.topk_ids, a.ro.topk_w, s_eff, s_run, a.ro, a.wv);
+    for (int i = p0 + static_cast<int>(threadIdx.x); i < p1; i += blockDim.x) {
+        if (i >= nh) a.ro.hit_pairs[i] = -1;
+        if (i >= nm) a.ro.miss_pairs[i] = -1;
+    }
+    if (a.shared_slot >= 0) {
+        for (int t = t0 + static_cast<int>(threadIdx.x); t < t1; t += blockDim.x) {
+            a.wv.row_tok[nh + t] = t;
+            a.wv.row_pair[nh + t] = T * k + t;
+            a.wv.row_gate[nh + t] = 1.0f;
+        }
+    }
 }
 
 // ---------------------------------------------------------------------------------------
@@ -672,8 +707,10 @@ static hipError_t launch_route_npl(RouteArgs a, hipStream_t s) {
         return hipGetLastError();
     }
     const int nblk = (a.T + kTokPerBlk - 1) / kTokPerBlk;
-    a.scan_parts = max(1, min(1024 / a.E, nblk));
+    const int nparts = (nblk + kBlkPerPart - 1) / kBlkPerPart;
+    a.scan_parts = max(1, min(1024 / a.E, nparts));
     hipLaunchKernelGGL(route_tokens<NPL>, dim3(nblk), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(route_partscan, dim3(nparts, (a.E + 255) / 256), dim3(256), 0, s, a, nblk);
     const int scan_lds = 4 * (6 * a.E + 3 + a.scan_parts * a.E + ncnt);
     hipLaunchKernelGGL(route_scan, dim3(1), dim3(1024), scan_lds, s, a, nblk);
     hipLaunchKernelGGL(route_scatter, dim3(nblk), dim3(64), 0, s, a);
