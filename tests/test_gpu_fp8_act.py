@@ -117,7 +117,9 @@ def test_fp8_act_zero_block_scales(T):
     check_output_aq(out, ref)
 
 
-@pytest.mark.parametrize("name,T", [("dsv3_decode", 16), ("dsv3_decode", 64)])
+# one and two tokens: the gate/up kernel routes the call itself, after the activation quantiser
+@pytest.mark.parametrize("name,T", [("dsv3_decode", 1), ("dsv3_decode", 2), ("dsv3_decode", 16),
+                                    ("dsv3_decode", 64)])
 def test_fp8_act_decode_configs_full(name, T):
     _say(f"fp8 activations {name} T={T}")
     lay = workloads.make_layer(name, T, device="cuda")
