@@ -179,7 +179,8 @@ def test_forward_configs_full(name, T):
 # workgroup routes with one wave; workgroup 0 writes the routing's outputs).  Its edges through
 # the whole layer: two and four experts per router lane, an expert count that is not a multiple
 # of 64, 64 pairs (every lane holds one), the shared expert's rows after the hit rows, every
-# weight dtype, sigmoid gating, no resident expert, and a faulty slot table.
+# weight dtype, sigmoid gating, no resident expert, and a faulty slot table.  The cases of three
+# to eight tokens check the same shapes just past that edge, where the router kernel runs first.
 @pytest.mark.parametrize("seed,E,k,T,gating,shared,wdt,n_res", [
     (40, 128, 8, 2, workloads.GATE_SOFTMAX, False, workloads.DT_BF16, None),
     (41, 200, 3, 1, workloads.GATE_SIGMOID, True, workloads.DT_FP8, None),
@@ -187,7 +188,12 @@ def test_forward_configs_full(name, T):
     (43, 256, 6, 2, workloads.GATE_SIGMOID, False, workloads.DT_F32, None),
     (44, 256, 8, 1, workloads.GATE_SOFTMAX, True, workloads.DT_BF16, 256),
     (45, 129, 4, 2, workloads.GATE_SOFTMAX, True, workloads.DT_FP8, 0),
-    (46, 192, 16, 2, workloads.GATE_SOFTMAX, False, workloads.DT_BF16, 0)])
+    (46, 192, 16, 2, workloads.GATE_SOFTMAX, False, workloads.DT_BF16, 0),
+    (48, 128, 8, 8, workloads.GATE_SOFTMAX, True, workloads.DT_BF16, None),
+    (49, 256, 8, 5, workloads.GATE_SIGMOID, False, workloads.DT_FP8, None),
+    (50, 200, 16, 4, workloads.GATE_SOFTMAX, True, workloads.DT_MXFP4, None),
+    (51, 130, 2, 7, workloads.GATE_SOFTMAX, False, workloads.DT_F32, 0),
+    (52, 256, 6, 3, workloads.GATE_SIGMOID, True, workloads.DT_BF16, 256)])
 def test_forward_self_routed(seed, E, k, T, gating, shared, wdt, n_res):
     _say(f"forward self-routed seed={seed} E={E} k={k} T={T} dtype={wdt} shared={shared} resident={n_res}")
     lay = workloads.random_layer(seed, hidden=256, inter=256, n_experts=E, top_k=k, tokens=T, gating=gating,
